@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Training-step throughput of the Flash EQ-Linear layer on one MI355X.
+
+One step = the whole hot path for one batch: weight spectrum, forward (rDFT ->
+per-bin MFMA GEMMs -> irDFT + bias), input gradient and weight gradient, all
+through the C ABI of libeqlinear.so.  Default workload: the EQ-ViT-B MLP
+up-projection, T = 8, Cin = 96 -> Cout = 384 per group element, N = 64*197 =
+12608 tokens, fp16 storage with fp32 transforms and accumulation.
+
+Inputs are seeded synthetic tensors already resident in HBM.  ``--rotate``
+input sets (default 4, about 0.8 GB for the default workload) are used in
+turn so that no step finds its operands in the 256 MB MALL or in L2.
+
+Prints one JSON line.  ``roofline`` is for the entry point with the largest
+average duration, timed live with HIP events on the stream the kernels run
+on; ``cpu_baseline`` times the fp64 oracle on the host cores on a sample of
+rows of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "fwd+bwd tokens/s + MFMA util % at T=8, 96->384 ch, fp16 (EQ-ViT-B MLP shape)"
+PROFILES = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default=None, help="layer name from synth.LAYERS")
+    ap.add_argument("--dtype", default=None, choices=["f32", "f16"])
+    ap.add_argument("--rotate", type=int, default=4, help="input sets used in turn")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-rows", type=int, default=0,
+                    help="rows of the oracle sample (0: sized to about 15 s of host work)")
+    ap.add_argument("--all", action="store_true",
+                    help="also time every other workload and dtype (one JSON line each on stderr)")
+    return ap.parse_args()
+
+
+def source_digest() -> str:
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2607_21271_amd", "csrc")
+    for f in sorted(os.listdir(csrc)):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(workload, dtype, kernel_key, digest):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(PROFILES, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    rec = data.get("%s/%s/%s" % (workload, dtype, kernel_key))
+    if not rec or rec.get("source_digest") != digest:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+class Workload:
+    def __init__(self, layer, dt, rotate):
+        import numpy as np
+        import torch
+
+        import synth
+        from paper_2607_21271_amd import ops
+        self.layer, self.dt, self.ops = layer, dt, ops
+        tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+        l = layer
+        inp = synth.draw_layer(l).rounded(dt)
+        self.inp = inp
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+        self.w = dev(inp.w)
+        self.b = dev(inp.b) if inp.b is not None else None
+        x0, dy0 = dev(inp.x), dev(inp.dy)
+        self.sets = []
+        for r in range(rotate):
+            # distinct buffers per set; contents of later sets are permuted copies
+            x = x0 if r == 0 else torch.roll(x0, r, dims=0).contiguous()
+            dy = dy0 if r == 0 else torch.roll(dy0, r, dims=0).contiguous()
+            y = torch.empty(l.N, l.Cout, l.T, dtype=tdt, device="cuda")
+            dx = torch.empty(l.N, l.Cin, l.T, dtype=tdt, device="cuda")
+            self.sets.append((x, dy, y, dx))
+        self.wspec = torch.empty(ops._lib.eqlinear_weight_spectrum_bytes(l.T, l.Cin, l.Cout,
+                                                                         ops._DT[tdt]),
+                                 dtype=torch.uint8, device="cuda")
+        self.dw = torch.empty(l.T, l.Cout, l.Cin, dtype=tdt, device="cuda")
+        self.db = torch.empty(l.Cout, dtype=tdt, device="cuda") if l.bias else None
+        nws = ops.workspace_bytes(l.N, l.T, l.Cin, l.Cout, tdt)
+        self.ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
+        self.stream = torch.cuda.current_stream()
+        self.events = []
+
+    def step(self, i, record):
+        import torch
+        l, ops = self.layer, self.ops
+        x, dy, y, dx = self.sets[i % len(self.sets)]
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
+        if record:
+            ev[0].record(self.stream)
+        ops.weight_spectrum(self.w, out=self.wspec, stream=self.stream)
+        if record:
+            ev[1].record(self.stream)
+        ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=self.stream)
+        if record:
+            ev[2].record(self.stream)
+        ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=self.stream)
+        if record:
+            ev[3].record(self.stream)
+        ops.backward_weight(x, dy, l.T, l.Cin, l.Cout, with_bias=l.bias, dw=self.dw, db=self.db,
+                            workspace=self.ws, stream=self.stream)
+        if record:
+            ev[4].record(self.stream)
+            self.events.append(ev)
+
+    def run(self, steps, warmup):
+        import torch
+        for i in range(warmup):
+            self.step(i, False)
+        torch.cuda.synchronize()
+        self.events = []
+        t0 = time.perf_counter()
+        for i in range(steps):
+            self.step(warmup + i, True)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        names = ["wspec", "fwd", "dx", "dw"]
+        per = {n: 0.0 for n in names}
+        for ev in self.events:
+            for k, n in enumerate(names):
+                per[n] += ev[k].elapsed_time(ev[k + 1]) * 1e3  # us
+        per = {n: v / steps for n, v in per.items()}
+        return (t1 - t0) / steps, per
+
+
+def cpu_baseline(layer, dt, inp, rows_req):
+    """Time the fp64 oracle (fwd + dx + dw) on the first rows of the same draw."""
+    import numpy as np
+    threads = len(os.sched_getaffinity(0))
+    os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+    import oracle
+    orc = oracle.oracle()
+    l = layer
+    macs_per_row = 3 * l.T * l.T * l.Cin * l.Cout
+    if rows_req <= 0:
+        # calibrate on a small slice, then size the sample to about 15 s
+        n0 = max(8, min(l.N, int(2e8 // macs_per_row)))
+        t0 = time.perf_counter()
+        orc.forward(inp.x[:n0], inp.w, inp.b)
+        rate = n0 / max(time.perf_counter() - t0, 1e-6) / 3.0
+        rows_req = int(rate * 15.0)
+    n = max(1, min(l.N, rows_req))
+    xs, dys = inp.x[:n], inp.dy[:n]
+    t0 = time.perf_counter()
+    orc.forward(xs, inp.w, inp.b)
+    orc.backward_input(dys, inp.w)
+    orc.backward_weight(xs, dys, with_bias=inp.b is not None)
+    t = time.perf_counter() - t0
+    return {"value": n / t, "unit": "tokens/s", "cores": int(os.environ["OMP_NUM_THREADS"]),
+            "kind": "oracle",
+            "sample": "first %d of %d rows of the same seeded %s draw, fwd + dx + dw in fp64 "
+                      "(direct circular-convolution sums), %.1f s" % (n, l.N, dt, t),
+            "seconds": t}
+
+
+def measure(layer, dt, args, digest, with_cpu):
+    import torch
+
+    from paper_2607_21271_amd import roofline as rf
+    l = layer
+    wl = Workload(l, dt, max(1, args.rotate))
+    sec, per = wl.run(args.steps, args.warmup)
+    N = l.N
+    flops = 3 * rf.pass_flops(N, l.T, l.Cin, l.Cout)
+    dense = 3 * rf.dense_equiv_flops(N, l.T, l.Cin, l.Cout)
+    nbytes = {k: rf.pass_bytes(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
+              for k in ("wspec", "fwd", "dx", "dw")}
+    dom = max(("fwd", "dx", "dw"), key=lambda k: per[k])
+    bound = "hbm" if dt == "f16" or rf.pass_bytes(dom, N, l.T, l.Cin, l.Cout, dt) / (
+        rf.PEAK_HBM_GBS * 1e9) > rf.pass_flops(N, l.T, l.Cin, l.Cout) / (
+        rf.PEAK_MFMA_TFLOPS[dt] * 1e12) else "mfma"
+    t_dom = per[dom] * 1e-6
+    if bound == "hbm":
+        achieved = nbytes[dom] / t_dom / 1e9
+        peak, unit = rf.PEAK_HBM_GBS, "GB/s"
+    else:
+        achieved = rf.pass_flops(N, l.T, l.Cin, l.Cout) / t_dom / 1e12
+        peak, unit = rf.PEAK_MFMA_TFLOPS[dt], "TFLOP/s"
+    traffic = stored_traffic(l.name, dt, dom, digest)
+    roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
+            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": {
+                "fwd": "eqlinear_forward (eql_gemm_kernel, forward)",
+                "dx": "eqlinear_backward_input (eql_gemm_kernel, input gradient)",
+                "dw": "eqlinear_backward_weight (eql_wgrad_kernel + eql_wgrad_reduce_kernel)"}[dom],
+            "algorithmic_bytes_per_launch": nbytes[dom], "avg_launch_us": round(per[dom], 2)}
+    roof_all = sum(rf.roofline_time_s(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
+                   for k in ("wspec", "fwd", "dx", "dw"))
+    rec = {
+        "metric": METRIC, "value": round(N / sec, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": dt,
+        "data": "synthetic: seeded N(0,1) activations and gradients, N(0,1/(T*Cin)) weights, "
+                "resident in HBM, %d input sets in turn" % max(1, args.rotate),
+        "config": {"workload": "%s: T=%d Cin=%d Cout=%d N=%d %s, weight spectrum + forward + "
+                               "input gradient + weight gradient%s" % (
+                                   l.name, l.T, l.Cin, l.Cout, N, dt, " (+bias)" if l.bias else ""),
+                   "T": l.T, "Cin": l.Cin, "Cout": l.Cout, "tokens": N, "bias": l.bias},
+        "mfma_util_pct": round(100 * flops / sec / (rf.PEAK_MFMA_TFLOPS[dt] * 1e12), 2),
+        "tflops_actual": round(flops / sec / 1e12, 2),
+        "tflops_dense_equiv": round(dense / sec / 1e12, 2),
+        "pass_us": {k: round(v, 2) for k, v in per.items()},
+        "pass_hbm_gbs": {k: round(nbytes[k] / (per[k] * 1e-6) / 1e9, 1) for k in per},
+        "roofline": roof,
+        "roofline_step_us": round(roof_all * 1e6, 2),
+        "roofline_step_frac": round(roof_all / sec, 4),
+        "source_digest": digest,
+        "device": torch.cuda.get_device_name(0),
+    }
+    if with_cpu:
+        rec["cpu_baseline"] = cpu_baseline(l, dt, wl.inp, args.cpu_sample_rows)
+    del wl
+    torch.cuda.empty_cache()
+    return rec
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the layer's hot path runs on a single MI355X "
+              "and no multi-GPU path is built (requested --gpus %d, WORLD_SIZE %d)" %
+              (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    digest = source_digest()
+    name = args.workload or synth.HEADLINE
+    layer = synth.LAYERS[name]
+    dt = args.dtype or layer.dtypes[0]
+    rec = measure(layer, dt, args, digest, with_cpu=not args.no_cpu_baseline)
+    if args.all:
+        for n2, l2 in synth.LAYERS.items():
+            for d2 in l2.dtypes:
+                if (n2, d2) == (name, dt):
+                    continue
+                r2 = measure(l2, d2, args, digest, with_cpu=False)
+                print(json.dumps(r2), file=sys.stderr, flush=True)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,136 @@
+/*
+ * eqlinear.h -- C ABI of the MI355X (gfx950) library for the equivariant linear
+ * layer over the cyclic group C_T, computed the Flash EQ-Linear way
+ * (arXiv 2607.21271): real DFT along the group axis, one GEMM per non-redundant
+ * frequency bin, inverse real DFT.
+ *
+ * The operation (Sec. 3.1, Eq. 1-2, read with the convolution lag direction
+ * that the convolution theorem of Eq. 3 and Alg. 1 imply):
+ *
+ *     y[n,o,t] = sum_{j=0}^{T-1} sum_{c=0}^{Cin-1} w[j,o,c] * x[n,c,(t-j) mod T] + b[o]
+ *
+ * Layouts (row-major, contiguous, group axis innermost as in Appendix A.2
+ * "Memory layout and vectorization"):
+ *     x, dx   [N, Cin, T]        y, dy   [N, Cout, T]
+ *     w, dw   [T, Cout, Cin]     (j = lag)
+ *     b, db   [Cout]
+ * A caller whose weights follow Eq. 2's printed index (s - t) reverses the lag
+ * axis: w[j] = W_paper[(T - j) mod T].
+ *
+ * Common rules for every entry point:
+ *   - dtype is EQL_F32 or EQL_F16 and applies to every tensor of the call;
+ *     FP16 tensors are IEEE binary16, every transform and accumulation is fp32,
+ *     and each output is rounded once (round-to-nearest-even).
+ *   - All pointers are device pointers owned by the caller.  The library never
+ *     allocates, frees or synchronises; work is enqueued on `stream` (a
+ *     hipStream_t passed as void*, NULL = the null stream) and the call returns
+ *     as soon as it is enqueued.
+ *   - Arguments are checked before any HIP call.  On any error nothing is
+ *     enqueued and no output is touched.  Checks: 1 <= T <= 16 (T > 16 is
+ *     EQL_ERR_UNSUPPORTED), 1 <= Cin, Cout <= 65536, 0 <= N <= 2^36, non-null
+ *     pointers (bias and dbias may be NULL; with N = 0 the row tensors may be
+ *     NULL), 16-byte aligned x, y, dy, dx, wspec and workspace and
+ *     element-aligned w, dw, bias, dbias (EQL_ERR_ALIGNMENT), no byte overlap
+ *     between any two tensors of a call (EQL_ERR_INVALID_ARG), and a large
+ *     enough workspace (EQL_ERR_WORKSPACE).  Then: no visible HIP device is
+ *     EQL_ERR_NO_DEVICE, a device other than gfx950 is EQL_ERR_UNSUPPORTED, and
+ *     a failed launch is EQL_ERR_LAUNCH.
+ *   - Outputs are overwritten, never accumulated into.
+ *   - Results are bitwise reproducible for the same inputs, shape, dtype and
+ *     device model: no atomics, fixed summation orders.
+ *   - Calls are thread-safe; concurrent calls that share no output buffer may
+ *     run on different streams.
+ */
+#ifndef EQLINEAR_H
+#define EQLINEAR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EQLINEAR_ABI_VERSION 1
+#define EQLINEAR_MAX_T 16
+
+typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
+
+typedef enum {
+  EQL_OK = 0,
+  EQL_ERR_INVALID_ARG = 1,
+  EQL_ERR_UNSUPPORTED = 2,
+  EQL_ERR_ALIGNMENT = 3,
+  EQL_ERR_WORKSPACE = 4,
+  EQL_ERR_NO_DEVICE = 5,
+  EQL_ERR_LAUNCH = 6
+} eql_status_t;
+
+/* EQLINEAR_ABI_VERSION of the built library. */
+int eqlinear_abi_version(void);
+
+/* Static, NUL-terminated description of a status code ("unknown status" for
+ * values outside eql_status_t).  Never NULL. */
+const char* eqlinear_status_string(int status);
+
+/* Bytes of the opaque weight-spectrum buffer for (T, Cin, Cout, dtype); 0 if
+ * the arguments are invalid. */
+size_t eqlinear_weight_spectrum_bytes(int T, int Cin, int Cout, int dtype);
+
+/* Weight spectrum (Alg. 1 step 1 for the shared parameters; Sec. 3.2.1 Eq. 4):
+ *     What_k[o,c] = sum_j w[j,o,c] e^{-2 pi i j k / T},   k = 0..floor(T/2),
+ * kept as T real planes (the imaginary parts of bin 0 and, for even T, of bin
+ * T/2 are zero and not stored), in the frequency-domain plane form that the
+ * paper's kernels keep their weights in (Sec. 3.5).  w is [T,Cout,Cin] in
+ * `dtype`; wspec is an opaque device buffer of
+ * eqlinear_weight_spectrum_bytes() bytes, fully overwritten (padding
+ * included).  For EQL_F16 the spectrum is computed in fp32 and rounded once to
+ * fp16.  It stays valid until w changes and serves eqlinear_forward and
+ * eqlinear_backward_input of the same (T, Cin, Cout, dtype). */
+int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cout, int dtype,
+                             void* stream);
+
+/* Forward pass (Alg. 1; Sec. 3.2.1 Eq. 4-7): rDFT of x along the group axis,
+ * one product Yhat_k = What_k Xhat_k per bin k = 0..floor(T/2) (complex bins
+ * as real block products, conjugate bins never formed), inverse rDFT, plus
+ * bias.  x [N,Cin,T] in, y [N,Cout,T] out, bias [Cout] or NULL.  N = 0 is a
+ * no-op.  x and y must not overlap (y is written directly in its final
+ * layout, never staged through x). */
+int eqlinear_forward(const void* x, const void* wspec, const void* bias, void* y, int64_t N,
+                     int T, int Cin, int Cout, int dtype, void* stream);
+
+/* Input gradient (the backward pass "in the same Fourier basis" of Appendix
+ * A.2 "Forward and backward passes"): dYhat = rDFT(dy),
+ *     dXhat_k[n,c] = sum_o dYhat_k[n,o] conj(What_k[o,c]),
+ * dx = irDFT(dXhat), i.e. dx[n,c,s] = sum_j sum_o w[j,o,c] dy[n,o,(s+j) mod T].
+ * dy [N,Cout,T] in, dx [N,Cin,T] out; wspec as produced by
+ * eqlinear_weight_spectrum.  N = 0 is a no-op. */
+int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t N, int T,
+                            int Cin, int Cout, int dtype, void* stream);
+
+/* Bytes of device workspace that eqlinear_backward_weight needs for this
+ * problem (fp32 partial sums of the row splits); 0 if the arguments are
+ * invalid or N = 0. */
+size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype);
+
+/* Weight and bias gradients with respect to the original parameters (Appendix
+ * A.2 "Forward and backward passes"; the dW and db of Sec. 4.3 Table 4):
+ *     H_k[c,o]  = sum_n conj(Xhat_k[n,c]) dYhat_k[n,o]          (fp32, split over rows)
+ *     dw[j,o,c] = (1/T) sum_{k=0}^{T-1} H_k[c,o] e^{+2 pi i j k / T}
+ *               = sum_n sum_t dy[n,o,t] x[n,c,(t-j) mod T]
+ *     db[o]     = sum_n sum_t dy[n,o,t]
+ * The row splits are summed in a fixed order by a second kernel (no atomics).
+ * x [N,Cin,T] and dy [N,Cout,T] in; dw [T,Cout,Cin] and dbias [Cout] (or NULL
+ * to skip it) out.  workspace is caller-owned device memory of at least
+ * eqlinear_backward_weight_workspace_bytes() bytes (may be NULL when that is
+ * 0); its contents on entry do not matter.  N = 0 writes zeros to dw and
+ * dbias. */
+int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
+                             size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
+                             void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EQLINEAR_H */

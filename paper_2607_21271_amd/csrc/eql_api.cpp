@@ -1,0 +1,245 @@
+// eql_api.cpp -- the C ABI declared in include/eqlinear.h: argument checks,
+// device checks, workspace planning and dispatch to the gfx950 kernels.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <mutex>
+
+#include "../../include/eqlinear.h"
+#include "eql_launch.h"
+
+namespace eqk {
+
+WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+  WgradPlan p{};
+  p.BC = p.BO = (T <= 8) ? 64 : 32;
+  p.KR = f16 ? 32 : 16;
+  p.n_ct = (Cin + p.BC - 1) / p.BC;
+  p.n_ot = (Cout + p.BO - 1) / p.BO;
+  p.Cin_pad = p.n_ct * p.BC;
+  p.Cout_pad = p.n_ot * p.BO;
+  if (N <= 0) {
+    p.S = 0;
+    p.rows_per_split = 0;
+  } else {
+    // Aim for about two workgroups per CU of a 256-CU device, without splits
+    // shorter than one row chunk.
+    const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
+    int64_t s = (512 + tiles - 1) / tiles;
+    const int64_t max_s = (N + p.KR - 1) / p.KR;
+    if (s > max_s) s = max_s;
+    if (s < 1) s = 1;
+    int64_t rows = (N + s - 1) / s;
+    rows = (rows + p.KR - 1) / p.KR * p.KR;
+    p.rows_per_split = rows;
+    p.S = (int)((N + rows - 1) / rows);
+  }
+  p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
+  p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
+  return p;
+}
+
+}  // namespace eqk
+
+namespace {
+
+constexpr int64_t kMaxN = (int64_t)1 << 36;
+constexpr int kMaxC = 65536;
+
+size_t elem_bytes(int dtype) { return dtype == EQL_F16 ? 2 : 4; }
+
+size_t align256(size_t v) { return (v + 255) / 256 * 256; }
+
+struct Range {
+  const void* p;
+  size_t bytes;
+};
+
+bool overlaps(Range a, Range b) {
+  if (!a.p || !b.p || a.bytes == 0 || b.bytes == 0) return false;
+  const uintptr_t a0 = (uintptr_t)a.p, a1 = a0 + a.bytes;
+  const uintptr_t b0 = (uintptr_t)b.p, b1 = b0 + b.bytes;
+  return a0 < b1 && b0 < a1;
+}
+
+bool any_overlap(const Range* r, int n) {
+  for (int i = 0; i < n; ++i)
+    for (int j = i + 1; j < n; ++j)
+      if (overlaps(r[i], r[j])) return true;
+  return false;
+}
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+int check_shape(int64_t N, int T, int Cin, int Cout, int dtype) {
+  if (dtype != EQL_F32 && dtype != EQL_F16) return EQL_ERR_INVALID_ARG;
+  if (T < 1 || Cin < 1 || Cout < 1 || N < 0) return EQL_ERR_INVALID_ARG;
+  if (T > EQLINEAR_MAX_T || Cin > kMaxC || Cout > kMaxC || N > kMaxN) return EQL_ERR_UNSUPPORTED;
+  return EQL_OK;
+}
+
+// Per-device cache: is this a gfx950 device?  Filled once per device.
+constexpr int kMaxDevices = 64;
+std::once_flag g_once[kMaxDevices];
+int g_arch_ok[kMaxDevices];
+
+int check_device() {
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || count <= 0) {
+    (void)hipGetLastError();
+    return EQL_ERR_NO_DEVICE;
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return EQL_ERR_NO_DEVICE;
+  }
+  std::call_once(g_once[dev], [dev] {
+    hipDeviceProp_t prop;
+    g_arch_ok[dev] = 0;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess)
+      g_arch_ok[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
+    else
+      (void)hipGetLastError();
+  });
+  return g_arch_ok[dev] ? EQL_OK : EQL_ERR_UNSUPPORTED;
+}
+
+int launched(hipError_t e) { return e == hipSuccess ? EQL_OK : EQL_ERR_LAUNCH; }
+
+}  // namespace
+
+extern "C" {
+
+int eqlinear_abi_version(void) { return EQLINEAR_ABI_VERSION; }
+
+const char* eqlinear_status_string(int status) {
+  switch (status) {
+    case EQL_OK: return "ok";
+    case EQL_ERR_INVALID_ARG: return "invalid argument (shape, null pointer, dtype or overlapping buffers)";
+    case EQL_ERR_UNSUPPORTED: return "unsupported (T > 16, size limit exceeded, or device is not gfx950)";
+    case EQL_ERR_ALIGNMENT: return "misaligned pointer (tensors need 16-byte alignment, weights element alignment)";
+    case EQL_ERR_WORKSPACE: return "workspace too small or missing";
+    case EQL_ERR_NO_DEVICE: return "no HIP device available";
+    case EQL_ERR_LAUNCH: return "kernel launch failed";
+    default: return "unknown status";
+  }
+}
+
+size_t eqlinear_weight_spectrum_bytes(int T, int Cin, int Cout, int dtype) {
+  if (check_shape(0, T, Cin, Cout, dtype) != EQL_OK) return 0;
+  const eqk::WspecDims d = eqk::wspec_dims(Cin, Cout);
+  return (size_t)T * ((size_t)d.CoF * d.CiF + (size_t)d.CinB * d.CoutB) * elem_bytes(dtype);
+}
+
+int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cout, int dtype,
+                             void* stream) {
+  int st = check_shape(0, T, Cin, Cout, dtype);
+  if (st) return st;
+  if (!w || !wspec) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if (!aligned(w, e) || !aligned(wspec, 16)) return EQL_ERR_ALIGNMENT;
+  const Range r[2] = {{w, (size_t)T * Cin * Cout * e},
+                      {wspec, eqlinear_weight_spectrum_bytes(T, Cin, Cout, dtype)}};
+  if (any_overlap(r, 2)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  hipStream_t s = (hipStream_t)stream;
+  return launched(dtype == EQL_F16 ? eqk::launch_wspec_f16(T, w, wspec, Cin, Cout, s)
+                                   : eqk::launch_wspec_f32(T, w, wspec, Cin, Cout, s));
+}
+
+static int gemm_common(const void* in, const void* wspec, const void* bias, void* out, int64_t N,
+                       int T, int Cin, int Cout, int dtype, void* stream, bool bwd) {
+  int st = check_shape(N, T, Cin, Cout, dtype);
+  if (st) return st;
+  if (!wspec) return EQL_ERR_INVALID_ARG;
+  if (N > 0 && (!in || !out)) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if (!aligned(wspec, 16) || (in && !aligned(in, 16)) || (out && !aligned(out, 16)) ||
+      (bias && !aligned(bias, e)))
+    return EQL_ERR_ALIGNMENT;
+  const int Ci = bwd ? Cout : Cin;
+  const int Co = bwd ? Cin : Cout;
+  const Range r[4] = {{in, (size_t)N * Ci * T * e},
+                      {out, (size_t)N * Co * T * e},
+                      {wspec, eqlinear_weight_spectrum_bytes(T, Cin, Cout, dtype)},
+                      {bias, bias ? (size_t)Cout * e : 0}};
+  if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  if (N == 0) return EQL_OK;
+  const eqk::WspecDims d = eqk::wspec_dims(Cin, Cout);
+  eqk::GemmArgs a{};
+  a.in = in;
+  a.bias = bias;
+  a.out = out;
+  a.N = N;
+  a.Ci = Ci;
+  a.Co = Co;
+  a.stream = (hipStream_t)stream;
+  if (!bwd) {
+    a.wsp = wspec;
+    a.Co_pad = d.CoF;
+    a.Ci_pad = d.CiF;
+  } else {
+    a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
+    a.Co_pad = d.CinB;
+    a.Ci_pad = d.CoutB;
+  }
+  return launched(dtype == EQL_F16 ? eqk::launch_gemm_f16(T, bwd, a)
+                                   : eqk::launch_gemm_f32(T, bwd, a));
+}
+
+int eqlinear_forward(const void* x, const void* wspec, const void* bias, void* y, int64_t N,
+                     int T, int Cin, int Cout, int dtype, void* stream) {
+  return gemm_common(x, wspec, bias, y, N, T, Cin, Cout, dtype, stream, false);
+}
+
+int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t N, int T,
+                            int Cin, int Cout, int dtype, void* stream) {
+  return gemm_common(dy, wspec, nullptr, dx, N, T, Cin, Cout, dtype, stream, true);
+}
+
+size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype) {
+  if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK || N == 0) return 0;
+  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  return align256(p.part_bytes) + align256(p.dbpart_bytes);
+}
+
+int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
+                             size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
+                             void* stream) {
+  int st = check_shape(N, T, Cin, Cout, dtype);
+  if (st) return st;
+  if (!dw) return EQL_ERR_INVALID_ARG;
+  if (N > 0 && (!x || !dy)) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if ((x && !aligned(x, 16)) || (dy && !aligned(dy, 16)) || !aligned(dw, e) ||
+      (dbias && !aligned(dbias, e)) || (workspace && !aligned(workspace, 16)))
+    return EQL_ERR_ALIGNMENT;
+  const size_t need = eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return EQL_ERR_WORKSPACE;
+  const Range r[5] = {{x, (size_t)N * Cin * T * e},
+                      {dy, (size_t)N * Cout * T * e},
+                      {dw, (size_t)T * Cin * Cout * e},
+                      {dbias, dbias ? (size_t)Cout * e : 0},
+                      {workspace, need}};
+  if (any_overlap(r, 5)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  eqk::WgradArgs a{};
+  a.x = x;
+  a.dy = dy;
+  a.dw = dw;
+  a.db = dbias;
+  a.part = (float*)workspace;
+  a.dbpart = workspace ? (float*)((char*)workspace + align256(p.part_bytes)) : nullptr;
+  a.N = N;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.stream = (hipStream_t)stream;
+  return launched(dtype == EQL_F16 ? eqk::launch_wgrad_f16(T, a, p)
+                                   : eqk::launch_wgrad_f32(T, a, p));
+}
+
+}  // extern "C"

@@ -1,0 +1,364 @@
+// eql_common.h -- device building blocks shared by the gfx950 kernels of the
+// C_T equivariant linear layer (Flash EQ-Linear, arXiv 2607.21271).
+//
+//  * compile-time twiddles cos/sin(2*pi*m/T), evaluated in double and rounded
+//    once to float, so no device sin/cos is ever called;
+//  * the real DFT along the group axis, keeping the non-redundant bins
+//    k = 0..floor(T/2) (Alg. 1 step 1, Sec. 3.2.1 Eq. 4), and its inverse with
+//    conjugate pairs folded into weights 2 (Alg. 1 steps 3-4, Eq. 6-7 and the
+//    conjugate-pair form of Appendix A.1);
+//  * MFMA fragment helpers for v_mfma_f32_16x16x32_f16 and
+//    v_mfma_f32_16x16x4_f32.
+//
+// Spectral planes.  A length-T real signal is held as exactly T reals:
+//   plane 0            Re X_0                       (bin 0 is real)
+//   plane 1            X_{T/2}        (even T only; the Nyquist bin is real)
+//   plane R+2(k-1)     Re X_k,  k = 1..K
+//   plane R+2(k-1)+1   Im X_k
+// with R = 1 + [T even] real bins and K = floor((T-1)/2) complex bins, so that
+// R + 2K = T.  The forward transform is unnormalised, X_k = sum_t x_t e^{-2 pi i k t/T};
+// the inverse carries the 1/T.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+namespace eqk {
+
+// ---------------------------------------------------------------------------
+// Compile-time twiddles.
+constexpr double kPi = 3.14159265358979323846264338327950288;
+
+constexpr double cos_series(double x) {  // |x| <= pi; Taylor series, 40 terms
+  double term = 1.0, sum = 1.0;
+  const double x2 = x * x;
+  for (int i = 1; i < 40; ++i) {
+    term *= -x2 / ((2.0 * i - 1.0) * (2.0 * i));
+    sum += term;
+  }
+  return sum;
+}
+
+// cos(2*pi*m/T) with exact values at the quarter points.
+constexpr double cos2pi(long m, long T) {
+  m %= T;
+  if (m < 0) m += T;
+  if (m == 0) return 1.0;
+  if (2 * m == T) return -1.0;
+  if (4 * m == T || 4 * m == 3 * T) return 0.0;
+  double x = 2.0 * kPi * (double)m / (double)T;
+  if (x > kPi) x -= 2.0 * kPi;
+  return cos_series(x);
+}
+
+// sin(2*pi*m/T) = cos(2*pi*(4m - T)/(4T)).
+constexpr double sin2pi(long m, long T) { return cos2pi(4 * m - T, 4 * T); }
+
+template <int T>
+struct Bins {
+  static constexpr int R = 1 + (T % 2 == 0 ? 1 : 0);  // real bins
+  static constexpr int K = (T - 1) / 2;               // complex bins
+  static constexpr int S = (T - 1) / 2;               // symmetric pairs (s, T-s)
+  static constexpr bool kEven = (T % 2 == 0);
+  static constexpr int re(int k) { return R + 2 * (k - 1); }
+  static constexpr int im(int k) { return R + 2 * (k - 1) + 1; }
+};
+
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+// f(integral_constant<int, i>) for i = 0..N-1, fully unrolled at compile time.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// acc += C * v for a compile-time constant C; terms with C = 0 vanish and
+// C = +-1 become an add or a subtract.
+template <float C>
+__device__ __forceinline__ void axpy_c(float& acc, float v) {
+  if constexpr (C == 1.0f) {
+    acc += v;
+  } else if constexpr (C == -1.0f) {
+    acc -= v;
+  } else if constexpr (C != 0.0f) {
+    acc = __builtin_fmaf(C, v, acc);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Real DFT of v[0..T-1] into T spectral planes (layout above).  Input pairs
+// (s, T-s) are folded into e_s = v_s + v_{T-s} and d_s = v_s - v_{T-s} so
+// that each bin takes about T/2 multiply-adds:
+//   Re X_k = v_0 + (-1)^k v_{T/2} + sum_s e_s cos(2 pi k s/T)
+//   Im X_k = -sum_s d_s sin(2 pi k s/T)
+template <int T>
+__device__ __forceinline__ void rdft(const float (&v)[T], float (&P)[T]) {
+  using B = Bins<T>;
+  constexpr int S = B::S;
+  float e[S + 1], d[S + 1];
+  static_for<S>([&](auto si) {
+    constexpr int s = decltype(si)::value + 1;
+    e[s] = v[s] + v[T - s];
+    d[s] = v[s] - v[T - s];
+  });
+  float a = v[0];
+  static_for<S>([&](auto si) { a += e[decltype(si)::value + 1]; });
+  if constexpr (B::kEven) a += v[T / 2];
+  P[0] = a;
+  if constexpr (B::kEven) {
+    float b = v[0];
+    static_for<S>([&](auto si) {
+      constexpr int s = decltype(si)::value + 1;
+      if constexpr (s & 1) b -= e[s]; else b += e[s];
+    });
+    if constexpr ((T / 2) & 1) b -= v[T / 2]; else b += v[T / 2];
+    P[1] = b;
+  }
+  static_for<B::K>([&](auto ki) {
+    constexpr int k = decltype(ki)::value + 1;
+    float re = v[0];
+    float im = 0.0f;
+    static_for<S>([&](auto si) {
+      constexpr int s = decltype(si)::value + 1;
+      axpy_c<(float)cos2pi((long)k * s, T)>(re, e[s]);
+      axpy_c<(float)-sin2pi((long)k * s, T)>(im, d[s]);
+    });
+    if constexpr (B::kEven) {
+      if constexpr (k & 1) re -= v[T / 2]; else re += v[T / 2];
+    }
+    P[B::re(k)] = re;
+    P[B::im(k)] = im;
+  });
+}
+
+// Inverse real DFT of T spectral planes, u_t = (1/T) sum_{k=0}^{T-1} X_k e^{2 pi i k t/T},
+// with the conjugate bins folded in:
+//   u_t = (X_0 + (-1)^t X_{T/2})/T + (2/T) sum_{k=1}^{K} (Re X_k cos(2 pi k t/T) - Im X_k sin(2 pi k t/T)).
+// Output pairs (t, T-t) share the even part E_t and differ in the sign of the odd part O_t.
+template <int T>
+__device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
+  using B = Bins<T>;
+  constexpr int S = B::S;
+  constexpr float inv = (float)(1.0 / T);
+  float A = P[0] * inv;
+  float Bn = 0.0f;
+  if constexpr (B::kEven) Bn = P[1] * inv;
+  const float base_e = A + Bn;  // (-1)^t = +1
+  const float base_o = A - Bn;  // (-1)^t = -1
+  static_for<S>([&](auto ti) {
+    constexpr int t = decltype(ti)::value + 1;
+    float E = 0.0f, O = 0.0f;
+    static_for<B::K>([&](auto ki) {
+      constexpr int k = decltype(ki)::value + 1;
+      axpy_c<(float)(2.0 * cos2pi((long)k * t, T) / T)>(E, P[B::re(k)]);
+      axpy_c<(float)(2.0 * sin2pi((long)k * t, T) / T)>(O, P[B::im(k)]);
+    });
+    const float base = (t & 1) ? base_o : base_e;
+    u[t] = base + (E - O);
+    u[T - t] = base + (E + O);
+  });
+  float u0 = base_e;
+  static_for<B::K>([&](auto ki) {
+    constexpr int k = decltype(ki)::value + 1;
+    axpy_c<(float)(2.0 / T)>(u0, P[B::re(k)]);
+  });
+  u[0] = u0;
+  if constexpr (B::kEven) {
+    float uh = ((T / 2) & 1) ? base_o : base_e;
+    static_for<B::K>([&](auto ki) {
+      constexpr int k = decltype(ki)::value + 1;
+      axpy_c<(float)((k & 1 ? -2.0 : 2.0) / T)>(uh, P[B::re(k)]);
+    });
+    u[T / 2] = uh;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Element types.  F16 tensors hold IEEE binary16; arithmetic is fp32.
+template <bool F16>
+struct Elem;
+template <>
+struct Elem<true> {
+  using T = _Float16;
+  static constexpr int bytes = 2;
+};
+template <>
+struct Elem<false> {
+  using T = float;
+  static constexpr int bytes = 4;
+};
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// One MFMA operand fragment is 16 bytes per lane: 8 fp16 values (one
+// v_mfma_f32_16x16x32_f16 K-slice of 32) or 4 fp32 values (four
+// v_mfma_f32_16x16x4_f32 K-slices of 4).  Lane l = 16*g + i holds row/column i
+// and the g-th 16-byte group of the contraction index; A and B use the same
+// group-to-index map, so the contraction covers each index exactly once.
+template <bool F16>
+struct Mma;
+
+template <>
+struct Mma<true> {
+  static constexpr int kPerFrag = 8;  // contraction elements per lane fragment
+  static constexpr int kPerTile = 32; // contraction elements per 4 lane groups
+  static __device__ __forceinline__ void run(floatx4& acc, u32x4 a, u32x4 b) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
+                                                 __builtin_bit_cast(half8, b), acc, 0, 0, 0);
+  }
+  static __device__ __forceinline__ u32x4 neg(u32x4 a) { return a ^ 0x80008000u; }
+};
+
+template <>
+struct Mma<false> {
+  static constexpr int kPerFrag = 4;
+  static constexpr int kPerTile = 16;
+  static __device__ __forceinline__ void run(floatx4& acc, u32x4 a, u32x4 b) {
+    const floatx4 af = __builtin_bit_cast(floatx4, a);
+    const floatx4 bf = __builtin_bit_cast(floatx4, b);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[0], bf[0], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[1], bf[1], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[2], bf[2], acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[3], bf[3], acc, 0, 0, 0);
+  }
+  static __device__ __forceinline__ u32x4 neg(u32x4 a) { return a ^ 0x80000000u; }
+};
+
+// LDS tiles are rows of 64 bytes (four 16-byte chunks); chunk c of row r is
+// stored at chunk c ^ ((r >> 1) & 3), which spreads the 16 rows read by one
+// fragment load over all banks.
+__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
+__device__ __forceinline__ int lds_off(int row, int byte_in_row) {
+  return row * 64 + (swz(row, byte_in_row >> 4) << 4) + (byte_in_row & 15);
+}
+
+// ---------------------------------------------------------------------------
+// Contiguous loads / stores of L elements at an element offset.  VEC is the
+// widest power-of-two byte width (<= 16) that divides L * elem bytes; the
+// caller states whether the start is VEC-aligned.  Loads convert to float.
+template <bool F16, int L>
+__device__ __forceinline__ void load_run(const void* base, int64_t elem_off, bool vec_ok,
+                                         float (&out)[L]) {
+  using E = typename Elem<F16>::T;
+  constexpr int NB = L * Elem<F16>::bytes;
+  constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
+  const E* p = reinterpret_cast<const E*>(base) + elem_off;
+  if (vec_ok && VEC >= 4) {
+    constexpr int PER = VEC / Elem<F16>::bytes;
+#pragma unroll
+    for (int v = 0; v < L / PER; ++v) {
+      if constexpr (VEC == 16) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(p + v * PER);
+        E tmp[PER];
+        __builtin_memcpy(tmp, &w, 16);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
+      } else if constexpr (VEC == 8) {
+        const u32x2 w = *reinterpret_cast<const u32x2*>(p + v * PER);
+        E tmp[PER];
+        __builtin_memcpy(tmp, &w, 8);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
+      } else {
+        const uint32_t w = *reinterpret_cast<const uint32_t*>(p + v * PER);
+        E tmp[PER];
+        __builtin_memcpy(tmp, &w, 4);
+#pragma unroll
+        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < L; ++q) out[q] = (float)p[q];
+  }
+}
+
+// Same as load_run, but only the first n_valid elements are read; the rest are zero.
+template <bool F16, int L>
+__device__ __forceinline__ void load_run_masked(const void* base, int64_t elem_off, int n_valid,
+                                                float (&out)[L]) {
+  using E = typename Elem<F16>::T;
+  const E* p = reinterpret_cast<const E*>(base) + elem_off;
+#pragma unroll
+  for (int q = 0; q < L; ++q) out[q] = (q < n_valid) ? (float)p[q] : 0.0f;
+}
+
+template <bool F16, int L>
+__device__ __forceinline__ void store_run(void* base, int64_t elem_off, bool vec_ok, int n_valid,
+                                          const float (&v)[L]) {
+  using E = typename Elem<F16>::T;
+  constexpr int NB = L * Elem<F16>::bytes;
+  constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
+  E* p = reinterpret_cast<E*>(base) + elem_off;
+  if (vec_ok && n_valid >= L && VEC >= 4) {
+    constexpr int PER = VEC / Elem<F16>::bytes;
+#pragma unroll
+    for (int s = 0; s < L / PER; ++s) {
+      E tmp[PER];
+#pragma unroll
+      for (int q = 0; q < PER; ++q) tmp[q] = (E)v[s * PER + q];
+      if constexpr (VEC == 16) {
+        u32x4 w;
+        __builtin_memcpy(&w, tmp, 16);
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p + s * PER));
+      } else if constexpr (VEC == 8) {
+        u32x2 w;
+        __builtin_memcpy(&w, tmp, 8);
+        __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(p + s * PER));
+      } else {
+        uint32_t w;
+        __builtin_memcpy(&w, tmp, 4);
+        __builtin_nontemporal_store(w, reinterpret_cast<uint32_t*>(p + s * PER));
+      }
+    }
+  } else {
+#pragma unroll
+    for (int q = 0; q < L; ++q)
+      if (q < n_valid) p[q] = (E)v[q];
+  }
+}
+
+// Pack PC consecutive float values into PC elements of type E in a byte buffer.
+template <bool F16, int PC>
+__device__ __forceinline__ void pack_store_lds(char* lds, int off, const float (&v)[PC]) {
+  using E = typename Elem<F16>::T;
+  constexpr int NB = PC * Elem<F16>::bytes;
+  E tmp[PC];
+#pragma unroll
+  for (int q = 0; q < PC; ++q) tmp[q] = (E)v[q];
+  if constexpr (NB == 16) {
+    u32x4 w;
+    __builtin_memcpy(&w, tmp, 16);
+    *reinterpret_cast<u32x4*>(lds + off) = w;
+  } else if constexpr (NB == 8) {
+    u32x2 w;
+    __builtin_memcpy(&w, tmp, 8);
+    *reinterpret_cast<u32x2*>(lds + off) = w;
+  } else if constexpr (NB == 4) {
+    uint32_t w;
+    __builtin_memcpy(&w, tmp, 4);
+    *reinterpret_cast<uint32_t*>(lds + off) = w;
+  } else {
+    __builtin_memcpy(lds + off, tmp, NB);
+  }
+}
+
+// Workgroup-id remap for the 8 XCDs of MI355X: the hardware deals consecutive
+// workgroup ids round-robin to XCDs, so id b runs on XCD b % 8.  Returning
+// tile = (b % 8) * per + b / 8 gives every XCD a contiguous range of tiles,
+// which keeps tiles that share operand rows in one L2.  `grid` must be a
+// multiple of 8; ids past `n_tiles` return -1.
+__device__ __forceinline__ int xcd_tile(int b, int grid, int n_tiles) {
+  const int per = grid >> 3;
+  const int t = (b & 7) * per + (b >> 3);
+  return t < n_tiles ? t : -1;
+}
+
+}  // namespace eqk

@@ -1,0 +1,57 @@
+"""Helpers shared by the GPU tests: run the HIP path on seeded inputs and compare
+with the fp64 oracle on the same dtype-rounded values."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import synth
+
+TOL = {"f32": 1e-5, "f16": 5e-3}   # max|gpu - ref| / max|ref|, per output tensor
+
+
+def torch_dtype(dt):
+    import torch
+    return {"f32": torch.float32, "f16": torch.float16}[dt]
+
+
+def rel_err(gpu, ref):
+    gpu = np.asarray(gpu, np.float64)
+    ref = np.asarray(ref, np.float64)
+    assert gpu.shape == ref.shape, (gpu.shape, ref.shape)
+    scale = np.max(np.abs(ref)) if ref.size else 0.0
+    if ref.size == 0:
+        return 0.0
+    if scale == 0.0:
+        return float(np.max(np.abs(gpu)))
+    return float(np.max(np.abs(gpu - ref)) / scale)
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(a, dt):
+    import torch
+    return torch.from_numpy(np.ascontiguousarray(a.astype(synth.DTYPES[dt]))).to("cuda")
+
+
+def run_gpu(inp: synth.Inputs, dt: str, want=("y", "dx", "dw")):
+    """Run weight spectrum, forward, backward_input, backward_weight on the GPU."""
+    import torch
+    from paper_2607_21271_amd import ops
+    T, Cout, Cin = inp.w.shape
+    x, w, dy = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.dy, dt)
+    b = to_dev(inp.b, dt) if inp.b is not None else None
+    wspec = ops.weight_spectrum(w)
+    out = {}
+    if "y" in want:
+        out["y"] = ops.forward(x, wspec, b, T, Cin, Cout)
+    if "dx" in want:
+        out["dx"] = ops.backward_input(dy, wspec, T, Cin, Cout)
+    if "dw" in want:
+        out["dw"], out["db"] = ops.backward_weight(x, dy, T, Cin, Cout, with_bias=b is not None)
+    torch.cuda.synchronize()
+    return {k: (v.float().cpu().numpy() if v is not None else None) for k, v in out.items()}

@@ -1,0 +1,139 @@
+"""C-ABI checks that need no GPU: the library loads, exports what include/eqlinear.h
+declares, and rejects bad arguments before touching the device (CPU only)."""
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "eqlinear.h")
+
+L = pytest.importorskip("paper_2607_21271_amd._lib")
+
+
+def _header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(eqlinear_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        pytest.fail("libeqlinear.so is not built; run __graft_entry__.build()")
+    return L.lib()
+
+
+def _gpu_visible():
+    try:
+        import torch
+        return torch.cuda.device_count() > 0
+    except Exception:
+        return False
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _header_functions()
+    assert len(names) == 8, names
+    for n in names:
+        assert hasattr(lib, n), n
+        assert n in L.SIGNATURES, n
+
+
+def test_abi_version_matches_header(lib):
+    m = re.search(r"#define EQLINEAR_ABI_VERSION (\d+)", open(HEADER).read())
+    assert L.eqlinear_abi_version() == int(m.group(1))
+
+
+def test_status_strings(lib):
+    seen = set()
+    for s in range(7):
+        t = L.eqlinear_status_string(s)
+        assert t and t != "unknown status"
+        seen.add(t)
+    assert len(seen) == 7
+    assert L.eqlinear_status_string(99) == "unknown status"
+    assert L.eqlinear_status_string(-1) == "unknown status"
+
+
+def test_weight_spectrum_bytes(lib):
+    # T real planes, two padded layouts (rows to 128, columns to 32)
+    assert L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_F16) == 8 * (384 * 96 + 128 * 384) * 2
+    assert L.eqlinear_weight_spectrum_bytes(4, 16, 16, L.EQL_F32) == 4 * (128 * 32 * 2) * 4
+    for bad in [(0, 4, 4, 0), (17, 4, 4, 0), (4, 0, 4, 0), (4, 4, 0, 0), (4, 4, 4, 2),
+                (4, 65537, 4, 0)]:
+        assert L.eqlinear_weight_spectrum_bytes(*bad) == 0, bad
+
+
+def test_workspace_bytes(lib):
+    assert L.eqlinear_backward_weight_workspace_bytes(0, 8, 96, 384, L.EQL_F16) == 0
+    a = L.eqlinear_backward_weight_workspace_bytes(12608, 8, 96, 384, L.EQL_F16)
+    assert a > 0 and a % 256 == 0
+    assert L.eqlinear_backward_weight_workspace_bytes(-1, 8, 96, 384, L.EQL_F16) == 0
+    assert L.eqlinear_backward_weight_workspace_bytes(10, 17, 4, 4, L.EQL_F16) == 0
+
+
+A = 0x10000000  # fake, 16-byte aligned device addresses: never dereferenced on these paths
+MB = 1 << 20
+
+
+def test_forward_argument_checks(lib):
+    f = L.eqlinear_forward
+    ok = (A, A + 8 * MB, None, A + 16 * MB, 100, 4, 8, 8, L.EQL_F32, None)
+    def call(**kw):
+        args = list(ok)
+        names = ["x", "wspec", "bias", "y", "N", "T", "Cin", "Cout", "dtype", "stream"]
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return f(*args)
+    assert call(T=0) == L.EQL_ERR_INVALID_ARG
+    assert call(T=17) == L.EQL_ERR_UNSUPPORTED
+    assert call(Cin=0) == L.EQL_ERR_INVALID_ARG
+    assert call(Cout=-3) == L.EQL_ERR_INVALID_ARG
+    assert call(Cout=70000) == L.EQL_ERR_UNSUPPORTED
+    assert call(N=-1) == L.EQL_ERR_INVALID_ARG
+    assert call(N=1 << 40) == L.EQL_ERR_UNSUPPORTED
+    assert call(dtype=7) == L.EQL_ERR_INVALID_ARG
+    assert call(x=None) == L.EQL_ERR_INVALID_ARG
+    assert call(y=None) == L.EQL_ERR_INVALID_ARG
+    assert call(wspec=None) == L.EQL_ERR_INVALID_ARG
+    assert call(x=A + 4) == L.EQL_ERR_ALIGNMENT
+    assert call(y=A + 16 * MB + 8) == L.EQL_ERR_ALIGNMENT
+    assert call(wspec=A + 8 * MB + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(bias=A + 24 * MB + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(y=A + 16) == L.EQL_ERR_INVALID_ARG           # y overlaps x
+    assert call(bias=A + 32) == L.EQL_ERR_INVALID_ARG        # bias inside x
+    assert call(wspec=A + 16 * MB) == L.EQL_ERR_INVALID_ARG  # wspec overlaps y
+
+
+def test_backward_argument_checks(lib):
+    g = L.eqlinear_backward_input
+    assert g(A, A + 8 * MB, A + 16 * MB, 10, 0, 4, 4, 0, None) == L.EQL_ERR_INVALID_ARG
+    assert g(A, A + 8 * MB, A, 10, 4, 4, 4, 0, None) == L.EQL_ERR_INVALID_ARG
+    assert g(A + 8, A + 8 * MB, A + 16 * MB, 10, 4, 4, 4, 0, None) == L.EQL_ERR_ALIGNMENT
+    h = L.eqlinear_backward_weight
+    need = L.eqlinear_backward_weight_workspace_bytes(1000, 8, 16, 16, L.EQL_F32)
+    base = [A, A + 8 * MB, A + 16 * MB, A + 17 * MB, A + 24 * MB, need, 1000, 8, 16, 16, L.EQL_F32, None]
+    def call(i, v):
+        args = list(base)
+        args[i] = v
+        return h(*args)
+    assert call(5, need - 1) == L.EQL_ERR_WORKSPACE
+    assert call(4, None) == L.EQL_ERR_WORKSPACE
+    assert call(2, None) == L.EQL_ERR_INVALID_ARG
+    assert call(0, None) == L.EQL_ERR_INVALID_ARG
+    assert call(2, A + 8 * MB + 4) == L.EQL_ERR_INVALID_ARG   # dw overlaps dy
+    assert call(3, A + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(4, A + 24 * MB + 4) == L.EQL_ERR_ALIGNMENT
+    assert call(7, 17) == L.EQL_ERR_UNSUPPORTED
+    w = L.eqlinear_weight_spectrum
+    assert w(None, A, 4, 4, 4, 0, None) == L.EQL_ERR_INVALID_ARG
+    assert w(A + 2, A + MB, 4, 4, 4, 0, None) == L.EQL_ERR_ALIGNMENT
+    assert w(A, A + 64, 4, 4, 4, 0, None) == L.EQL_ERR_INVALID_ARG   # wspec overlaps w
+
+
+@pytest.mark.skipif(_gpu_visible(), reason="would launch on fake addresses when a GPU is present")
+def test_valid_arguments_without_device_report_no_device(lib):
+    assert L.eqlinear_forward(A, A + 8 * MB, None, A + 16 * MB, 100, 4, 8, 8, 0, None) == \
+        L.EQL_ERR_NO_DEVICE
+    assert L.eqlinear_weight_spectrum(A, A + MB, 4, 8, 8, 1, None) == L.EQL_ERR_NO_DEVICE

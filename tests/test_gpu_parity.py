@@ -1,0 +1,214 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar (per output tensor): max|gpu - oracle| / max|oracle| <= 1e-5 for fp32 and
+<= 5e-3 for fp16, with the oracle fed the same dtype-rounded inputs.
+"""
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import TOL, rel_err, run_gpu, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+# Reduced row counts: several row tiles plus a ragged tail, oracle in seconds.
+REDUCED_N = {"tiny_c4": 256, "vit_s_proj": 1037, "vit_b_mlp_up": 517, "vit_b_mlp_down": 517,
+             "swin_s1": 2085, "sweep_T3": 1029, "sweep_T5": 1029, "sweep_T12": 1029,
+             "sweep_T16": 1029}
+CASES = [(name, dt) for name, l in synth.LAYERS.items() for dt in l.dtypes]
+
+
+def _check_all(inp, dt, orc, tag):
+    g = run_gpu(inp, dt)
+    y = orc.forward(inp.x, inp.w, inp.b)
+    dx = orc.backward_input(inp.dy, inp.w)
+    dw, db = orc.backward_weight(inp.x, inp.dy, with_bias=inp.b is not None)
+    errs = {"y": rel_err(g["y"], y), "dx": rel_err(g["dx"], dx), "dw": rel_err(g["dw"], dw)}
+    if db is not None:
+        errs["db"] = rel_err(g["db"], db)
+    say(tag, dt, {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (tag, dt, k, v)
+    return g
+
+
+@pytest.mark.parametrize("name,dt", CASES, ids=["%s-%s" % c for c in CASES])
+def test_layer_reduced_rows(orc, name, dt):
+    l = synth.LAYERS[name]
+    say("case", name, dt, "N =", REDUCED_N[name])
+    inp = synth.draw(l.T, l.Cin, l.Cout, REDUCED_N[name], l.bias, l.seed).rounded(dt)
+    _check_all(inp, dt, orc, name)
+
+
+@pytest.mark.parametrize("name,dt", CASES, ids=["%s-%s" % c for c in CASES])
+def test_layer_full_size_sampled(orc, name, dt):
+    """Full workload size, the benchmark's launch configuration; the oracle checks
+    sampled rows of y and dx, sampled entries of dw, and all of db."""
+    l = synth.LAYERS[name]
+    say("case full", name, dt, "N =", l.N)
+    inp = synth.draw_layer(l).rounded(dt)
+    g = run_gpu(inp, dt)
+    rs = np.random.RandomState(7)
+    rows = np.unique(np.concatenate([rs.randint(0, l.N, 24), [0, l.N - 1]]))
+    y = orc.forward(inp.x[rows], inp.w, inp.b)
+    dx = orc.backward_input(inp.dy[rows], inp.w)
+    j = rs.randint(0, l.T, 48)
+    o = rs.randint(0, l.Cout, 48)
+    c = rs.randint(0, l.Cin, 48)
+    dw = orc.backward_weight_entries(inp.x, inp.dy, j, o, c)
+    errs = {"y": rel_err(g["y"][rows], y), "dx": rel_err(g["dx"][rows], dx),
+            "dw": rel_err(g["dw"][j, o, c], dw)}
+    if inp.b is not None:
+        errs["db"] = rel_err(g["db"], inp.dy.astype(np.float64).sum(axis=(0, 2)))
+    say(name, dt, {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (name, dt, k, v)
+
+
+EDGE = []
+for T in range(1, 17):
+    EDGE.append((T, 5, 7, 37, True))
+    EDGE.append((T, 33, 19, 70, False))
+EDGE += [(3, 3, 5, 11, True), (5, 1, 1, 1, True), (7, 2, 9, 16, True), (4, 24, 96, 17, False),
+         (8, 96, 384, 1, False), (8, 384, 96, 33, False), (16, 64, 64, 65, True),
+         (12, 64, 1, 63, True), (2, 129, 130, 31, True), (6, 40, 200, 50, True)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", EDGE,
+                         ids=["T%d-%dx%d-N%d%s" % (e[0], e[1], e[2], e[3], "-b" if e[4] else "")
+                              for e in EDGE])
+def test_edge_shapes(orc, T, Cin, Cout, N, bias, dt):
+    say("edge", T, Cin, Cout, N, bias, dt)
+    inp = synth.draw(T, Cin, Cout, N, bias, 9000 + 97 * T + Cin + 7 * Cout + N).rounded(dt)
+    _check_all(inp, dt, orc, "edge T%d %dx%d N%d" % (T, Cin, Cout, N))
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_zero_rows(dt):
+    from paper_2607_21271_amd import ops
+    T, Cin, Cout = 8, 16, 24
+    w = to_dev(np.random.RandomState(1).standard_normal((T, Cout, Cin)), dt)
+    b = to_dev(np.ones(Cout), dt)
+    wspec = ops.weight_spectrum(w)
+    x = torch.empty(0, Cin, T, dtype=w.dtype, device="cuda")
+    y = ops.forward(x, wspec, b, T, Cin, Cout)
+    dx = ops.backward_input(torch.empty(0, Cout, T, dtype=w.dtype, device="cuda"), wspec, T, Cin, Cout)
+    dw = torch.full((T, Cout, Cin), 7.0, dtype=w.dtype, device="cuda")
+    db = torch.full((Cout,), 7.0, dtype=w.dtype, device="cuda")
+    ops.backward_weight(x, torch.empty(0, Cout, T, dtype=w.dtype, device="cuda"), T, Cin, Cout,
+                        True, dw=dw, db=db)
+    torch.cuda.synchronize()
+    assert y.shape == (0, Cout, T) and dx.shape == (0, Cin, T)
+    assert torch.all(dw == 0) and torch.all(db == 0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_bitwise_determinism(dt):
+    l = synth.LAYERS["vit_b_mlp_up"] if dt == "f16" else synth.LAYERS["vit_s_proj"]
+    inp = synth.draw_layer(l.with_n(3001)).rounded(dt)
+    a = run_gpu(inp, dt)
+    b = run_gpu(inp, dt)
+    for k in a:
+        if a[k] is not None:
+            assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_guard_bands_untouched(dt):
+    """Outputs written into views of larger sentinel-filled buffers leave the slack alone."""
+    from paper_2607_21271_amd import ops
+    T, Cin, Cout, N = 5, 24, 40, 77
+    inp = synth.draw(T, Cin, Cout, N, True, 77).rounded(dt)
+    x, w, dy, b = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.dy, dt), to_dev(inp.b, dt)
+    wspec = ops.weight_spectrum(w)
+    SENT, PAD = 12345.0, 64   # PAD elements keep 16-byte alignment of the view
+
+    def guarded(n):
+        buf = torch.full((PAD + n + PAD,), SENT, dtype=w.dtype, device="cuda")
+        return buf, buf[PAD:PAD + n]
+
+    yb, yv = guarded(N * Cout * T)
+    dxb, dxv = guarded(N * Cin * T)
+    dwb, dwv = guarded(T * Cout * Cin)
+    dbb, dbv = guarded(Cout)
+    ops.forward(x, wspec, b, T, Cin, Cout, out=yv.view(N, Cout, T))
+    ops.backward_input(dy, wspec, T, Cin, Cout, out=dxv.view(N, Cin, T))
+    ops.backward_weight(x, dy, T, Cin, Cout, True, dw=dwv.view(T, Cout, Cin), db=dbv)
+    torch.cuda.synchronize()
+    for buf in (yb, dxb, dwb, dbb):
+        assert torch.all(buf[:PAD] == SENT) and torch.all(buf[-PAD:] == SENT)
+        assert not torch.any(buf[PAD:-PAD] == SENT)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_roll_equivariance_gpu(dt):
+    """f(G x) = G f(x): rolling x along the group axis rolls y (Table 5's test)."""
+    from paper_2607_21271_amd import ops
+    for T in (4, 8, 5):
+        inp = synth.draw(T, 32, 48, 300, True, 31 + T).rounded(dt)
+        x, w, b = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.b, dt)
+        wspec = ops.weight_spectrum(w)
+        y = ops.forward(x, wspec, b, T, 32, 48).double()
+        for r in range(1, T):
+            yr = ops.forward(torch.roll(x, r, dims=2).contiguous(), wspec, b, T, 32, 48).double()
+            err = (yr - torch.roll(y, r, dims=2)).abs().max().item() / y.abs().max().item()
+            assert err <= TOL[dt], (T, r, err)
+
+
+def test_nan_propagates():
+    from paper_2607_21271_amd import ops
+    T, Cin, Cout, N = 4, 8, 8, 40
+    inp = synth.draw(T, Cin, Cout, N, True, 5).rounded("f32")
+    x, w, b = to_dev(inp.x, "f32"), to_dev(inp.w, "f32"), to_dev(inp.b, "f32")
+    x[3, 2, 1] = float("nan")
+    y = ops.forward(x, ops.weight_spectrum(w), b, T, Cin, Cout)
+    torch.cuda.synchronize()
+    assert torch.isnan(y[3]).all()
+    assert torch.isfinite(y[:3]).all() and torch.isfinite(y[4:]).all()
+
+
+def test_error_paths_with_device_pointers():
+    from paper_2607_21271_amd import _lib, ops
+    T, Cin, Cout, N = 4, 8, 8, 16
+    w = torch.randn(T, Cout, Cin, device="cuda")
+    wspec = ops.weight_spectrum(w)
+    buf = torch.randn(N * Cin * T + 1, device="cuda")
+    x_mis = buf[1:].view(N, Cin, T)             # 4-byte offset: misaligned
+    with pytest.raises(_lib.EqlError) as e:
+        ops.forward(x_mis, wspec, None, T, Cin, Cout)
+    assert e.value.status == _lib.EQL_ERR_ALIGNMENT
+    x = torch.randn(N, Cin, T, device="cuda")
+    with pytest.raises(_lib.EqlError) as e:        # y aliases x
+        ops.forward(x, wspec, None, T, Cin, Cout, out=x)
+    assert e.value.status == _lib.EQL_ERR_INVALID_ARG
+
+
+def test_autograd_module_matches_oracle(orc):
+    from paper_2607_21271_amd.ops import EQLinear
+    T, Cin, Cout, N = 8, 24, 40, 130
+    inp = synth.draw(T, Cin, Cout, N, True, 4242).rounded("f32")
+    m = EQLinear(T, Cin, Cout, bias=True, device="cuda")
+    with torch.no_grad():
+        m.weight.copy_(torch.from_numpy(inp.w))
+        m.bias.copy_(torch.from_numpy(inp.b))
+    x = to_dev(inp.x, "f32").view(2, 65, Cin, T).requires_grad_(True)
+    y = m(x)
+    y.backward(to_dev(inp.dy, "f32").view(2, 65, Cout, T))
+    torch.cuda.synchronize()
+    ref_y = orc.forward(inp.x, inp.w, inp.b)
+    ref_dx = orc.backward_input(inp.dy, inp.w)
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy)
+    assert rel_err(y.detach().cpu().numpy().reshape(N, Cout, T), ref_y) <= 1e-5
+    assert rel_err(x.grad.cpu().numpy().reshape(N, Cin, T), ref_dx) <= 1e-5
+    assert rel_err(m.weight.grad.cpu().numpy(), ref_dw) <= 1e-5
+    assert rel_err(m.bias.grad.cpu().numpy(), ref_db) <= 1e-5
