@@ -22,8 +22,10 @@ SOURCES = ["eql_api.cpp", "eql_f32.hip", "eql_f16.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed-fp32 instructions are switched off for all device code.
+# MFMA accumulators may live in arch VGPRs (gfx950 has a unified register
+# file); with this selection the large-tile kernels allocate without scratch.
 DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
-                "-packed-fp32-ops"]
+                "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
 COMMON_FLAGS = ["-O3", "-std=c++20", "-fPIC", "-Wall", "-Wno-unused-function",
                 "-I" + os.path.join(os.path.dirname(HERE), "include")]
 

@@ -23,10 +23,15 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
     p.S = 0;
     p.rows_per_split = 0;
   } else {
-    // Aim for about two workgroups per CU of a 256-CU device, without splits
-    // shorter than one row chunk.
+    // Aim for one workgroup per CU of a 256-CU device, but keep the fp32
+    // partials (written once, read once) under about 1/3 of the bytes of x
+    // and dy, and no split shorter than one row chunk.
     const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
-    int64_t s = (512 + tiles - 1) / tiles;
+    int64_t s = (256 + tiles - 1) / tiles;
+    const double in_bytes = (double)N * (Cin + Cout) * T * (f16 ? 2 : 4);
+    const double part_per_split = (double)T * p.Cout_pad * p.Cin_pad * 4.0;
+    const int64_t s_budget = (int64_t)(in_bytes / 3.0 / (2.0 * part_per_split));
+    if (s > s_budget) s = s_budget;
     const int64_t max_s = (N + p.KR - 1) / p.KR;
     if (s > max_s) s = max_s;
     if (s < 1) s = 1;
@@ -76,6 +81,9 @@ int check_shape(int64_t N, int T, int Cin, int Cout, int dtype) {
   if (dtype != EQL_F32 && dtype != EQL_F16) return EQL_ERR_INVALID_ARG;
   if (T < 1 || Cin < 1 || Cout < 1 || N < 0) return EQL_ERR_INVALID_ARG;
   if (T > EQLINEAR_MAX_T || Cin > kMaxC || Cout > kMaxC || N > kMaxN) return EQL_ERR_UNSUPPORTED;
+  // the weight spectrum (two padded copies) must stay under 2^31 bytes
+  if ((double)T * 2.0 * (Cin + 127) * (Cout + 127) * (dtype == EQL_F16 ? 2 : 4) >= 2147483648.0)
+    return EQL_ERR_UNSUPPORTED;
   return EQL_OK;
 }
 
@@ -83,6 +91,7 @@ int check_shape(int64_t N, int T, int Cin, int Cout, int dtype) {
 constexpr int kMaxDevices = 64;
 std::once_flag g_once[kMaxDevices];
 int g_arch_ok[kMaxDevices];
+int g_cus[kMaxDevices];
 
 int check_device() {
   int count = 0;
@@ -98,10 +107,13 @@ int check_device() {
   std::call_once(g_once[dev], [dev] {
     hipDeviceProp_t prop;
     g_arch_ok[dev] = 0;
-    if (hipGetDeviceProperties(&prop, dev) == hipSuccess)
+    g_cus[dev] = 256;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess) {
       g_arch_ok[dev] = strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 0;
-    else
+      if (prop.multiProcessorCount > 0) g_cus[dev] = prop.multiProcessorCount;
+    } else {
       (void)hipGetLastError();
+    }
   });
   return g_arch_ok[dev] ? EQL_OK : EQL_ERR_UNSUPPORTED;
 }
@@ -109,6 +121,18 @@ int check_device() {
 int launched(hipError_t e) { return e == hipSuccess ? EQL_OK : EQL_ERR_LAUNCH; }
 
 }  // namespace
+
+namespace eqk {
+// Valid after check_device() succeeded on the current device.
+int device_cu_count() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices || g_cus[dev] <= 0) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  return g_cus[dev];
+}
+}  // namespace eqk
 
 extern "C" {
 
@@ -129,8 +153,10 @@ const char* eqlinear_status_string(int status) {
 
 size_t eqlinear_weight_spectrum_bytes(int T, int Cin, int Cout, int dtype) {
   if (check_shape(0, T, Cin, Cout, dtype) != EQL_OK) return 0;
-  const eqk::WspecDims d = eqk::wspec_dims(Cin, Cout);
-  return (size_t)T * ((size_t)d.CoF * d.CiF + (size_t)d.CinB * d.CoutB) * elem_bytes(dtype);
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype == EQL_F16);
+  const size_t bytes =
+      (size_t)T * ((size_t)d.CoF * d.CiF + (size_t)d.CinB * d.CoutB) * elem_bytes(dtype);
+  return bytes < ((size_t)1 << 31) ? bytes : 0;  // kernels address the spectrum with 31-bit offsets
 }
 
 int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cout, int dtype,
@@ -168,7 +194,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   if (N == 0) return EQL_OK;
-  const eqk::WspecDims d = eqk::wspec_dims(Cin, Cout);
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype == EQL_F16);
   eqk::GemmArgs a{};
   a.in = in;
   a.bias = bias;
@@ -177,13 +203,12 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   a.Ci = Ci;
   a.Co = Co;
   a.stream = (hipStream_t)stream;
+  a.plan = eqk::gemm_plan(T, Ci, Co, dtype == EQL_F16);
   if (!bwd) {
     a.wsp = wspec;
-    a.Co_pad = d.CoF;
     a.Ci_pad = d.CiF;
   } else {
     a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
-    a.Co_pad = d.CinB;
     a.Ci_pad = d.CoutB;
   }
   return launched(dtype == EQL_F16 ? eqk::launch_gemm_f16(T, bwd, a)

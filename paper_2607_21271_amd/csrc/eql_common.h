@@ -96,7 +96,7 @@ __device__ __forceinline__ void axpy_c(float& acc, float v) {
 //   Re X_k = v_0 + (-1)^k v_{T/2} + sum_s e_s cos(2 pi k s/T)
 //   Im X_k = -sum_s d_s sin(2 pi k s/T)
 template <int T>
-__device__ __forceinline__ void rdft(const float (&v)[T], float (&P)[T]) {
+__device__ __forceinline__ void rdft_direct(const float (&v)[T], float (&P)[T]) {
   using B = Bins<T>;
   constexpr int S = B::S;
   float e[S + 1], d[S + 1];
@@ -140,7 +140,7 @@ __device__ __forceinline__ void rdft(const float (&v)[T], float (&P)[T]) {
 //   u_t = (X_0 + (-1)^t X_{T/2})/T + (2/T) sum_{k=1}^{K} (Re X_k cos(2 pi k t/T) - Im X_k sin(2 pi k t/T)).
 // Output pairs (t, T-t) share the even part E_t and differ in the sign of the odd part O_t.
 template <int T>
-__device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
+__device__ __forceinline__ void irdft_direct(const float (&P)[T], float (&u)[T]) {
   using B = Bins<T>;
   constexpr int S = B::S;
   constexpr float inv = (float)(1.0 / T);
@@ -175,6 +175,159 @@ __device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
     });
     u[T / 2] = uh;
   }
+}
+
+// ---------------------------------------------------------------------------
+// FFT forms for T = 4, 8, 16 (same planes, same results up to rounding order).
+//
+// T = 4: two length-2 butterflies.  Planes: 0 X0, 1 X2, 2 Re X1, 3 Im X1.
+__device__ __forceinline__ void rdft4(const float (&v)[4], float (&P)[4]) {
+  const float a0 = v[0] + v[2], a1 = v[1] + v[3];
+  P[0] = a0 + a1;
+  P[1] = a0 - a1;
+  P[2] = v[0] - v[2];
+  P[3] = v[3] - v[1];
+}
+__device__ __forceinline__ void irdft4(const float (&P)[4], float (&u)[4]) {
+  const float e = (P[0] + P[1]) * 0.25f, o = (P[0] - P[1]) * 0.25f;
+  u[0] = __builtin_fmaf(0.5f, P[2], e);
+  u[2] = __builtin_fmaf(-0.5f, P[2], e);
+  u[1] = __builtin_fmaf(-0.5f, P[3], o);
+  u[3] = __builtin_fmaf(0.5f, P[3], o);
+}
+
+// T = 8: radix-2 split on (s, s+4), a DFT4 of the sums for the even bins and a
+// twiddled DFT4 of the differences for the odd bins.
+// Planes: 0 X0, 1 X4, 2/3 Re/Im X1, 4/5 Re/Im X2, 6/7 Re/Im X3.
+constexpr float kR2 = 0.70710678118654752440f;  // 1/sqrt(2)
+__device__ __forceinline__ void rdft8(const float (&v)[8], float (&P)[8]) {
+  const float a0 = v[0] + v[4], a1 = v[1] + v[5], a2 = v[2] + v[6], a3 = v[3] + v[7];
+  const float b0 = v[0] - v[4], b1 = v[1] - v[5], b2 = v[2] - v[6], b3 = v[3] - v[7];
+  const float s02 = a0 + a2, s13 = a1 + a3;
+  P[0] = s02 + s13;
+  P[1] = s02 - s13;
+  P[4] = a0 - a2;
+  P[5] = a3 - a1;
+  const float p = b1 - b3, q = b1 + b3;
+  P[2] = __builtin_fmaf(kR2, p, b0);
+  P[6] = __builtin_fmaf(-kR2, p, b0);
+  P[3] = __builtin_fmaf(-kR2, q, -b2);
+  P[7] = __builtin_fmaf(-kR2, q, b2);
+}
+// Inverse: even outputs from X0+X4, Re X2 and the sums/differences of bins 1
+// and 3; odd outputs from X0-X4, Im X2 and bins 1, 3 rotated by e^{i pi/4}.
+__device__ __forceinline__ void irdft8(const float (&P)[8], float (&u)[8]) {
+  constexpr float h = 0.125f, q = 0.25f, qr = 0.25f * kR2;
+  const float A = (P[0] + P[1]) * h, Bo = (P[0] - P[1]) * h;
+  const float S = P[2] + P[6], D = P[7] - P[3];
+  const float e1 = __builtin_fmaf(q, P[4], A), e2 = __builtin_fmaf(-q, P[4], A);
+  u[0] = __builtin_fmaf(q, S, e1);
+  u[4] = __builtin_fmaf(-q, S, e1);
+  u[2] = __builtin_fmaf(q, D, e2);
+  u[6] = __builtin_fmaf(-q, D, e2);
+  const float t1 = P[2] - P[3], t2 = P[6] + P[7], t3 = P[6] - P[7], t4 = P[2] + P[3];
+  const float sd = t1 - t2, dd = t3 - t4;
+  const float o1 = __builtin_fmaf(-q, P[5], Bo), o2 = __builtin_fmaf(q, P[5], Bo);
+  u[1] = __builtin_fmaf(qr, sd, o1);
+  u[5] = __builtin_fmaf(-qr, sd, o1);
+  u[3] = __builtin_fmaf(qr, dd, o2);
+  u[7] = __builtin_fmaf(-qr, dd, o2);
+}
+
+// T = 16: two DFT8 of the even and odd samples, combined with the twiddles
+// w^k = e^{-i pi k/8}: X_k = E_k + w^k O_k and X_{8-k} = conj(E_k - w^k O_k).
+// Planes: 0 X0, 1 X8, 2k/2k+1 Re/Im X_k for k = 1..7.
+__device__ __forceinline__ void rdft16(const float (&v)[16], float (&P)[16]) {
+  float ve[8], vo[8], E[8], O[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) { ve[i] = v[2 * i]; vo[i] = v[2 * i + 1]; }
+  rdft8(ve, E);
+  rdft8(vo, O);
+  // E, O planes: 0 X0, 1 X4, 2/3 X1, 4/5 X2, 6/7 X3 (length-8 spectra)
+  P[0] = E[0] + O[0];
+  P[1] = E[0] - O[0];
+  // k = 4: w^4 = -i and E_4, O_4 are the (real) Nyquist bins of E and O
+  P[8] = E[1];
+  P[9] = -O[1];
+  constexpr float c1 = 0.92387953251128675613f, s1 = 0.38268343236508977173f;  // cos, sin(pi/8)
+  // k = 1: Z = w O1 = (c - i s)(Or + i Oi)
+  {
+    const float zr = __builtin_fmaf(c1, O[2], s1 * O[3]);
+    const float zi = __builtin_fmaf(c1, O[3], -s1 * O[2]);
+    P[2] = E[2] + zr; P[3] = E[3] + zi;      // X1
+    P[14] = E[2] - zr; P[15] = zi - E[3];    // X7 = conj(E1 - Z)
+  }
+  // k = 2: w^2 = (1 - i)/sqrt2, uses E2/O2 planes 4/5
+  {
+    const float zr = kR2 * (O[4] + O[5]);
+    const float zi = kR2 * (O[5] - O[4]);
+    P[4] = E[4] + zr; P[5] = E[5] + zi;      // X2
+    P[12] = E[4] - zr; P[13] = zi - E[5];    // X6
+  }
+  // k = 3: w^3 = (s - i c), uses E3/O3 planes 6/7
+  {
+    const float zr = __builtin_fmaf(s1, O[6], c1 * O[7]);
+    const float zi = __builtin_fmaf(s1, O[7], -c1 * O[6]);
+    P[6] = E[6] + zr; P[7] = E[7] + zi;      // X3
+    P[10] = E[6] - zr; P[11] = zi - E[7];    // X5
+  }
+}
+// Inverse: even outputs are irdft8 of A_k = X_k + X_{k+8}, odd outputs irdft8
+// of B_k = (X_k - X_{k+8}) e^{i pi k/8}, each times 1/2.
+__device__ __forceinline__ void irdft16(const float (&P)[16], float (&u)[16]) {
+  // X_k (k = 1..7): Re P[2k], Im P[2k+1]; X_0 = P[0], X_8 = P[1].
+  // X_{k+8} = conj(X_{8-k}) for k = 1..4.
+  float A[8], Bq[8];
+  A[0] = 0.5f * (P[0] + P[1]);
+  Bq[0] = 0.5f * (P[0] - P[1]);
+  A[1] = 0.5f * (2.0f * P[8]);   // A_4 = 2 Re X4, length-8 Nyquist plane
+  Bq[1] = 0.5f * (-2.0f * P[9]); // B_4 = -2 Im X4
+  constexpr float c1 = 0.92387953251128675613f, s1 = 0.38268343236508977173f;
+  // k = 1: A1 = X1 + conj(X7); B1 = (X1 - conj(X7)) e^{i pi/8}
+  {
+    const float ar = P[2] + P[14], ai = P[3] - P[15];
+    const float dr = P[2] - P[14], di = P[3] + P[15];
+    A[2] = 0.5f * ar; A[3] = 0.5f * ai;
+    Bq[2] = 0.5f * __builtin_fmaf(c1, dr, -s1 * di);
+    Bq[3] = 0.5f * __builtin_fmaf(c1, di, s1 * dr);
+  }
+  // k = 2: with X6; rotation e^{i pi/4}
+  {
+    const float ar = P[4] + P[12], ai = P[5] - P[13];
+    const float dr = P[4] - P[12], di = P[5] + P[13];
+    A[4] = 0.5f * ar; A[5] = 0.5f * ai;
+    Bq[4] = (0.5f * kR2) * (dr - di);
+    Bq[5] = (0.5f * kR2) * (di + dr);
+  }
+  // k = 3: with X5; rotation e^{i 3pi/8} = (s1 + i c1)
+  {
+    const float ar = P[6] + P[10], ai = P[7] - P[11];
+    const float dr = P[6] - P[10], di = P[7] + P[11];
+    A[6] = 0.5f * ar; A[7] = 0.5f * ai;
+    Bq[6] = 0.5f * __builtin_fmaf(s1, dr, -c1 * di);
+    Bq[7] = 0.5f * __builtin_fmaf(s1, di, c1 * dr);
+  }
+  float ue[8], uo[8];
+  irdft8(A, ue);
+  irdft8(Bq, uo);
+#pragma unroll
+  for (int m = 0; m < 8; ++m) { u[2 * m] = ue[m]; u[2 * m + 1] = uo[m]; }
+}
+
+// Dispatch: FFT forms where written, the symmetric direct form otherwise.
+template <int T>
+__device__ __forceinline__ void rdft(const float (&v)[T], float (&P)[T]) {
+  if constexpr (T == 4) rdft4(v, P);
+  else if constexpr (T == 8) rdft8(v, P);
+  else if constexpr (T == 16) rdft16(v, P);
+  else rdft_direct<T>(v, P);
+}
+template <int T>
+__device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
+  if constexpr (T == 4) irdft4(P, u);
+  else if constexpr (T == 8) irdft8(P, u);
+  else if constexpr (T == 16) irdft16(P, u);
+  else irdft_direct<T>(P, u);
 }
 
 // ---------------------------------------------------------------------------
@@ -237,6 +390,13 @@ struct Mma<false> {
 __device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
 __device__ __forceinline__ int lds_off(int row, int byte_in_row) {
   return row * 64 + (swz(row, byte_in_row >> 4) << 4) + (byte_in_row & 15);
+}
+
+// Widest power-of-two byte width (<= 16) dividing a run of L elements.
+template <bool F16, int L>
+constexpr int run_vec_bytes() {
+  constexpr int NB = L * Elem<F16>::bytes;
+  return (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
 }
 
 // ---------------------------------------------------------------------------
@@ -307,15 +467,15 @@ __device__ __forceinline__ void store_run(void* base, int64_t elem_off, bool vec
       if constexpr (VEC == 16) {
         u32x4 w;
         __builtin_memcpy(&w, tmp, 16);
-        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(p + s * PER));
+        *reinterpret_cast<u32x4*>(p + s * PER) = w;
       } else if constexpr (VEC == 8) {
         u32x2 w;
         __builtin_memcpy(&w, tmp, 8);
-        __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(p + s * PER));
+        *reinterpret_cast<u32x2*>(p + s * PER) = w;
       } else {
         uint32_t w;
         __builtin_memcpy(&w, tmp, 4);
-        __builtin_nontemporal_store(w, reinterpret_cast<uint32_t*>(p + s * PER));
+        *reinterpret_cast<uint32_t*>(p + s * PER) = w;
       }
     }
   } else {

@@ -1,0 +1,496 @@
+// eql_gemm.h -- forward and input-gradient kernel of the C_T equivariant linear
+// layer for gfx950: rDFT prologue -> per-bin MFMA products -> irDFT (+bias)
+// epilogue, fused in one pass over the rows (Alg. 1 steps 1-4; Sec. 3.5).
+//
+// Work split.  The grid is persistent: workgroup w owns rows
+// [w*N/G, (w+1)*N/G), so every CU streams the same number of rows.  A
+// workgroup is 4 waves; its rows are dealt out in rounds of 64, row q of a
+// round going to wave q % 4, lane-row q / 4, so the waves of a workgroup get
+// equal shares even when the workgroup holds fewer than 64 rows.
+//
+// Activations never pass through LDS.  Lane (g, i) of a wave loads, for its
+// row i, the KW consecutive channels of quarter g of the contraction step,
+// all T group positions of each (KW*T contiguous elements), transforms them in
+// registers and packs the result straight into the MFMA B operand (row i,
+// contraction elements of group g) of every spectral plane.  Each activation
+// element is loaded and transformed once per o-chunk (once in total when the
+// spectrum stays resident, RES).
+//
+// Weight planes stream through LDS: per step a block of T planes x OC output
+// channels x KSTEP contraction channels is prefetched into registers, written
+// to the idle half of a double buffer and read as MFMA A operands by all four
+// waves; one barrier per step.
+//
+// MFMA computes D[o][n] = sum_k A[o][k] B[k][n]; each lane ends with 4
+// consecutive output channels of one row for every plane, so the inverse
+// transform and bias run in registers and each lane writes 4*T contiguous
+// outputs.
+#pragma once
+#include "eql_common.h"
+
+namespace eqk {
+
+template <int T, bool F16>
+struct GemmShape {
+  static constexpr int EB = F16 ? 2 : 4;
+  static constexpr int kw_fit = 128 / (T * EB);  // channels whose T values fill <= 128 bytes
+  static constexpr int KW = F16 ? (kw_fit >= 8 ? 8 : 4)
+                                : (kw_fit >= 8 ? 8 : kw_fit >= 4 ? 4 : kw_fit >= 2 ? 2 : 1);
+  static constexpr int KSTEP = 4 * KW;  // contraction channels per step (4 lane groups)
+  static constexpr int FB = KW * EB;    // operand fragment bytes per lane
+  static constexpr int RB = 4 * FB;     // bytes of one weight row per step
+  static constexpr int NBX = KW * T * EB;  // raw activation bytes per lane per step
+};
+
+template <int FB>
+struct Frag {
+  uint32_t w[FB / 4];
+};
+
+template <bool F16, int KW>
+__device__ __forceinline__ void frag_mma(floatx4& acc, const Frag<KW*(F16 ? 2 : 4)>& a,
+                                         const Frag<KW*(F16 ? 2 : 4)>& b) {
+  if constexpr (F16 && KW == 8) {
+    const u32x4 av = {a.w[0], a.w[1], a.w[2], a.w[3]};
+    const u32x4 bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, av),
+                                                 __builtin_bit_cast(half8, bv), acc, 0, 0, 0);
+  } else if constexpr (F16 && KW == 4) {
+    typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+    const u32x2 av = {a.w[0], a.w[1]};
+    const u32x2 bv = {b.w[0], b.w[1]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(half4, av),
+                                                __builtin_bit_cast(half4, bv), acc, 0, 0, 0);
+  } else {
+#pragma unroll
+    for (int s = 0; s < KW; ++s)
+      acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__builtin_bit_cast(float, a.w[s]),
+                                                 __builtin_bit_cast(float, b.w[s]), acc, 0, 0, 0);
+  }
+}
+
+template <bool F16, int FB>
+__device__ __forceinline__ Frag<FB> frag_neg(const Frag<FB>& a) {
+  Frag<FB> r;
+#pragma unroll
+  for (int j = 0; j < FB / 4; ++j) r.w[j] = a.w[j] ^ (F16 ? 0x80008000u : 0x80000000u);
+  return r;
+}
+
+// Swizzled LDS rows of RB bytes: 16-byte chunk c of row r lives at chunk
+// c ^ ((r >> 1) & (RB/16 - 1)).
+template <int RB>
+__device__ __forceinline__ int wl_off(int row, int byte) {
+  constexpr int NCH = RB / 16;
+  const int ch = byte >> 4;
+  return row * RB + ((ch ^ ((row >> 1) & (NCH - 1))) << 4) + (byte & 15);
+}
+
+template <int FB, int RB>
+__device__ __forceinline__ Frag<FB> lds_frag(const char* base, int row, int g) {
+  Frag<FB> f;
+  if constexpr (FB == 32) {
+    const u32x4 a = *reinterpret_cast<const u32x4*>(base + wl_off<RB>(row, g * 32));
+    const u32x4 b = *reinterpret_cast<const u32x4*>(base + wl_off<RB>(row, g * 32 + 16));
+    f.w[0] = a[0]; f.w[1] = a[1]; f.w[2] = a[2]; f.w[3] = a[3];
+    f.w[4] = b[0]; f.w[5] = b[1]; f.w[6] = b[2]; f.w[7] = b[3];
+  } else if constexpr (FB == 16) {
+    const u32x4 a = *reinterpret_cast<const u32x4*>(base + wl_off<RB>(row, g * 16));
+    f.w[0] = a[0]; f.w[1] = a[1]; f.w[2] = a[2]; f.w[3] = a[3];
+  } else {
+    static_assert(FB == 8, "fragment size");
+    const u32x2 a = *reinterpret_cast<const u32x2*>(base + wl_off<RB>(row, g * 8));
+    f.w[0] = a[0]; f.w[1] = a[1];
+  }
+  return f;
+}
+
+// Buffer resource over [base, base + bytes): loads past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+
+// Raw activation bytes of one lane for one step: NB bytes at byte offset off
+// of the resource.  vec is the widest load width (16, 8, 4) every row start
+// allows, 2 for 16-bit loads.  Elements past nvalid (a ragged last channel
+// group) are zeroed; bytes past the resource read as zero.
+template <int NB>
+__device__ __forceinline__ void load_raw(__amdgpu_buffer_rsrc_t rs, uint32_t off, int soff, int vec,
+                                         uint32_t (&r)[NB / 4]) {
+  if (vec == 16 && NB % 16 == 0) {
+#pragma unroll
+    for (int v = 0; v < NB / 16; ++v) {
+      const u32x4 x = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * v, soff, 0));
+      r[4 * v] = x[0]; r[4 * v + 1] = x[1]; r[4 * v + 2] = x[2]; r[4 * v + 3] = x[3];
+    }
+  } else if (vec >= 8 && NB % 8 == 0) {
+#pragma unroll
+    for (int v = 0; v < NB / 8; ++v) {
+      const u32x2 x = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, off + 8 * v, soff, 0));
+      r[2 * v] = x[0]; r[2 * v + 1] = x[1];
+    }
+  } else if (vec >= 4) {
+#pragma unroll
+    for (int v = 0; v < NB / 4; ++v) r[v] = __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4 * v, soff, 0);
+  } else {
+#pragma unroll
+    for (int v = 0; v < NB / 4; ++v) {
+      const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * v, soff, 0);
+      const uint32_t hi = __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * v + 2, soff, 0);
+      r[v] = (lo & 0xffffu) | (hi << 16);
+    }
+  }
+}
+
+// Zero the elements past nvalid (a ragged last channel group).
+template <int NB, int EB>
+__device__ __forceinline__ void mask_raw(int nvalid_elems, uint32_t (&r)[NB / 4]) {
+  if (nvalid_elems >= NB / EB) return;
+#pragma unroll
+  for (int v = 0; v < NB / 4; ++v) {
+    if constexpr (EB == 2) {
+      if (2 * v + 1 >= nvalid_elems) r[v] = (2 * v < nvalid_elems) ? (r[v] & 0xffffu) : 0u;
+    } else {
+      if (v >= nvalid_elems) r[v] = 0u;
+    }
+  }
+}
+
+template <bool F16>
+__device__ __forceinline__ float raw_elem(const uint32_t* r, int e) {
+  if constexpr (F16) {
+    const uint32_t w = r[e >> 1];
+    const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
+    return (float)__builtin_bit_cast(_Float16, h);
+  } else {
+    return __builtin_bit_cast(float, r[e]);
+  }
+}
+
+template <bool F16>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  if constexpr (F16) {
+    const uint16_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
+    const uint16_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
+    return (uint32_t)lo | ((uint32_t)hi << 16);
+  } else {
+    return __builtin_bit_cast(uint32_t, a);
+  }
+}
+
+// Transform the KW channels held raw by one lane into T operand fragments.
+template <int T, bool F16>
+__device__ __forceinline__ void raw_to_frags(const uint32_t (&r)[GemmShape<T, F16>::NBX / 4],
+                                             Frag<GemmShape<T, F16>::FB> (&B)[T]) {
+  using S = GemmShape<T, F16>;
+  constexpr int KW = S::KW;
+  if constexpr (F16) {
+#pragma unroll
+    for (int j = 0; j < KW; j += 2) {
+      float v0[T], v1[T], P0[T], P1[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        v0[t] = raw_elem<true>(r, j * T + t);
+        v1[t] = raw_elem<true>(r, (j + 1) * T + t);
+      }
+      rdft<T>(v0, P0);
+      rdft<T>(v1, P1);
+#pragma unroll
+      for (int p = 0; p < T; ++p) B[p].w[j >> 1] = pack2<true>(P0[p], P1[p]);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < KW; ++j) {
+      float v[T], P[T];
+#pragma unroll
+      for (int t = 0; t < T; ++t) v[t] = raw_elem<false>(r, j * T + t);
+      rdft<T>(v, P);
+#pragma unroll
+      for (int p = 0; p < T; ++p) B[p].w[j] = __builtin_bit_cast(uint32_t, P[p]);
+    }
+  }
+}
+
+// Transform the HKW channels held raw by one lane; P[p][j] is plane p of channel j.
+template <int T, bool F16, int HKW>
+__device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (F16 ? 2 : 4) / 4],
+                                              float (&P)[T][HKW]) {
+#pragma unroll
+  for (int j = 0; j < HKW; ++j) {
+    float v[T], q[T];
+#pragma unroll
+    for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(r, j * T + t);
+    rdft<T>(v, q);
+#pragma unroll
+    for (int p = 0; p < T; ++p) P[p][j] = q[p];
+  }
+}
+
+// Kernel parameters: the workgroup is 8 waves, wave w = 2*rg + oh.  Waves rg
+// own rows; the pair (rg, 0), (rg, 1) shares 16 rows and splits each o-chunk:
+// wave oh computes OT output tiles of 16, so an o-chunk holds OC = 32*OT
+// channels.  RES keeps each wave's operand spectrum of all NKR contraction
+// steps in registers across o-chunks (requires ceil(Ci / KSTEP) == NKR).
+//
+// Per contraction step a lane of wave oh transforms HKW = KW/2 channels of its
+// row and writes their planes to the pair's spectrum buffer in LDS; after a
+// barrier both waves read complete MFMA operands from it.  Weight blocks are
+// double buffered in LDS: the next block is loaded into registers while the
+// current one feeds the MFMAs, then written to the idle buffer.
+template <int T, bool F16, bool BWD, int OT, bool RES, int NKR>
+__global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ in,
+                                                       const void* __restrict__ wsp,
+                                                       const void* __restrict__ bias,
+                                                       void* __restrict__ out, int64_t N, int Ci,
+                                                       int Co, int Ci_pad, int Co_pad, int n_oc,
+                                                       int n_ks) {
+  using S = GemmShape<T, F16>;
+  using Bn = Bins<T>;
+  using FR = Frag<S::FB>;
+  using E = typename Elem<F16>::T;
+  constexpr int EB = S::EB;
+  constexpr int KW = S::KW;
+  constexpr int HKW = KW / 2;
+  constexpr int KSTEP = S::KSTEP;
+  constexpr int FB = S::FB;
+  constexpr int RB = S::RB;             // bytes of one row (weights or spectrum) per step
+  constexpr int NBH = HKW * T * EB;     // raw activation bytes per lane per step
+  constexpr int OC = 32 * OT;
+  constexpr int WBLK = T * OC * RB;     // bytes of one weight block
+  constexpr int NU = WBLK / 16;         // 16-byte units per block
+  constexpr int UPT = (NU + 511) / 512; // weight units per thread
+  constexpr int XBLK = 4 * T * 16 * RB; // spectrum buffer: 4 row groups x T planes x 16 rows
+  static_assert(KW >= 2, "contraction split");
+
+  __shared__ __attribute__((aligned(16))) char wl[2][WBLK];
+  __shared__ __attribute__((aligned(16))) char xl[XBLK];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int rg = wave >> 1;
+  const int oh = wave & 1;
+  const int g = lane >> 4;
+  const int li = lane & 15;
+  const int64_t r0 = (int64_t)blockIdx.x * N / gridDim.x;
+  const int64_t r1 = ((int64_t)blockIdx.x + 1) * N / gridDim.x;
+  const int64_t len = r1 - r0;
+  const int rounds = (int)((len + 63) / 64);
+  const int nks = RES ? NKR : n_ks;
+  const int64_t wplane = (int64_t)Co_pad * Ci_pad * EB;
+  const char* wbase = reinterpret_cast<const char*>(wsp);
+  const char* xin = reinterpret_cast<const char*>(in);
+  const int rowb = Ci * T * EB;
+  const int vec = (rowb % 16 == 0) ? 16 : (rowb % 8 == 0) ? 8 : (rowb % 4 == 0) ? 4 : 2;
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(xin + r0 * rowb, (uint32_t)(len * rowb));
+  if (rounds == 0) return;
+
+  // ---- weight block (oc, kc): global -> registers -> LDS buffer.  Per-thread
+  // unit offsets are fixed; a step only moves a uniform base.
+  u32x4 wr[UPT];
+  int goff[UPT];
+  int loff[UPT];
+#pragma unroll
+  for (int u = 0; u < UPT; ++u) {
+    const int unit = tid + 512 * u;
+    const int p = unit / (OC * RB / 16);
+    const int rem = unit - p * (OC * RB / 16);
+    const int row = rem / (RB / 16);
+    const int ch = rem - row * (RB / 16);
+    goff[u] = (unit < NU) ? (int)(p * wplane + (int64_t)row * Ci_pad * EB + ch * 16) : 0;
+    loff[u] = (unit < NU) ? p * OC * RB + wl_off<RB>(row, ch * 16) : 0;
+  }
+  auto issue_w = [&](int oc, int kc) {
+    const char* blk = wbase + ((int64_t)oc * OC * Ci_pad + kc * KSTEP) * EB;
+#pragma unroll
+    for (int u = 0; u < UPT; ++u)
+      if (NU % 512 == 0 || tid + 512 * u < NU) wr[u] = *reinterpret_cast<const u32x4*>(blk + goff[u]);
+  };
+  auto store_w = [&](int buf) {
+#pragma unroll
+    for (int u = 0; u < UPT; ++u)
+      if (NU % 512 == 0 || tid + 512 * u < NU) *reinterpret_cast<u32x4*>(&wl[buf][loff[u]]) = wr[u];
+  };
+
+  // ---- raw activations of (round m, step kc): HKW channels of this lane's row
+  uint32_t xr[NBH / 4];
+  int xr_valid = 0;  // valid elements in xr (the rest belong to the next row)
+  auto issue_x = [&](int m, int kc) {
+    const int q = m * 64 + 4 * li + rg;
+    const int c0 = oh * (KSTEP / 2) + g * HKW;  // channel within the step
+    const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
+    const int cabs = kc * KSTEP + c0;
+    xr_valid = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
+    load_raw<NBH>(xrs, voff, kc * KSTEP * T * EB, vec, xr);
+  };
+  // transform and publish this lane's part of the step's operand spectrum
+  auto publish_x = [&]() {
+    mask_raw<NBH, EB>(xr_valid, xr);
+    float P[T][HKW];
+    raw_to_planes<T, F16, HKW>(xr, P);
+    const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
+#pragma unroll
+    for (int p = 0; p < T; ++p) {
+      if constexpr (F16) {
+        uint32_t w[HKW / 2];
+#pragma unroll
+        for (int j = 0; j < HKW / 2; ++j) w[j] = pack2<true>(P[p][2 * j], P[p][2 * j + 1]);
+        char* dst = &xl[(rg * T + p) * 16 * RB + wl_off<RB>(li, byte)];
+        if constexpr (HKW == 4) *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
+        else *reinterpret_cast<uint32_t*>(dst) = w[0];
+      } else {
+        char* dst = &xl[(rg * T + p) * 16 * RB + wl_off<RB>(li, byte)];
+        if constexpr (HKW == 4) {
+          *reinterpret_cast<u32x4*>(dst) = u32x4{__builtin_bit_cast(uint32_t, P[p][0]), __builtin_bit_cast(uint32_t, P[p][1]),
+                                                 __builtin_bit_cast(uint32_t, P[p][2]), __builtin_bit_cast(uint32_t, P[p][3])};
+        } else if constexpr (HKW == 2) {
+          *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_bit_cast(uint32_t, P[p][0]), __builtin_bit_cast(uint32_t, P[p][1])};
+        } else {
+          *reinterpret_cast<uint32_t*>(dst) = __builtin_bit_cast(uint32_t, P[p][0]);
+        }
+      }
+    }
+  };
+  auto read_x = [&](FR (&B)[T]) {
+#pragma unroll
+    for (int p = 0; p < T; ++p) B[p] = lds_frag<FB, RB>(&xl[(rg * T + p) * 16 * RB], li, g);
+  };
+
+  floatx4 acc[T][OT];
+  FR xres[RES ? NKR : 1][T];
+  FR bcur[T];
+  const E* bp = reinterpret_cast<const E*>(bias);
+  const bool out_vec = ((int64_t)Co * T * EB) % run_vec_bytes<F16, 4 * T>() == 0;
+
+  // One step: weights of (oc, kc) in LDS buffer buf, B the operand spectrum.
+  // The sign of each complex product sits on a negated copy of one B plane
+  // (Im for the forward, Re for the input gradient), made once per step:
+  //   forward:  Re += Wr Xr + Wi (-Xi),   Im += Wi Xr + Wr Xi
+  //   backward: Re += Wr Dr + Wi Di,      Im += Wr Di + Wi (-Dr)
+  auto mma_step = [&](int oc, int buf, FR (&B)[T]) {
+    FR Bneg[Bn::K > 0 ? Bn::K : 1];
+    static_for<Bn::K>([&](auto ki) {
+      constexpr int k = decltype(ki)::value + 1;
+      Bneg[k - 1] = frag_neg<F16, FB>(B[BWD ? Bn::re(k) : Bn::im(k)]);
+    });
+#pragma unroll
+    for (int a = 0; a < OT; ++a) {
+      const int ot = oh * OT + a;                 // o-tile within the chunk
+      if (oc * OC + ot * 16 >= Co) continue;      // uniform across the wave
+      FR A[T];
+#pragma unroll
+      for (int p = 0; p < T; ++p) A[p] = lds_frag<FB, RB>(&wl[buf][p * OC * RB], ot * 16 + li, g);
+      frag_mma<F16, KW>(acc[0][a], A[0], B[0]);
+      if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a], A[1], B[1]);
+      static_for<Bn::K>([&](auto ki) {
+        constexpr int k = decltype(ki)::value + 1;
+        constexpr int r = Bn::re(k);
+        constexpr int i = Bn::im(k);
+        if constexpr (!BWD) {
+          frag_mma<F16, KW>(acc[r][a], A[r], B[r]);
+          frag_mma<F16, KW>(acc[i][a], A[i], B[r]);
+          frag_mma<F16, KW>(acc[r][a], A[i], Bneg[k - 1]);
+          frag_mma<F16, KW>(acc[i][a], A[r], B[i]);
+        } else {
+          frag_mma<F16, KW>(acc[r][a], A[r], B[r]);
+          frag_mma<F16, KW>(acc[i][a], A[r], B[i]);
+          frag_mma<F16, KW>(acc[r][a], A[i], B[i]);
+          frag_mma<F16, KW>(acc[i][a], A[i], Bneg[k - 1]);
+        }
+      });
+    }
+  };
+
+  // Per lane: 4 consecutive output channels of one row per o-tile, written as
+  // one contiguous run of 4*T elements (ordinary stores, so L2 merges the
+  // lanes' runs into whole lines).
+  auto epilogue = [&](int m, int oc) {
+    const int64_t q = (int64_t)m * 64 + 4 * li + rg;
+    if (q >= len) return;
+    const int64_t n = r0 + q;
+#pragma unroll
+    for (int a = 0; a < OT; ++a) {
+      const int ot = oh * OT + a;
+      const int o4 = oc * OC + ot * 16 + 4 * g;
+      if (oc * OC + ot * 16 >= Co || o4 >= Co) continue;
+      float u[4 * T];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float Pl[T], ul[T];
+#pragma unroll
+        for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
+        irdft<T>(Pl, ul);
+        float bv = 0.0f;
+        if constexpr (!BWD) {
+          if (bp != nullptr && o4 + r < Co) bv = (float)bp[o4 + r];
+        }
+#pragma unroll
+        for (int t = 0; t < T; ++t) u[r * T + t] = ul[t] + bv;
+      }
+      const int nvalid = (Co - o4 >= 4 ? 4 : Co - o4) * T;
+      store_run<F16, 4 * T>(out, (n * Co + o4) * T, out_vec, nvalid, u);
+    }
+  };
+
+  auto zero_acc = [&]() {
+#pragma unroll
+    for (int p = 0; p < T; ++p)
+#pragma unroll
+      for (int a = 0; a < OT; ++a) acc[p][a] = floatx4{0.f, 0.f, 0.f, 0.f};
+  };
+
+  // Step protocol (running step s, weights of s in wl[s & 1]):
+  //   publish X(s) to xl; barrier (1): X(s) and W(s) visible
+  //   issue loads W(s+1) -> registers, activations for s+1
+  //   read operands, MFMA(s); W(s+1) -> wl[(s+1) & 1] (last read at step s-1)
+  //   barrier (2): W(s+1) visible next step, xl free again
+  issue_w(0, 0);
+  issue_x(0, 0);
+  store_w(0);
+  int buf = 0;
+  for (int m = 0; m < rounds; ++m) {
+    for (int oc = 0; oc < n_oc; ++oc) {
+      zero_acc();
+      if constexpr (RES) {
+        static_for<NKR>([&](auto kci) {
+          constexpr int kc = decltype(kci)::value;
+          int noc = oc, nkc = kc + 1, nm = m;
+          if (nkc == NKR) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
+          const bool more = nm < rounds;
+          if (oc == 0) publish_x();
+          __syncthreads();
+          if (more) issue_w(noc, nkc);
+          if (oc == 0) {
+            if (kc + 1 < NKR) issue_x(m, kc + 1);
+            else if (m + 1 < rounds) issue_x(m + 1, 0);
+            read_x(xres[kc]);
+          }
+          mma_step(oc, buf, xres[kc]);
+          if (more) store_w(buf ^ 1);
+          __syncthreads();
+          buf ^= 1;
+        });
+      } else {
+        for (int kc = 0; kc < nks; ++kc) {
+          int noc = oc, nkc = kc + 1, nm = m;
+          if (nkc == nks) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
+          const bool more = nm < rounds;
+          publish_x();
+          __syncthreads();
+          if (more) {
+            issue_w(noc, nkc);
+            issue_x(nm, nkc);
+          }
+          read_x(bcur);
+          mma_step(oc, buf, bcur);
+          if (more) store_w(buf ^ 1);
+          __syncthreads();
+          buf ^= 1;
+        }
+      }
+      epilogue(m, oc);
+    }
+  }
+}
+
+}  // namespace eqk

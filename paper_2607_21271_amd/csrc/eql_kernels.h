@@ -2,8 +2,7 @@
 //
 //   eql_wspec_kernel        weight spectrum (Alg. 1 step 1 applied to the shared
 //                           parameters, Sec. 3.2.1 Eq. 4), stored as T real planes
-//   eql_gemm_kernel         forward (Alg. 1 steps 1-4) and input gradient: rDFT
-//                           prologue -> per-bin MFMA GEMMs -> irDFT (+bias) epilogue
+//   (eql_gemm_kernel, the forward and input-gradient kernel, is in eql_gemm.h)
 //   eql_wgrad_kernel        weight gradient, split over rows: spectra of x and dy,
 //                           per-bin conj(X)^T dY on MFMA, fp32 partials per split
 //   eql_wgrad_reduce_kernel fixed-order sum of the split partials, irDFT, db
@@ -14,29 +13,36 @@
 
 namespace eqk {
 
-template <bool F16, int L>
-constexpr int run_vec_bytes() {
-  constexpr int NB = L * Elem<F16>::bytes;
-  return (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
-}
-
 // ---------------------------------------------------------------------------
 // Weight spectrum.  For every (o, c): the T lags w[0..T-1, o, c] are transformed
 // by the same real DFT as the activations, giving What_k[o, c] in plane form.
 // Two zero-padded copies are written:
 //   forward  layout  F[p][o][c], dims [T][CoF][CiF]     (A operand of the forward)
 //   backward layout  B[p][c][o], dims [T][CinB][CoutB]  (A operand of the input gradient)
+// Threads [0, CoF*CiF) fill F with c fastest; the next CinB*CoutB threads fill
+// B with o fastest, so both sets of stores are coalesced.
 template <int T, bool F16>
 __global__ __launch_bounds__(256) void eql_wspec_kernel(const void* __restrict__ w,
                                                         void* __restrict__ wspec, int Cin, int Cout,
                                                         int CoF, int CiF, int CinB, int CoutB) {
   using E = typename Elem<F16>::T;
-  const int OD = CoF > CoutB ? CoF : CoutB;
-  const int CD = CiF > CinB ? CiF : CinB;
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)OD * CD) return;
-  const int o = (int)(idx / CD);
-  const int c = (int)(idx % CD);
+  const int64_t nF = (int64_t)CoF * CiF;
+  const int64_t nB = (int64_t)CinB * CoutB;
+  int o, c;
+  bool toF;
+  if (idx < nF) {
+    o = (int)(idx / CiF);
+    c = (int)(idx - (int64_t)o * CiF);
+    toF = true;
+  } else if (idx < nF + nB) {
+    const int64_t j = idx - nF;
+    c = (int)(j / CoutB);
+    o = (int)(j - (int64_t)c * CoutB);
+    toF = false;
+  } else {
+    return;
+  }
   float v[T];
   const E* wp = reinterpret_cast<const E*>(w);
   const bool ok = o < Cout && c < Cin;
@@ -45,179 +51,13 @@ __global__ __launch_bounds__(256) void eql_wspec_kernel(const void* __restrict__
   float P[T];
   rdft<T>(v, P);
   E* F = reinterpret_cast<E*>(wspec);
-  E* Bl = F + (int64_t)T * CoF * CiF;
-  if (o < CoF && c < CiF) {
+  if (toF) {
 #pragma unroll
     for (int p = 0; p < T; ++p) F[((int64_t)p * CoF + o) * CiF + c] = (E)P[p];
-  }
-  if (c < CinB && o < CoutB) {
+  } else {
+    E* Bl = F + (int64_t)T * CoF * CiF;
 #pragma unroll
     for (int p = 0; p < T; ++p) Bl[((int64_t)p * CinB + c) * CoutB + o] = (E)P[p];
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Spectral GEMM with fused transforms.
-//
-// BWD = false (forward):  in = x[N,Cin,T], out = y[N,Cout,T], Ci = Cin, Co = Cout,
-//   Yhat_k[n,o] = sum_c What_k[o,c] Xhat_k[n,c]                        (Eq. 5)
-// BWD = true (input gradient): in = dy, out = dx, Ci = Cout, Co = Cin,
-//   dXhat_k[n,c] = sum_o conj(What_k[o,c]) dYhat_k[n,o]
-// For a complex bin with planes (r, i) the product is the real block form
-//   forward:  Re += Wr Xr - Wi Xi,   Im += Wi Xr + Wr Xi
-//   backward: Re += Wr Dr + Wi Di,   Im += Wr Di - Wi Dr
-// (the p4 instance of the forward is the a0..a3 of Appendix A.2).
-//
-// One workgroup of 4 waves owns BM rows x BO = 4*WO output channels and all T
-// planes of them.  MFMA computes D[o][n] = sum_k A[o][k] B[k][n] with A the
-// weight planes (read straight from the L2-resident spectrum, layout
-// [T][Co_pad][Ci_pad]) and B the activation spectrum, which the prologue
-// builds once per K chunk in LDS and all waves share.  Each lane ends with 4
-// consecutive output channels of one row for every plane, so the epilogue
-// inverse transform runs in registers and writes 4*T contiguous outputs.
-template <int T, bool F16, bool BWD, int BM, int WO>
-__global__ __launch_bounds__(256) void eql_gemm_kernel(const void* __restrict__ in,
-                                                       const void* __restrict__ wsp,
-                                                       const void* __restrict__ bias,
-                                                       void* __restrict__ out, int64_t N, int Ci,
-                                                       int Co, int Ci_pad, int Co_pad, int n_otiles,
-                                                       int n_tiles) {
-  using MM = Mma<F16>;
-  using Bn = Bins<T>;
-  using E = typename Elem<F16>::T;
-  constexpr int EB = Elem<F16>::bytes;
-  constexpr int KC = 64 / EB;        // contraction channels per chunk (32 f16, 16 f32)
-  constexpr int BO = 4 * WO;
-  constexpr int RT = BM / 16;
-  constexpr int OT = WO / 16;
-  constexpr int PC = BM * KC / 256;  // channels per thread in the prologue
-  constexpr int TPR = KC / PC;       // prologue threads per row
-  constexpr int IN_RUN = PC * T;
-  constexpr int OUT_RUN = 4 * T;
-  static_assert(BM % 16 == 0 && WO % 16 == 0 && PC >= 1 && KC % PC == 0, "tile shape");
-
-  __shared__ __attribute__((aligned(16))) char xs[T * BM * 64];
-
-  const int tile = xcd_tile(blockIdx.x, gridDim.x, n_tiles);
-  if (tile < 0) return;
-  const int rt_idx = tile / n_otiles;
-  const int ot_idx = tile - rt_idx * n_otiles;
-  const int64_t row0 = (int64_t)rt_idx * BM;
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int g = lane >> 4;
-  const int li = lane & 15;
-  const int o_wave = ot_idx * BO + wave * WO;
-
-  floatx4 acc[T][OT][RT];
-#pragma unroll
-  for (int p = 0; p < T; ++p)
-#pragma unroll
-    for (int a = 0; a < OT; ++a)
-#pragma unroll
-      for (int b = 0; b < RT; ++b) acc[p][a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  const int pr = tid / TPR;
-  const int pcg = tid - pr * TPR;
-  const int64_t prow = row0 + pr;
-  const bool row_ok = prow < N;
-  const bool in_vec = ((int64_t)Ci * T * EB) % run_vec_bytes<F16, IN_RUN>() == 0;
-
-  for (int k0 = 0; k0 < Ci; k0 += KC) {
-    // ---- prologue: load PC channels x T of one row, transform, stage planes in LDS
-    const int c0 = k0 + pcg * PC;
-    float v[IN_RUN];
-    if (row_ok && c0 + PC <= Ci) {
-      load_run<F16, IN_RUN>(in, (prow * Ci + c0) * T, in_vec, v);
-    } else if (row_ok && c0 < Ci) {
-      load_run_masked<F16, IN_RUN>(in, (prow * Ci + c0) * T, (Ci - c0) * T, v);
-    } else {
-#pragma unroll
-      for (int q = 0; q < IN_RUN; ++q) v[q] = 0.0f;
-    }
-    float P[T][PC];
-#pragma unroll
-    for (int q = 0; q < PC; ++q) {
-      float vin[T], vout[T];
-#pragma unroll
-      for (int t = 0; t < T; ++t) vin[t] = v[q * T + t];
-      rdft<T>(vin, vout);
-#pragma unroll
-      for (int p = 0; p < T; ++p) P[p][q] = vout[p];
-    }
-    __syncthreads();  // the previous chunk's fragment reads are complete
-#pragma unroll
-    for (int p = 0; p < T; ++p) pack_store_lds<F16, PC>(xs, p * BM * 64 + lds_off(pr, pcg * PC * EB), P[p]);
-    __syncthreads();
-
-    // ---- per-bin products on MFMA
-#pragma unroll
-    for (int a = 0; a < OT; ++a) {
-      const int o = o_wave + a * 16;
-      if (o >= Co) continue;  // wave-uniform: this sub-tile lies past the last channel
-      u32x4 A[T];
-      const char* wrow = reinterpret_cast<const char*>(wsp) +
-                         ((int64_t)(o + li) * Ci_pad + k0) * EB + g * 16;
-#pragma unroll
-      for (int p = 0; p < T; ++p)
-        A[p] = *reinterpret_cast<const u32x4*>(wrow + (int64_t)p * Co_pad * Ci_pad * EB);
-#pragma unroll
-      for (int b = 0; b < RT; ++b) {
-        u32x4 Bf[T];
-#pragma unroll
-        for (int p = 0; p < T; ++p)
-          Bf[p] = *reinterpret_cast<const u32x4*>(xs + p * BM * 64 + lds_off(b * 16 + li, g * 16));
-        MM::run(acc[0][a][b], A[0], Bf[0]);
-        if constexpr (Bn::kEven) MM::run(acc[1][a][b], A[1], Bf[1]);
-        static_for<Bn::K>([&](auto ki) {
-          constexpr int k = decltype(ki)::value + 1;
-          constexpr int r = Bn::re(k);
-          constexpr int i = Bn::im(k);
-          if constexpr (!BWD) {
-            MM::run(acc[r][a][b], A[r], Bf[r]);
-            MM::run(acc[r][a][b], MM::neg(A[i]), Bf[i]);
-            MM::run(acc[i][a][b], A[i], Bf[r]);
-            MM::run(acc[i][a][b], A[r], Bf[i]);
-          } else {
-            MM::run(acc[r][a][b], A[r], Bf[r]);
-            MM::run(acc[r][a][b], A[i], Bf[i]);
-            MM::run(acc[i][a][b], A[r], Bf[i]);
-            MM::run(acc[i][a][b], MM::neg(A[i]), Bf[r]);
-          }
-        });
-      }
-    }
-  }
-
-  // ---- epilogue: inverse transform (+ bias) in registers, one contiguous run per lane
-  const bool out_vec = ((int64_t)Co * T * EB) % run_vec_bytes<F16, OUT_RUN>() == 0;
-  const E* bp = reinterpret_cast<const E*>(bias);
-#pragma unroll
-  for (int a = 0; a < OT; ++a) {
-    const int o4 = o_wave + a * 16 + 4 * g;
-    if (o_wave + a * 16 >= Co) continue;
-#pragma unroll
-    for (int b = 0; b < RT; ++b) {
-      const int64_t n = row0 + b * 16 + li;
-      if (n >= N || o4 >= Co) continue;
-      float u[OUT_RUN];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float Pl[T], ul[T];
-#pragma unroll
-        for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][b][r];
-        irdft<T>(Pl, ul);
-        float bv = 0.0f;
-        if constexpr (!BWD) {
-          if (bp != nullptr && o4 + r < Co) bv = (float)bp[o4 + r];
-        }
-#pragma unroll
-        for (int t = 0; t < T; ++t) u[r * T + t] = ul[t] + bv;
-      }
-      const int nvalid = (Co - o4 >= 4 ? 4 : Co - o4) * T;
-      store_run<F16, OUT_RUN>(out, (n * Co + o4) * T, out_vec, nvalid, u);
-    }
   }
 }
 
@@ -389,10 +229,12 @@ __global__ __launch_bounds__(256) void eql_wgrad_kernel(const void* __restrict__
   }
 }
 
-// Fixed-order sum of S split partials for every (o, c), then the inverse
-// transform over the planes: dw[j,o,c] = (1/T) sum_k H_k[c,o] e^{+2 pi i k j/T}
-// with conjugate bins folded into weight 2 (the same inverse as the forward
-// epilogue).  Threads past Cout*Cin reduce the bias gradient.
+// Fixed-order sum of the S split partials, then the inverse transform over
+// the planes: dw[j,o,c] = (1/T) sum_k H_k[c,o] e^{+2 pi i k j/T}, conjugate bins
+// folded into weight 2 (the same inverse as the forward epilogue).  A
+// workgroup takes 256 consecutive (o, c) pairs: thread t sums plane p of pair
+// t for every p (coalesced over c), then transforms its pair.  The last
+// workgroup (when db is requested) sums the bias-gradient partials.
 template <int T, bool F16>
 __global__ __launch_bounds__(256) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
                                                                const float* __restrict__ dbpart,
@@ -401,28 +243,45 @@ __global__ __launch_bounds__(256) void eql_wgrad_reduce_kernel(const float* __re
                                                                int Cin, int Cout, int Cin_pad,
                                                                int Cout_pad) {
   using E = typename Elem<F16>::T;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t nw = (int64_t)Cout * Cin;
-  if (idx < nw) {
-    const int o = (int)(idx / Cin);
-    const int c = (int)(idx - (int64_t)o * Cin);
-    float P[T], u[T];
+  const int64_t pairs = (int64_t)Cout * Cin;
+  const int64_t nblk = (pairs + 255) / 256;
+  const int tid = threadIdx.x;
+  if ((int64_t)blockIdx.x == nblk) {  // bias gradient
+    if (db == nullptr) return;
+    for (int o = tid; o < Cout; o += 256) {
+      float s = 0.0f;
+      for (int sp = 0; sp < S; ++sp) s += dbpart[(int64_t)sp * Cout_pad + o];
+      reinterpret_cast<E*>(db)[o] = (E)s;
+    }
+    return;
+  }
+  const int64_t idx = (int64_t)blockIdx.x * 256 + tid;
+  if (idx >= pairs) return;
+  const int o = (int)(idx / Cin);
+  const int c = (int)(idx - (int64_t)o * Cin);
+  const int64_t split_stride = (int64_t)T * Cout_pad * Cin_pad;
+  const float* src = part + (int64_t)o * Cin_pad + c;
+  float P[T];
+#pragma unroll
+  for (int p = 0; p < T; ++p) P[p] = 0.0f;
+  int sp = 0;
+  for (; sp + 4 <= S; sp += 4) {
 #pragma unroll
     for (int p = 0; p < T; ++p) {
-      float s = 0.0f;
-      for (int sp = 0; sp < S; ++sp) s += part[(((int64_t)sp * T + p) * Cout_pad + o) * Cin_pad + c];
-      P[p] = s;
+      const float* q = src + (int64_t)p * Cout_pad * Cin_pad + sp * split_stride;
+      const float a0 = q[0], a1 = q[split_stride], a2 = q[2 * split_stride], a3 = q[3 * split_stride];
+      P[p] = (((P[p] + a0) + a1) + a2) + a3;
     }
-    irdft<T>(P, u);
-    E* d = reinterpret_cast<E*>(dw);
-#pragma unroll
-    for (int j = 0; j < T; ++j) d[((int64_t)j * Cout + o) * Cin + c] = (E)u[j];
-  } else if (db != nullptr && idx < nw + Cout) {
-    const int o = (int)(idx - nw);
-    float s = 0.0f;
-    for (int sp = 0; sp < S; ++sp) s += dbpart[(int64_t)sp * Cout_pad + o];
-    reinterpret_cast<E*>(db)[o] = (E)s;
   }
+  for (; sp < S; ++sp) {
+#pragma unroll
+    for (int p = 0; p < T; ++p) P[p] += src[(int64_t)p * Cout_pad * Cin_pad + sp * split_stride];
+  }
+  float u[T];
+  irdft<T>(P, u);
+  E* d = reinterpret_cast<E*>(dw);
+#pragma unroll
+  for (int j = 0; j < T; ++j) d[((int64_t)j * Cout + o) * Cin + c] = (E)u[j];
 }
 
 }  // namespace eqk

@@ -1,6 +1,7 @@
 // eql_launch_impl.h -- tile choice and launches for one element type.  Included
 // by exactly one instantiation unit per dtype (EQK_F16 = 0 or 1).
 #pragma once
+#include "eql_gemm.h"
 #include "eql_kernels.h"
 #include "eql_launch.h"
 
@@ -8,39 +9,73 @@ namespace eqk {
 
 template <int T, bool F16>
 hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s) {
-  const WspecDims d = wspec_dims(Cin, Cout);
-  const int64_t OD = d.CoF > d.CoutB ? d.CoF : d.CoutB;
-  const int64_t CD = d.CiF > d.CinB ? d.CiF : d.CinB;
-  const int64_t total = OD * CD;
+  const WspecDims d = wspec_dims(T, Cin, Cout, F16);
+  const int64_t total = (int64_t)d.CoF * d.CiF + (int64_t)d.CinB * d.CoutB;
   const unsigned blocks = (unsigned)((total + 255) / 256);
   hipLaunchKernelGGL((eql_wspec_kernel<T, F16>), dim3(blocks), dim3(256), 0, s, w, wspec, Cin,
                      Cout, d.CoF, d.CiF, d.CinB, d.CoutB);
   return hipGetLastError();
 }
 
-template <int T, bool F16, bool BWD, int BM, int WO>
+// Persistent grid: one workgroup per resident slot (CUs x occupancy), and no
+// workgroup with fewer than 16 rows.
+template <typename K>
+int persistent_grid(K kernel, int threads, int64_t N, int64_t row_bytes) {
+  static int occ_cache[64];
+  int dev = 0;
+  (void)hipGetDevice(&dev);
+  int occ = (dev >= 0 && dev < 64) ? occ_cache[dev] : 0;
+  if (occ <= 0) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, 0) != hipSuccess || occ <= 0) {
+      (void)hipGetLastError();
+      occ = 1;
+    }
+    if (dev >= 0 && dev < 64) occ_cache[dev] = occ;
+  }
+  const int64_t slots = (int64_t)device_cu_count() * occ;
+  const int64_t by_rows = (N + 31) / 32;  // at least 32 rows per workgroup
+  int64_t g = slots < by_rows ? slots : by_rows;
+  if (g < 1) g = 1;
+  // each workgroup addresses its rows (plus one round of slack) with 31-bit offsets
+  while ((N / g + 65) * row_bytes >= ((int64_t)1 << 31)) g *= 2;
+  return (int)g;
+}
+
+template <int T, bool F16, bool BWD, int OT, bool RES, int NKR>
 hipError_t gemm_variant(const GemmArgs& a) {
-  constexpr int BO = 4 * WO;
-  const int64_t n_rt = (a.N + BM - 1) / BM;
-  const int n_ot = (a.Co + BO - 1) / BO;
-  const int64_t n_tiles = n_rt * n_ot;
-  const int64_t grid = (n_tiles + 7) / 8 * 8;
-  hipLaunchKernelGGL((eql_gemm_kernel<T, F16, BWD, BM, WO>), dim3((unsigned)grid), dim3(256), 0,
-                     a.stream, a.in, a.wsp, a.bias, a.out, a.N, a.Ci, a.Co, a.Ci_pad, a.Co_pad,
-                     n_ot, (int)n_tiles);
+  auto k = eql_gemm_kernel<T, F16, BWD, OT, RES, NKR>;
+  const int grid = persistent_grid(k, 512, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
+  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(512), 0, a.stream, a.in, a.wsp, a.bias, a.out,
+                     a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
   return hipGetLastError();
 }
 
-// Accumulators per lane are T * (WO/16) * (BM/16) * 4 floats; the variants keep
-// that at or below 128 so they stay resident beside the operand fragments.
 template <int T, bool F16, bool BWD>
 hipError_t gemm_t(const GemmArgs& a) {
-  if constexpr (T <= 8) {
-    if (a.Co > 64) return gemm_variant<T, F16, BWD, 32, 32>(a);
-    return gemm_variant<T, F16, BWD, 64, 16>(a);
-  } else {
-    return gemm_variant<T, F16, BWD, 32, 16>(a);
+  constexpr int OTM = gemm_otmax_c(T, GemmShape<T, F16>::KW, F16 ? 2 : 4);
+  constexpr int OTR = OTM / 2 < 1 ? 1 : OTM / 2;
+  constexpr bool kResOk = T <= 8 && GemmShape<T, F16>::FB <= 16;
+  const GemmPlan& p = a.plan;
+  if (p.res) {
+    if constexpr (kResOk) {
+      if (p.OT != OTR) return hipErrorInvalidValue;
+      if (p.n_ks == 1) return gemm_variant<T, F16, BWD, OTR, true, 1>(a);
+      if (p.n_ks == 2) return gemm_variant<T, F16, BWD, OTR, true, 2>(a);
+      if (p.n_ks == 3) return gemm_variant<T, F16, BWD, OTR, true, 3>(a);
+    }
+    return hipErrorInvalidValue;
   }
+  if (p.OT == 1) return gemm_variant<T, F16, BWD, 1, false, 0>(a);
+  if constexpr (OTM >= 2) {
+    if (p.OT == 2) return gemm_variant<T, F16, BWD, 2, false, 0>(a);
+  }
+  if constexpr (OTM > 4) {
+    if (p.OT == 4) return gemm_variant<T, F16, BWD, 4, false, 0>(a);
+  }
+  if constexpr (OTM > 2) {
+    if (p.OT == OTM) return gemm_variant<T, F16, BWD, OTM, false, 0>(a);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int T, bool F16, int BC, int BO>
@@ -55,10 +90,11 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  const int64_t total = (int64_t)a.Cout * a.Cin + a.Cout;
-  hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3((unsigned)((total + 255) / 256)),
-                     dim3(256), 0, a.stream, a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout,
-                     p.Cin_pad, p.Cout_pad);
+  // one workgroup per 256 (o, c) pairs, plus one for the bias gradient
+  const int64_t pairs = (int64_t)a.Cout * a.Cin;
+  const unsigned blocks = (unsigned)((pairs + 255) / 256 + (a.db ? 1 : 0));
+  hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3(blocks), dim3(256), 0, a.stream,
+                     a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad);
   return hipGetLastError();
 }
 

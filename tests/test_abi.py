@@ -57,9 +57,9 @@ def test_status_strings(lib):
 
 
 def test_weight_spectrum_bytes(lib):
-    # T real planes, two padded layouts (rows to 128, columns to 32)
-    assert L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_F16) == 8 * (384 * 96 + 128 * 384) * 2
-    assert L.eqlinear_weight_spectrum_bytes(4, 16, 16, L.EQL_F32) == 4 * (128 * 32 * 2) * 4
+    # T real planes, two padded layouts (rows to whole output-channel chunks, columns to 32)
+    assert L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_F16) == 8 * (384 * 96 + 96 * 384) * 2
+    assert L.eqlinear_weight_spectrum_bytes(4, 16, 16, L.EQL_F32) == 4 * (32 * 32 * 2) * 4
     for bad in [(0, 4, 4, 0), (17, 4, 4, 0), (4, 0, 4, 0), (4, 4, 0, 0), (4, 4, 4, 2),
                 (4, 65537, 4, 0)]:
         assert L.eqlinear_weight_spectrum_bytes(*bad) == 0, bad
