@@ -12,29 +12,48 @@
 namespace eqk {
 
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+  // Variants (wave grid rows, c-tiles, o-tiles per wave) with at most 96
+  // accumulator floats per lane: CT * OTW * T * 4 <= 96.  Pick the one that
+  // transforms the fewest (row, channel) pairs per row of input:
+  // n_ct * n_ot * (BC + BO); ties go to fewer workgroup tiles.
+  static const int kVariants[][3] = {{2, 1, 1}, {2, 2, 1}, {2, 3, 1}, {2, 1, 2},
+                                     {2, 1, 3}, {4, 1, 1}, {4, 1, 2}, {4, 1, 3}};
   WgradPlan p{};
-  p.BC = p.BO = (T <= 8) ? 64 : 32;
+  long best = -1;
+  for (const auto& v : kVariants) {
+    const int wgc = v[0], ct = v[1], otw = v[2], wgo = 8 / wgc;
+    if (ct * otw * T * 4 > 96) continue;
+    const int BC = wgc * 16 * ct, BO = wgo * 16 * otw;
+    if ((long)T * (BC + BO) * 64 > 160 * 1024 - 4096) continue;
+    const int nct = (Cin + BC - 1) / BC, not_ = (Cout + BO - 1) / BO;
+    const long cost = (long)nct * not_ * (BC + BO) * 1024 + nct * not_;
+    if (best < 0 || cost < best) {
+      best = cost;
+      p.wgc = wgc; p.ct = ct; p.otw = otw; p.BC = BC; p.BO = BO; p.n_ct = nct; p.n_ot = not_;
+    }
+  }
   p.KR = f16 ? 32 : 16;
-  p.n_ct = (Cin + p.BC - 1) / p.BC;
-  p.n_ot = (Cout + p.BO - 1) / p.BO;
   p.Cin_pad = p.n_ct * p.BC;
   p.Cout_pad = p.n_ot * p.BO;
   if (N <= 0) {
     p.S = 0;
     p.rows_per_split = 0;
   } else {
-    // Aim for one workgroup per CU of a 256-CU device, but keep the fp32
-    // partials (written once, read once) under about 1/3 of the bytes of x
-    // and dy, and no split shorter than one row chunk.
+    // About one workgroup per CU of a 256-CU device, fp32 partials (written
+    // once, read once) at most the bytes of x and dy, at least two row chunks
+    // per split, and each split's rows addressable with 31 bits.
     const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
     int64_t s = (256 + tiles - 1) / tiles;
-    const double in_bytes = (double)N * (Cin + Cout) * T * (f16 ? 2 : 4);
+    const double eb = f16 ? 2.0 : 4.0;
+    const double in_bytes = (double)N * (Cin + Cout) * T * eb;
     const double part_per_split = (double)T * p.Cout_pad * p.Cin_pad * 4.0;
-    const int64_t s_budget = (int64_t)(in_bytes / 3.0 / (2.0 * part_per_split));
+    const int64_t s_budget = (int64_t)(in_bytes / (2.0 * part_per_split));
     if (s > s_budget) s = s_budget;
-    const int64_t max_s = (N + p.KR - 1) / p.KR;
+    const int64_t max_s = (N + 2 * p.KR - 1) / (2 * p.KR);
     if (s > max_s) s = max_s;
     if (s < 1) s = 1;
+    const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
+    while ((double)((N + s - 1) / s + p.KR) * row_bytes >= 2147483648.0) ++s;
     int64_t rows = (N + s - 1) / s;
     rows = (rows + p.KR - 1) / p.KR * p.KR;
     p.rows_per_split = rows;

@@ -78,10 +78,12 @@ inline WspecDims wspec_dims(int T, int Cin, int Cout, bool f16) {
 // Compute units of the current device (cached); 256 if unknown.
 int device_cu_count();
 
-// Plan of the split-row weight gradient: tile sizes, split count and the
-// padded partial extents.  Depends only on the problem, not on the device,
-// so results are reproducible across devices of the same model.
+// Plan of the split-row weight gradient: workgroup tile (a WGC x WGO wave grid
+// of CT x OTW tiles of 16 channels per wave), split count and the padded
+// partial extents.  Depends only on the problem, not on the device, so results
+// are reproducible across devices of the same model.
 struct WgradPlan {
+  int wgc, ct, otw; // variant: wave grid rows (WGO = 8 / wgc), tiles per wave
   int BC, BO;       // channel tile of one workgroup
   int KR;           // rows per chunk
   int n_ct, n_ot;   // channel tiles

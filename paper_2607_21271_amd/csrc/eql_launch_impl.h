@@ -3,6 +3,7 @@
 #pragma once
 #include "eql_gemm.h"
 #include "eql_kernels.h"
+#include "eql_wgrad.h"
 #include "eql_launch.h"
 
 namespace eqk {
@@ -78,21 +79,21 @@ hipError_t gemm_t(const GemmArgs& a) {
   return hipErrorInvalidValue;
 }
 
-template <int T, bool F16, int BC, int BO>
+template <int T, bool F16, int WGC, int CT, int OTW>
 hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
-  const int per = p.n_ct * p.n_ot;
   if (p.S > 0) {
-    const int64_t n_tiles = (int64_t)p.S * per;
-    const int64_t grid = (n_tiles + 7) / 8 * 8;
-    hipLaunchKernelGGL((eql_wgrad_kernel<T, F16, BC, BO>), dim3((unsigned)grid), dim3(256), 0,
-                       a.stream, a.x, a.dy, a.part, a.db ? a.dbpart : nullptr, a.N, a.Cin, a.Cout,
-                       p.rows_per_split, p.n_ct, p.n_ot, (int)n_tiles, p.Cin_pad, p.Cout_pad);
+    const int64_t n_tiles = (int64_t)p.S * p.n_ct * p.n_ot;
+    hipLaunchKernelGGL((eql_wgrad_kernel<T, F16, WGC, 8 / WGC, CT, OTW>), dim3((unsigned)n_tiles),
+                       dim3(512), 0, a.stream, a.x, a.dy, a.part, a.db ? a.dbpart : nullptr, a.N,
+                       a.Cin, a.Cout, p.rows_per_split, p.n_ct, p.n_ot, (int)n_tiles, p.Cin_pad,
+                       p.Cout_pad);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // one workgroup per 256 (o, c) pairs, plus one for the bias gradient
-  const int64_t pairs = (int64_t)a.Cout * a.Cin;
-  const unsigned blocks = (unsigned)((pairs + 255) / 256 + (a.db ? 1 : 0));
+  // one workgroup per 64/T (4-channel group, o) items, plus one for the bias gradient
+  constexpr int IPW = 64 / T > 0 ? 64 / T : 1;
+  const int64_t items = (int64_t)(p.Cin_pad / 4) * a.Cout;
+  const unsigned blocks = (unsigned)((items + IPW - 1) / IPW + (a.db ? 1 : 0));
   hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3(blocks), dim3(256), 0, a.stream,
                      a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad);
   return hipGetLastError();
@@ -100,14 +101,23 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
 
 template <int T, bool F16>
 hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
-  // The plan picks 64 x 64 tiles for T <= 8 and 32 x 32 above (see wgrad_plan).
-  if constexpr (T <= 8) {
-    if (p.BC != 64) return hipErrorInvalidValue;
-    return wgrad_variant<T, F16, 64, 64>(a, p);
-  } else {
-    if (p.BC != 32) return hipErrorInvalidValue;
-    return wgrad_variant<T, F16, 32, 32>(a, p);
+  // the variants of wgrad_plan whose accumulators fit (CT * OTW * T * 4 <= 96)
+#define EQK_WG(W_, C_, O_)                                                                    \
+  if constexpr ((C_) * (O_) * T * 4 <= 96 &&                                                 \
+                T * ((W_) * 16 * (C_) + (8 / (W_)) * 16 * (O_)) * 64 <= 160 * 1024 - 4096) {   \
+    if (p.wgc == (W_) && p.ct == (C_) && p.otw == (O_))                                      \
+      return wgrad_variant<T, F16, W_, C_, O_>(a, p);                                         \
   }
+  EQK_WG(2, 1, 1)
+  EQK_WG(2, 2, 1)
+  EQK_WG(2, 3, 1)
+  EQK_WG(2, 1, 2)
+  EQK_WG(2, 1, 3)
+  EQK_WG(4, 1, 1)
+  EQK_WG(4, 1, 2)
+  EQK_WG(4, 1, 3)
+#undef EQK_WG
+  return hipErrorInvalidValue;
 }
 
 #define EQK_T_SWITCH(T_, CALL)       \

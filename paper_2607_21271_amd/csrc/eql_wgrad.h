@@ -1,0 +1,348 @@
+// eql_wgrad.h -- weight- and bias-gradient kernels of the C_T equivariant
+// linear layer for gfx950.
+//
+//   H_k[c,o]  = sum_n conj(Xhat_k[n,c]) dYhat_k[n,o]          (one split of rows)
+//   dw[j,o,c] = (1/T) sum_{k=0}^{T-1} H_k[c,o] e^{+2 pi i k j/T}
+//   db[o]     = sum_n dYhat_0[n,o] = sum_n sum_t dy[n,o,t]
+// (the gradients with respect to the original parameters, Appendix A.2
+// "Forward and backward passes").  Complex bin (r, i):
+//   Re H += Xr Dr + Xi Di,   Im H += Xr Di + (-Xi) Dr.
+//
+// eql_wgrad_kernel: one workgroup of 8 waves (WGC x WGO grid) owns BC input x
+// BO output channels, all T planes, for one split of rows.  Per chunk of KR
+// rows the raw x and dy of the next chunk are loaded into registers while the
+// MFMAs of the current chunk run; every (row, channel) is transformed once
+// per workgroup and its planes staged in LDS with the row index contiguous
+// (the MFMA contraction index), so D[c][o] = sum_n A[c][n] B[n][o].  The fp32
+// partial goes to part[split][p][c/4][o][c%4] (each lane's four consecutive
+// c form one 16-byte run, and the 16 lanes of a quarter write 256 contiguous
+// bytes); tiles with ct == 0 also write the split's bias partial.
+//
+// eql_wgrad_reduce_kernel: fixed-order sum over splits, inverse transform over
+// the planes, dw (and db) in the output dtype.
+#pragma once
+#include "eql_common.h"
+#include "eql_gemm.h"
+
+namespace eqk {
+
+// The T elements of one (row, channel), EB bytes each, packed into words
+// (element e in half e%2 of word e/2 for 16-bit data).  vec is the widest
+// aligned load width that every row start allows.
+template <int T, int EB>
+__device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t rs, uint32_t off, int vec,
+                                         uint32_t (&w)[(T * EB + 3) / 4]) {
+  constexpr int NB = T * EB;
+  if constexpr (NB % 4 == 0) {
+    load_raw<NB>(rs, off, 0, vec, w);
+  } else {
+#pragma unroll
+    for (int q = 0; q < (NB + 3) / 4; ++q) {
+      const uint32_t lo = __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * q, 0, 0);
+      const uint32_t hi = (4 * q + 2 < NB) ? __builtin_amdgcn_raw_buffer_load_b16(rs, off + 4 * q + 2, 0, 0) : 0u;
+      w[q] = (lo & 0xffffu) | (hi << 16);
+    }
+  }
+}
+
+template <int T, bool F16, int WGC, int WGO, int CT, int OTW>
+__global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__ x,
+                                                        const void* __restrict__ dy,
+                                                        float* __restrict__ part,
+                                                        float* __restrict__ dbpart, int64_t N,
+                                                        int Cin, int Cout, int64_t rows_per_split,
+                                                        int n_ct, int n_ot, int n_tiles, int Cin_pad,
+                                                        int Cout_pad) {
+  using Bn = Bins<T>;
+  constexpr int EB = F16 ? 2 : 4;
+  constexpr int KW = F16 ? 8 : 4;            // rows per lane group per fragment
+  constexpr int KR = 4 * KW;                 // rows per chunk (one MFMA contraction step)
+  constexpr int FB = KW * EB;                // 16 bytes
+  constexpr int RB = KR * EB;                // 64 bytes: one channel's chunk of rows
+  using FR = Frag<FB>;
+  static_assert(WGC * WGO == 8, "8 waves");
+  constexpr int BC = WGC * 16 * CT;
+  constexpr int BO = WGO * 16 * OTW;
+  constexpr int NIX = BC * KR / 2;           // (channel, row pair) items of x per chunk
+  constexpr int NID = BO * KR / 2;
+  constexpr int UX = (NIX + 511) / 512;
+  constexpr int UD = (NID + 511) / 512;
+  constexpr int WPR = (T * EB + 3) / 4;      // words of one (row, channel)
+  constexpr int RAW = 2 * WPR;               // words of one item (two rows)
+
+  __shared__ __attribute__((aligned(16))) char xs[T * BC * RB];
+  __shared__ __attribute__((aligned(16))) char ds[T * BO * RB];
+  __shared__ float dred[512];
+
+  const int per_split = n_ct * n_ot;
+  const int split = blockIdx.x / per_split;
+  const int rem = blockIdx.x - split * per_split;
+  const int ct = rem / n_ot;
+  const int ot = rem - ct * n_ot;
+  const int64_t n_begin = (int64_t)split * rows_per_split;
+  const int64_t n_end = (n_begin + rows_per_split < N) ? n_begin + rows_per_split : N;
+  const int nchunks = (int)((n_end - n_begin + KR - 1) / KR);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int g = lane >> 4;
+  const int li = lane & 15;
+  const int wc = wave / WGO;
+  const int wo = wave - wc * WGO;
+
+  // rows of this split as buffer ranges: bytes past the split read as zero
+  const int rowx = Cin * T * EB, rowd = Cout * T * EB;
+  const __amdgpu_buffer_rsrc_t xrs =
+      make_rsrc(reinterpret_cast<const char*>(x) + n_begin * rowx, (uint32_t)((n_end - n_begin) * rowx));
+  const __amdgpu_buffer_rsrc_t drs =
+      make_rsrc(reinterpret_cast<const char*>(dy) + n_begin * rowd, (uint32_t)((n_end - n_begin) * rowd));
+  constexpr int ITB = T * EB;  // bytes of one (row, channel)
+  const int vx = (rowx % 16 == 0 && ITB % 16 == 0) ? 16 : (rowx % 8 == 0 && ITB % 8 == 0) ? 8
+               : (rowx % 4 == 0 && ITB % 4 == 0) ? 4 : 2;
+  const int vd = (rowd % 16 == 0 && ITB % 16 == 0) ? 16 : (rowd % 8 == 0 && ITB % 8 == 0) ? 8
+               : (rowd % 4 == 0 && ITB % 4 == 0) ? 4 : 2;
+
+  uint32_t rx[UX][RAW], rd[UD][RAW];
+  // item u of this thread: channel (item % B?), row pair (item / B?)
+  auto issue = [&](int chunk) {
+    const int n0 = chunk * KR;  // row offset within the split
+#pragma unroll
+    for (int u = 0; u < UX; ++u) {
+      const int item = tid + 512 * u;
+      const int c = item % BC, rp = item / BC;
+      const int cg = ct * BC + c;
+      if ((NIX % 512 == 0 || item < NIX) && cg < Cin) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          uint32_t w[WPR];
+          load_row<T, EB>(xrs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cin + cg) * ITB), vx, w);
+#pragma unroll
+          for (int q = 0; q < WPR; ++q) rx[u][h * WPR + q] = w[q];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < RAW; ++q) rx[u][q] = 0u;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UD; ++u) {
+      const int item = tid + 512 * u;
+      const int o = item % BO, rp = item / BO;
+      const int og = ot * BO + o;
+      if ((NID % 512 == 0 || item < NID) && og < Cout) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          uint32_t w[WPR];
+          load_row<T, EB>(drs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cout + og) * ITB), vd, w);
+#pragma unroll
+          for (int q = 0; q < WPR; ++q) rd[u][h * WPR + q] = w[q];
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < RAW; ++q) rd[u][q] = 0u;
+      }
+    }
+  };
+
+  float dbacc[UD];
+#pragma unroll
+  for (int u = 0; u < UD; ++u) dbacc[u] = 0.0f;
+
+  // transform the prefetched items and stage their planes (two rows each)
+  auto publish = [&]() {
+#pragma unroll
+    for (int u = 0; u < UX; ++u) {
+      const int item = tid + 512 * u;
+      if (NIX % 512 != 0 && item >= NIX) continue;
+      const int c = item % BC, rp = item / BC;
+      float P0[T], P1[T];
+      {
+        float v[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rx[u], t);
+        rdft<T>(v, P0);
+#pragma unroll
+        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rx[u] + WPR, t);
+        rdft<T>(v, P1);
+      }
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        char* dst = &xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)];
+        if constexpr (F16) *reinterpret_cast<uint32_t*>(dst) = pack2<true>(P0[p], P1[p]);
+        else *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UD; ++u) {
+      const int item = tid + 512 * u;
+      if (NID % 512 != 0 && item >= NID) continue;
+      const int o = item % BO, rp = item / BO;
+      float P0[T], P1[T];
+      {
+        float v[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rd[u], t);
+        rdft<T>(v, P0);
+#pragma unroll
+        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rd[u] + WPR, t);
+        rdft<T>(v, P1);
+      }
+      dbacc[u] += P0[0] + P1[0];
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        char* dst = &ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)];
+        if constexpr (F16) *reinterpret_cast<uint32_t*>(dst) = pack2<true>(P0[p], P1[p]);
+        else *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
+      }
+    }
+  };
+
+  floatx4 acc[T][CT][OTW];
+#pragma unroll
+  for (int p = 0; p < T; ++p)
+#pragma unroll
+    for (int a = 0; a < CT; ++a)
+#pragma unroll
+      for (int b = 0; b < OTW; ++b) acc[p][a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+  auto mma_chunk = [&]() {
+#pragma unroll
+    for (int b = 0; b < OTW; ++b) {
+      const int ol = (wo * OTW + b) * 16 + li;
+      FR Bf[T];
+#pragma unroll
+      for (int p = 0; p < T; ++p) Bf[p] = lds_frag<FB, RB>(&ds[p * BO * RB], ol, g);
+#pragma unroll
+      for (int a = 0; a < CT; ++a) {
+        const int cl = (wc * CT + a) * 16 + li;
+        FR A[T];
+#pragma unroll
+        for (int p = 0; p < T; ++p) A[p] = lds_frag<FB, RB>(&xs[p * BC * RB], cl, g);
+        frag_mma<F16, KW>(acc[0][a][b], A[0], Bf[0]);
+        if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a][b], A[1], Bf[1]);
+        static_for<Bn::K>([&](auto ki) {
+          constexpr int k = decltype(ki)::value + 1;
+          constexpr int r = Bn::re(k);
+          constexpr int i = Bn::im(k);
+          frag_mma<F16, KW>(acc[r][a][b], A[r], Bf[r]);
+          frag_mma<F16, KW>(acc[i][a][b], A[r], Bf[i]);
+          frag_mma<F16, KW>(acc[r][a][b], A[i], Bf[i]);
+          frag_mma<F16, KW>(acc[i][a][b], frag_neg<F16, FB>(A[i]), Bf[r]);
+        });
+      }
+    }
+  };
+
+  if (nchunks > 0) issue(0);
+  for (int ch = 0; ch < nchunks; ++ch) {
+    publish();
+    __syncthreads();                       // spectra of chunk ch visible
+    if (ch + 1 < nchunks) issue(ch + 1);   // in flight during the MFMAs
+    mma_chunk();
+    __syncthreads();                       // xs / ds free for the next chunk
+  }
+
+  // ---- partials: part[split][p][c/4][o][c%4]
+  const int CQ = Cin_pad / 4;
+#pragma unroll
+  for (int a = 0; a < CT; ++a) {
+    const int cq = (ct * BC + (wc * CT + a) * 16) / 4 + g;
+#pragma unroll
+    for (int b = 0; b < OTW; ++b) {
+      const int oo = ot * BO + (wo * OTW + b) * 16 + li;
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        float* dst = part + ((((int64_t)split * T + p) * CQ + cq) * Cout_pad + oo) * 4;
+        *reinterpret_cast<floatx4*>(dst) = acc[p][a][b];
+      }
+    }
+  }
+  if (ct == 0 && dbpart != nullptr) {
+    // threads with the same o (item % BO) hold partial sums of different rows
+#pragma unroll
+    for (int u = 0; u < UD; ++u) {
+      __syncthreads();
+      dred[tid] = dbacc[u];
+      __syncthreads();
+      if (tid < BO && (NID % 512 == 0 || tid + 512 * u < NID)) {
+        float s = 0.0f;
+        for (int q = tid; q < 512; q += BO)
+          if (NID % 512 == 0 || q + 512 * u < NID) s += dred[q];
+        const int o = (tid + 512 * u) % BO;
+        if (u == 0) dbpart[(int64_t)split * Cout_pad + ot * BO + o] = s;
+        else dbpart[(int64_t)split * Cout_pad + ot * BO + o] += s;
+      }
+    }
+  }
+}
+
+// Fixed-order sum of the S split partials, then the inverse transform over
+// the planes (the same inverse as the forward epilogue).  An item is one
+// 16-byte run of the partial layout: four consecutive input channels of one
+// output channel.  A workgroup takes IPW = 64/T items x T planes = 64 slots and
+// splits the splits four ways: thread (q, e) sums splits q, q+4, ... of slot e,
+// the four group sums are added in a fixed order through LDS, and one thread
+// per (item, channel) transforms the planes and writes dw.  The extra last
+// workgroup sums the bias-gradient partials.
+template <int T, bool F16>
+__global__ __launch_bounds__(256) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
+                                                               const float* __restrict__ dbpart,
+                                                               void* __restrict__ dw,
+                                                               void* __restrict__ db, int S,
+                                                               int Cin, int Cout, int Cin_pad,
+                                                               int Cout_pad) {
+  using E = typename Elem<F16>::T;
+  constexpr int IPW = 64 / T > 0 ? 64 / T : 1;  // items per workgroup
+  constexpr int SLOTS = IPW * T;
+  __shared__ floatx4 red[4][64];
+  const int CQ = Cin_pad / 4;
+  const int64_t items = (int64_t)CQ * Cout;
+  const int64_t nblk = (items + IPW - 1) / IPW;
+  const int tid = threadIdx.x;
+  if ((int64_t)blockIdx.x == nblk) {  // bias gradient
+    if (db == nullptr) return;
+    for (int o = tid; o < Cout; o += 256) {
+      float s = 0.0f;
+      for (int sp = 0; sp < S; ++sp) s += dbpart[(int64_t)sp * Cout_pad + o];
+      reinterpret_cast<E*>(db)[o] = (E)s;
+    }
+    return;
+  }
+  const int q = tid >> 6;     // split group
+  const int e = tid & 63;     // slot: item e / T, plane e % T
+  const int64_t plane_stride = (int64_t)CQ * Cout_pad * 4;
+  const int64_t split_stride = (int64_t)T * plane_stride;
+  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+  const int64_t item = (int64_t)blockIdx.x * IPW + e / T;
+  if (e < SLOTS && item < items) {
+    const int cq = (int)(item / Cout);
+    const int o = (int)(item - (int64_t)cq * Cout);
+    const float* src = part + (e % T) * plane_stride + ((int64_t)cq * Cout_pad + o) * 4;
+    for (int sp = q; sp < S; sp += 4) acc += *reinterpret_cast<const floatx4*>(src + sp * split_stride);
+  }
+  red[q][e] = acc;
+  __syncthreads();
+  if (tid < SLOTS) red[0][tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+  __syncthreads();
+  if (tid < IPW * 4) {
+    const int il = tid >> 2, ce = tid & 3;
+    const int64_t it = (int64_t)blockIdx.x * IPW + il;
+    if (it < items) {
+      const int cq = (int)(it / Cout);
+      const int o = (int)(it - (int64_t)cq * Cout);
+      const int c = cq * 4 + ce;
+      if (c < Cin) {
+        float Pl[T], u[T];
+#pragma unroll
+        for (int p = 0; p < T; ++p) Pl[p] = red[0][il * T + p][ce];
+        irdft<T>(Pl, u);
+        E* d = reinterpret_cast<E*>(dw);
+#pragma unroll
+        for (int j = 0; j < T; ++j) d[((int64_t)j * Cout + o) * Cin + c] = (E)u[j];
+      }
+    }
+  }
+}
+
+}  // namespace eqk
