@@ -1,7 +1,9 @@
 """Build libeqlinear.so (gfx950) in-tree with hipcc.
 
 Each translation unit is compiled in its own hipcc process (in parallel), then
-linked into ``paper_2607_21271_amd/libeqlinear.so``.  Always rebuilds.
+linked into ``paper_2607_21271_amd/libeqlinear.so``.  Always rebuilds.  The
+device assembly is kept (-save-temps) and scanned by isa_check before the
+library is installed; a finding fails the build.
 Usage: ``python -m paper_2607_21271_amd.build`` or ``build()``.
 """
 from __future__ import annotations
@@ -33,18 +35,22 @@ COMMON_FLAGS = ["-O3", "-std=c++20", "-fPIC", "-Wall", "-Wno-unused-function",
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON_FLAGS, *lang, "-c", os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON_FLAGS, "-save-temps", *lang, "-c", os.path.join(CSRC, src),
+           "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD_DIR)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr[-20000:]))
     return obj
 
 
 def build(verbose: bool = True) -> str:
+    shutil.rmtree(BUILD_DIR, ignore_errors=True)
     os.makedirs(BUILD_DIR, exist_ok=True)
     jobs = min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4)))
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
         objs = list(ex.map(_compile, SOURCES))
+    from . import isa_check
+    isa_check.check_build(BUILD_DIR)
     tmp = OUT + ".tmp%d" % os.getpid()
     cmd = [HIPCC, *DEVICE_FLAGS, "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

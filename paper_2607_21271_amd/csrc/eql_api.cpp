@@ -2,6 +2,7 @@
 // device checks, workspace planning and dispatch to the gfx950 kernels.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <mutex>
@@ -142,6 +143,11 @@ int launched(hipError_t e) { return e == hipSuccess ? EQL_OK : EQL_ERR_LAUNCH; }
 }  // namespace
 
 namespace eqk {
+// Read on every plan so that tests can switch it within one process.
+int gemm_forced_mode() {
+  const char* v = getenv("EQL_GEMM_MODE");
+  return (v != nullptr && v[0] >= '0' && v[0] <= '2' && v[1] == 0) ? v[0] - '0' : -1;
+}
 // Valid after check_device() succeeded on the current device.
 int device_cu_count() {
   int dev = 0;

@@ -67,12 +67,12 @@ struct Bins {
 };
 
 template <typename F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+__host__ __device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
   (f(std::integral_constant<int, I>{}), ...);
 }
 // f(integral_constant<int, i>) for i = 0..N-1, fully unrolled at compile time.
 template <int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
+__host__ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
@@ -350,106 +350,42 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// One MFMA operand fragment is 16 bytes per lane: 8 fp16 values (one
-// v_mfma_f32_16x16x32_f16 K-slice of 32) or 4 fp32 values (four
-// v_mfma_f32_16x16x4_f32 K-slices of 4).  Lane l = 16*g + i holds row/column i
-// and the g-th 16-byte group of the contraction index; A and B use the same
-// group-to-index map, so the contraction covers each index exactly once.
-template <bool F16>
-struct Mma;
-
-template <>
-struct Mma<true> {
-  static constexpr int kPerFrag = 8;  // contraction elements per lane fragment
-  static constexpr int kPerTile = 32; // contraction elements per 4 lane groups
-  static __device__ __forceinline__ void run(floatx4& acc, u32x4 a, u32x4 b) {
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, a),
-                                                 __builtin_bit_cast(half8, b), acc, 0, 0, 0);
+// Raw words -> floats (fp16: two elements per word, low half first; fp32:
+// one).  Each fp16 word is read exactly once, by one asm statement that
+// converts both halves.  (With the halves read by separate instructions the
+// compiler, in some kernels, reused a word's register after its first read
+// and the second read then saw the converted value.)
+__device__ __forceinline__ void f16x2_to_f32(uint32_t w, float& lo, float& hi) {
+  asm("v_cvt_f32_f16_e32 %0, %2\n\t"
+      "v_cvt_f32_f16_sdwa %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:WORD_1"
+      : "=&v"(lo), "=v"(hi)
+      : "v"(w));
+}
+template <bool F16, int NW>
+__device__ __forceinline__ void raw_to_floats(const uint32_t* r, float (&f)[F16 ? 2 * NW : NW]) {
+#pragma unroll
+  for (int v = 0; v < NW; ++v) {
+    if constexpr (F16) f16x2_to_f32(r[v], f[2 * v], f[2 * v + 1]);
+    else f[v] = __builtin_bit_cast(float, r[v]);
   }
-  static __device__ __forceinline__ u32x4 neg(u32x4 a) { return a ^ 0x80008000u; }
-};
-
-template <>
-struct Mma<false> {
-  static constexpr int kPerFrag = 4;
-  static constexpr int kPerTile = 16;
-  static __device__ __forceinline__ void run(floatx4& acc, u32x4 a, u32x4 b) {
-    const floatx4 af = __builtin_bit_cast(floatx4, a);
-    const floatx4 bf = __builtin_bit_cast(floatx4, b);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[0], bf[0], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[1], bf[1], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[2], bf[2], acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(af[3], bf[3], acc, 0, 0, 0);
-  }
-  static __device__ __forceinline__ u32x4 neg(u32x4 a) { return a ^ 0x80000000u; }
-};
-
-// LDS tiles are rows of 64 bytes (four 16-byte chunks); chunk c of row r is
-// stored at chunk c ^ ((r >> 1) & 3), which spreads the 16 rows read by one
-// fragment load over all banks.
-__device__ __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 3); }
-__device__ __forceinline__ int lds_off(int row, int byte_in_row) {
-  return row * 64 + (swz(row, byte_in_row >> 4) << 4) + (byte_in_row & 15);
 }
 
-// Widest power-of-two byte width (<= 16) dividing a run of L elements.
-template <bool F16, int L>
-constexpr int run_vec_bytes() {
-  constexpr int NB = L * Elem<F16>::bytes;
-  return (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
+// Two floats rounded to fp16 (round to nearest even) and packed, a in the low half.
+template <bool F16>
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  if constexpr (F16) {
+    const uint16_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
+    const uint16_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
+    return (uint32_t)lo | ((uint32_t)hi << 16);
+  } else {
+    return __builtin_bit_cast(uint32_t, a);
+  }
 }
 
 // ---------------------------------------------------------------------------
-// Contiguous loads / stores of L elements at an element offset.  VEC is the
-// widest power-of-two byte width (<= 16) that divides L * elem bytes; the
-// caller states whether the start is VEC-aligned.  Loads convert to float.
-template <bool F16, int L>
-__device__ __forceinline__ void load_run(const void* base, int64_t elem_off, bool vec_ok,
-                                         float (&out)[L]) {
-  using E = typename Elem<F16>::T;
-  constexpr int NB = L * Elem<F16>::bytes;
-  constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
-  const E* p = reinterpret_cast<const E*>(base) + elem_off;
-  if (vec_ok && VEC >= 4) {
-    constexpr int PER = VEC / Elem<F16>::bytes;
-#pragma unroll
-    for (int v = 0; v < L / PER; ++v) {
-      if constexpr (VEC == 16) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(p + v * PER);
-        E tmp[PER];
-        __builtin_memcpy(tmp, &w, 16);
-#pragma unroll
-        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
-      } else if constexpr (VEC == 8) {
-        const u32x2 w = *reinterpret_cast<const u32x2*>(p + v * PER);
-        E tmp[PER];
-        __builtin_memcpy(tmp, &w, 8);
-#pragma unroll
-        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
-      } else {
-        const uint32_t w = *reinterpret_cast<const uint32_t*>(p + v * PER);
-        E tmp[PER];
-        __builtin_memcpy(tmp, &w, 4);
-#pragma unroll
-        for (int q = 0; q < PER; ++q) out[v * PER + q] = (float)tmp[q];
-      }
-    }
-  } else {
-#pragma unroll
-    for (int q = 0; q < L; ++q) out[q] = (float)p[q];
-  }
-}
-
-// Same as load_run, but only the first n_valid elements are read; the rest are zero.
-template <bool F16, int L>
-__device__ __forceinline__ void load_run_masked(const void* base, int64_t elem_off, int n_valid,
-                                                float (&out)[L]) {
-  using E = typename Elem<F16>::T;
-  const E* p = reinterpret_cast<const E*>(base) + elem_off;
-#pragma unroll
-  for (int q = 0; q < L; ++q) out[q] = (q < n_valid) ? (float)p[q] : 0.0f;
-}
-
+// Contiguous store of L elements at an element offset, converting from float.
+// VEC is the widest power-of-two byte width (<= 16) that divides L * elem
+// bytes; the caller states whether the start is VEC-aligned.
 template <bool F16, int L>
 __device__ __forceinline__ void store_run(void* base, int64_t elem_off, bool vec_ok, int n_valid,
                                           const float (&v)[L]) {
@@ -483,42 +419,6 @@ __device__ __forceinline__ void store_run(void* base, int64_t elem_off, bool vec
     for (int q = 0; q < L; ++q)
       if (q < n_valid) p[q] = (E)v[q];
   }
-}
-
-// Pack PC consecutive float values into PC elements of type E in a byte buffer.
-template <bool F16, int PC>
-__device__ __forceinline__ void pack_store_lds(char* lds, int off, const float (&v)[PC]) {
-  using E = typename Elem<F16>::T;
-  constexpr int NB = PC * Elem<F16>::bytes;
-  E tmp[PC];
-#pragma unroll
-  for (int q = 0; q < PC; ++q) tmp[q] = (E)v[q];
-  if constexpr (NB == 16) {
-    u32x4 w;
-    __builtin_memcpy(&w, tmp, 16);
-    *reinterpret_cast<u32x4*>(lds + off) = w;
-  } else if constexpr (NB == 8) {
-    u32x2 w;
-    __builtin_memcpy(&w, tmp, 8);
-    *reinterpret_cast<u32x2*>(lds + off) = w;
-  } else if constexpr (NB == 4) {
-    uint32_t w;
-    __builtin_memcpy(&w, tmp, 4);
-    *reinterpret_cast<uint32_t*>(lds + off) = w;
-  } else {
-    __builtin_memcpy(lds + off, tmp, NB);
-  }
-}
-
-// Workgroup-id remap for the 8 XCDs of MI355X: the hardware deals consecutive
-// workgroup ids round-robin to XCDs, so id b runs on XCD b % 8.  Returning
-// tile = (b % 8) * per + b / 8 gives every XCD a contiguous range of tiles,
-// which keeps tiles that share operand rows in one L2.  `grid` must be a
-// multiple of 8; ids past `n_tiles` return -1.
-__device__ __forceinline__ int xcd_tile(int b, int grid, int n_tiles) {
-  const int per = grid >> 3;
-  const int t = (b & 7) * per + (b >> 3);
-  return t < n_tiles ? t : -1;
 }
 
 }  // namespace eqk

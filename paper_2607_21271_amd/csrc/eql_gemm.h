@@ -4,27 +4,27 @@
 //
 // Work split.  The grid is persistent: workgroup w owns rows
 // [w*N/G, (w+1)*N/G), so every CU streams the same number of rows.  A
-// workgroup is 4 waves; its rows are dealt out in rounds of 64, row q of a
-// round going to wave q % 4, lane-row q / 4, so the waves of a workgroup get
-// equal shares even when the workgroup holds fewer than 64 rows.
+// workgroup is 8 waves in 4 pairs; its rows are dealt out in rounds of 64, row
+// q of a round going to pair q % 4, tile row q / 4.  The two waves of a pair
+// share those 16 rows and split every o-chunk between them.
 //
-// Activations never pass through LDS.  Lane (g, i) of a wave loads, for its
-// row i, the KW consecutive channels of quarter g of the contraction step,
-// all T group positions of each (KW*T contiguous elements), transforms them in
-// registers and packs the result straight into the MFMA B operand (row i,
-// contraction elements of group g) of every spectral plane.  Each activation
-// element is loaded and transformed once per o-chunk (once in total when the
-// spectrum stays resident, RES).
+// Activations.  Per contraction step each lane loads, for one row, HKW
+// channels with all T group positions (HKW*T contiguous elements), transforms
+// them in registers and writes their T planes to the pair's spectrum buffer in
+// LDS (double buffered); both waves then read complete MFMA operands from it.
+// With RES the spectrum of all contraction steps stays in registers across
+// o-chunks, so each activation is loaded and transformed once.
 //
-// Weight planes stream through LDS: per step a block of T planes x OC output
-// channels x KSTEP contraction channels is prefetched into registers, written
-// to the idle half of a double buffer and read as MFMA A operands by all four
-// waves; one barrier per step.
+// Weights.  Per step a block of T planes x OC output channels x KSTEP
+// contraction channels is prefetched into registers, written to the idle half
+// of a double buffer in LDS and read as MFMA operands by all eight waves.  One
+// barrier per step orders both exchanges.
 //
-// MFMA computes D[o][n] = sum_k A[o][k] B[k][n]; each lane ends with 4
-// consecutive output channels of one row for every plane, so the inverse
-// transform and bias run in registers and each lane writes 4*T contiguous
-// outputs.
+// MFMA computes D[n][o] = sum_c X[n][c] W[o][c] (activation spectrum as the
+// row operand); each lane ends with one output channel of 4 rows for every
+// plane, so the inverse transform and bias run in registers, and the 16 lanes
+// of a lane group store 16 consecutive channels (16*T contiguous elements) of
+// one row.
 #pragma once
 #include "eql_common.h"
 
@@ -39,7 +39,10 @@ struct GemmShape {
   static constexpr int KSTEP = 4 * KW;  // contraction channels per step (4 lane groups)
   static constexpr int FB = KW * EB;    // operand fragment bytes per lane
   static constexpr int RB = 4 * FB;     // bytes of one weight row per step
-  static constexpr int NBX = KW * T * EB;  // raw activation bytes per lane per step
+  static constexpr int NBH = KW / 2 * T * EB;  // raw activation bytes per lane per step
+  // widest load (<= 16 bytes) dividing a lane's run; valid when the row stride
+  // Ci*T*EB is a multiple of it, else the narrow kernel loads single elements
+  static constexpr int WV = NBH % 16 == 0 ? 16 : NBH % 8 == 0 ? 8 : 4;
 };
 
 template <int FB>
@@ -110,26 +113,30 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
-// Raw activation bytes of one lane for one step: NB bytes at byte offset off
-// of the resource.  vec is the widest load width (16, 8, 4) every row start
-// allows, 2 for 16-bit loads.  Elements past nvalid (a ragged last channel
-// group) are zeroed; bytes past the resource read as zero.
-template <int NB>
-__device__ __forceinline__ void load_raw(__amdgpu_buffer_rsrc_t rs, uint32_t off, int soff, int vec,
+// Raw bytes of one lane for one step: NB bytes at byte offset off (+ soff) of
+// the resource, with loads of W bytes (W = 2: 16-bit loads paired into words).
+// The width is a compile-time constant so that every kernel has a single load
+// shape: with the width chosen at run time among several load shapes feeding
+// the same registers, the register allocator in this toolchain produced code
+// that overwrote live raw words in some kernels.  Bytes past the resource
+// read as zero.
+template <int NB, int W>
+__device__ __forceinline__ void load_raw(__amdgpu_buffer_rsrc_t rs, uint32_t off, int soff,
                                          uint32_t (&r)[NB / 4]) {
-  if (vec == 16 && NB % 16 == 0) {
+  static_assert(NB % W == 0 && NB % 4 == 0, "load width");
+  if constexpr (W == 16) {
 #pragma unroll
     for (int v = 0; v < NB / 16; ++v) {
       const u32x4 x = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, off + 16 * v, soff, 0));
       r[4 * v] = x[0]; r[4 * v + 1] = x[1]; r[4 * v + 2] = x[2]; r[4 * v + 3] = x[3];
     }
-  } else if (vec >= 8 && NB % 8 == 0) {
+  } else if constexpr (W == 8) {
 #pragma unroll
     for (int v = 0; v < NB / 8; ++v) {
       const u32x2 x = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(rs, off + 8 * v, soff, 0));
       r[2 * v] = x[0]; r[2 * v + 1] = x[1];
     }
-  } else if (vec >= 4) {
+  } else if constexpr (W == 4) {
 #pragma unroll
     for (int v = 0; v < NB / 4; ++v) r[v] = __builtin_amdgcn_raw_buffer_load_b32(rs, off + 4 * v, soff, 0);
   } else {
@@ -156,88 +163,54 @@ __device__ __forceinline__ void mask_raw(int nvalid_elems, uint32_t (&r)[NB / 4]
   }
 }
 
-template <bool F16>
-__device__ __forceinline__ float raw_elem(const uint32_t* r, int e) {
-  if constexpr (F16) {
-    const uint32_t w = r[e >> 1];
-    const uint16_t h = (e & 1) ? (uint16_t)(w >> 16) : (uint16_t)(w & 0xffffu);
-    return (float)__builtin_bit_cast(_Float16, h);
-  } else {
-    return __builtin_bit_cast(float, r[e]);
-  }
-}
-
-template <bool F16>
-__device__ __forceinline__ uint32_t pack2(float a, float b) {
-  if constexpr (F16) {
-    const uint16_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
-    const uint16_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
-    return (uint32_t)lo | ((uint32_t)hi << 16);
-  } else {
-    return __builtin_bit_cast(uint32_t, a);
-  }
-}
-
-// Transform the KW channels held raw by one lane into T operand fragments.
-template <int T, bool F16>
-__device__ __forceinline__ void raw_to_frags(const uint32_t (&r)[GemmShape<T, F16>::NBX / 4],
-                                             Frag<GemmShape<T, F16>::FB> (&B)[T]) {
-  using S = GemmShape<T, F16>;
-  constexpr int KW = S::KW;
-  if constexpr (F16) {
-#pragma unroll
-    for (int j = 0; j < KW; j += 2) {
-      float v0[T], v1[T], P0[T], P1[T];
-#pragma unroll
-      for (int t = 0; t < T; ++t) {
-        v0[t] = raw_elem<true>(r, j * T + t);
-        v1[t] = raw_elem<true>(r, (j + 1) * T + t);
-      }
-      rdft<T>(v0, P0);
-      rdft<T>(v1, P1);
-#pragma unroll
-      for (int p = 0; p < T; ++p) B[p].w[j >> 1] = pack2<true>(P0[p], P1[p]);
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < KW; ++j) {
-      float v[T], P[T];
-#pragma unroll
-      for (int t = 0; t < T; ++t) v[t] = raw_elem<false>(r, j * T + t);
-      rdft<T>(v, P);
-#pragma unroll
-      for (int p = 0; p < T; ++p) B[p].w[j] = __builtin_bit_cast(uint32_t, P[p]);
-    }
-  }
-}
-
 // Transform the HKW channels held raw by one lane; P[p][j] is plane p of channel j.
 template <int T, bool F16, int HKW>
 __device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (F16 ? 2 : 4) / 4],
                                               float (&P)[T][HKW]) {
+  constexpr int NW = HKW * T * (F16 ? 2 : 4) / 4;
+  float f[F16 ? 2 * NW : NW];
+  raw_to_floats<F16, NW>(r, f);
 #pragma unroll
   for (int j = 0; j < HKW; ++j) {
     float v[T], q[T];
 #pragma unroll
-    for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(r, j * T + t);
+    for (int t = 0; t < T; ++t) v[t] = f[j * T + t];
     rdft<T>(v, q);
 #pragma unroll
     for (int p = 0; p < T; ++p) P[p][j] = q[p];
   }
 }
 
+// How the weight blocks reach LDS (MODE):
+//   kStream  two block buffers; the block of the next step is prefetched into
+//            registers while the current one feeds the MFMAs
+//   kRes     as kStream, and each wave's operand spectrum of all NKR
+//            contraction steps stays in registers across o-chunks
+//            (requires ceil(Ci / KSTEP) == NKR)
+//   kStat    every block of the layer is loaded into LDS once per workgroup;
+//            inside the row loop only activations move
+enum GemmMode { kStream = 0, kRes = 1, kStat = 2 };
+
+// LDS arena of one workgroup: two spectrum buffers, then the weight blocks.
+template <int T, bool F16, int OT>
+struct GemmLds {
+  static constexpr int RB = GemmShape<T, F16>::RB;
+  static constexpr int XBLK = 4 * T * 16 * RB;  // 4 row groups x T planes x 16 rows
+  static constexpr int WBLK = T * 32 * OT * RB; // T planes x OC channels
+  static constexpr int bytes(int n_wblocks) { return 2 * XBLK + n_wblocks * WBLK; }
+};
+
 // Kernel parameters: the workgroup is 8 waves, wave w = 2*rg + oh.  Waves rg
 // own rows; the pair (rg, 0), (rg, 1) shares 16 rows and splits each o-chunk:
 // wave oh computes OT output tiles of 16, so an o-chunk holds OC = 32*OT
-// channels.  RES keeps each wave's operand spectrum of all NKR contraction
-// steps in registers across o-chunks (requires ceil(Ci / KSTEP) == NKR).
+// channels.
 //
 // Per contraction step a lane of wave oh transforms HKW = KW/2 channels of its
 // row and writes their planes to the pair's spectrum buffer in LDS; after a
 // barrier both waves read complete MFMA operands from it.  Weight blocks are
 // double buffered in LDS: the next block is loaded into registers while the
 // current one feeds the MFMAs, then written to the idle buffer.
-template <int T, bool F16, bool BWD, int OT, bool RES, int NKR>
+template <int T, bool F16, bool BWD, int OT, int MODE, int NKR, bool NARROW>
 __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ in,
                                                        const void* __restrict__ wsp,
                                                        const void* __restrict__ bias,
@@ -254,16 +227,19 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   constexpr int KSTEP = S::KSTEP;
   constexpr int FB = S::FB;
   constexpr int RB = S::RB;             // bytes of one row (weights or spectrum) per step
-  constexpr int NBH = HKW * T * EB;     // raw activation bytes per lane per step
+  constexpr int NBH = S::NBH;           // raw activation bytes per lane per step
   constexpr int OC = 32 * OT;
-  constexpr int WBLK = T * OC * RB;     // bytes of one weight block
+  constexpr bool RES = MODE == kRes;
+  constexpr int WBLK = GemmLds<T, F16, OT>::WBLK;  // bytes of one weight block
   constexpr int NU = WBLK / 16;         // 16-byte units per block
   constexpr int UPT = (NU + 511) / 512; // weight units per thread
-  constexpr int XBLK = 4 * T * 16 * RB; // spectrum buffer: 4 row groups x T planes x 16 rows
+  constexpr int XBLK = GemmLds<T, F16, OT>::XBLK;  // bytes of one spectrum buffer
   static_assert(KW >= 2, "contraction split");
 
-  __shared__ __attribute__((aligned(16))) char wl[2][WBLK];
-  __shared__ __attribute__((aligned(16))) char xl[XBLK];
+  // dynamic LDS: xl[2][XBLK], then the weight blocks (2, or n_oc * n_ks for kStat)
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char* const xlb = smem;
+  char* const wlb = smem + 2 * XBLK;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -281,7 +257,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   const char* wbase = reinterpret_cast<const char*>(wsp);
   const char* xin = reinterpret_cast<const char*>(in);
   const int rowb = Ci * T * EB;
-  const int vec = (rowb % 16 == 0) ? 16 : (rowb % 8 == 0) ? 8 : (rowb % 4 == 0) ? 4 : 2;
+  constexpr int LW = NARROW ? EB : S::WV;  // load width; the host checks rowb % LW == 0
   const __amdgpu_buffer_rsrc_t xrs = make_rsrc(xin + r0 * rowb, (uint32_t)(len * rowb));
   if (rounds == 0) return;
 
@@ -306,13 +282,16 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     for (int u = 0; u < UPT; ++u)
       if (NU % 512 == 0 || tid + 512 * u < NU) wr[u] = *reinterpret_cast<const u32x4*>(blk + goff[u]);
   };
-  auto store_w = [&](int buf) {
+  auto store_w = [&](int blk) {
 #pragma unroll
     for (int u = 0; u < UPT; ++u)
-      if (NU % 512 == 0 || tid + 512 * u < NU) *reinterpret_cast<u32x4*>(&wl[buf][loff[u]]) = wr[u];
+      if (NU % 512 == 0 || tid + 512 * u < NU) *reinterpret_cast<u32x4*>(wlb + blk * WBLK + loff[u]) = wr[u];
   };
 
-  // ---- raw activations of (round m, step kc): HKW channels of this lane's row
+  // ---- raw activations of (round m, step kc): HKW channels of this lane's row.
+  // Issued unconditionally, also for the round after the last one (those rows
+  // lie past the buffer resource and read as zero); offsets stay below 2^31
+  // because the grid keeps one round of slack.
   uint32_t xr[NBH / 4];
   int xr_valid = 0;  // valid elements in xr (the rest belong to the next row)
   auto issue_x = [&](int m, int kc) {
@@ -321,10 +300,10 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
     const int cabs = kc * KSTEP + c0;
     xr_valid = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
-    load_raw<NBH>(xrs, voff, kc * KSTEP * T * EB, vec, xr);
+    load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr);
   };
   // transform and publish this lane's part of the step's operand spectrum
-  auto publish_x = [&]() {
+  auto publish_x = [&](int xb) {
     mask_raw<NBH, EB>(xr_valid, xr);
     float P[T][HKW];
     raw_to_planes<T, F16, HKW>(xr, P);
@@ -335,11 +314,11 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
         uint32_t w[HKW / 2];
 #pragma unroll
         for (int j = 0; j < HKW / 2; ++j) w[j] = pack2<true>(P[p][2 * j], P[p][2 * j + 1]);
-        char* dst = &xl[(rg * T + p) * 16 * RB + wl_off<RB>(li, byte)];
+        char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
         if constexpr (HKW == 4) *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
         else *reinterpret_cast<uint32_t*>(dst) = w[0];
       } else {
-        char* dst = &xl[(rg * T + p) * 16 * RB + wl_off<RB>(li, byte)];
+        char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
         if constexpr (HKW == 4) {
           *reinterpret_cast<u32x4*>(dst) = u32x4{__builtin_bit_cast(uint32_t, P[p][0]), __builtin_bit_cast(uint32_t, P[p][1]),
                                                  __builtin_bit_cast(uint32_t, P[p][2]), __builtin_bit_cast(uint32_t, P[p][3])};
@@ -351,84 +330,79 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
       }
     }
   };
-  auto read_x = [&](FR (&B)[T]) {
+  auto read_x = [&](int xb, FR (&B)[T]) {
 #pragma unroll
-    for (int p = 0; p < T; ++p) B[p] = lds_frag<FB, RB>(&xl[(rg * T + p) * 16 * RB], li, g);
+    for (int p = 0; p < T; ++p) B[p] = lds_frag<FB, RB>(xlb + xb * XBLK + (rg * T + p) * 16 * RB, li, g);
   };
 
   floatx4 acc[T][OT];
   FR xres[RES ? NKR : 1][T];
   FR bcur[T];
   const E* bp = reinterpret_cast<const E*>(bias);
-  const bool out_vec = ((int64_t)Co * T * EB) % run_vec_bytes<F16, 4 * T>() == 0;
 
-  // One step: weights of (oc, kc) in LDS buffer buf, B the operand spectrum.
-  // The sign of each complex product sits on a negated copy of one B plane
+  // One step: weights of (oc, kc) in LDS block blk, X the activation spectrum.
+  // The sign of each complex product sits on a negated copy of one X plane
   // (Im for the forward, Re for the input gradient), made once per step:
   //   forward:  Re += Wr Xr + Wi (-Xi),   Im += Wi Xr + Wr Xi
   //   backward: Re += Wr Dr + Wi Di,      Im += Wr Di + Wi (-Dr)
-  auto mma_step = [&](int oc, int buf, FR (&B)[T]) {
-    FR Bneg[Bn::K > 0 ? Bn::K : 1];
+  auto mma_step = [&](int oc, int blk, FR (&X)[T]) {
+    FR Xneg[Bn::K > 0 ? Bn::K : 1];
     static_for<Bn::K>([&](auto ki) {
       constexpr int k = decltype(ki)::value + 1;
-      Bneg[k - 1] = frag_neg<F16, FB>(B[BWD ? Bn::re(k) : Bn::im(k)]);
+      Xneg[k - 1] = frag_neg<F16, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
     });
 #pragma unroll
     for (int a = 0; a < OT; ++a) {
       const int ot = oh * OT + a;                 // o-tile within the chunk
       if (oc * OC + ot * 16 >= Co) continue;      // uniform across the wave
-      FR A[T];
+      FR W[T];
 #pragma unroll
-      for (int p = 0; p < T; ++p) A[p] = lds_frag<FB, RB>(&wl[buf][p * OC * RB], ot * 16 + li, g);
-      frag_mma<F16, KW>(acc[0][a], A[0], B[0]);
-      if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a], A[1], B[1]);
+      for (int p = 0; p < T; ++p) W[p] = lds_frag<FB, RB>(wlb + blk * WBLK + p * OC * RB, ot * 16 + li, g);
+      frag_mma<F16, KW>(acc[0][a], X[0], W[0]);
+      if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a], X[1], W[1]);
       static_for<Bn::K>([&](auto ki) {
         constexpr int k = decltype(ki)::value + 1;
         constexpr int r = Bn::re(k);
         constexpr int i = Bn::im(k);
         if constexpr (!BWD) {
-          frag_mma<F16, KW>(acc[r][a], A[r], B[r]);
-          frag_mma<F16, KW>(acc[i][a], A[i], B[r]);
-          frag_mma<F16, KW>(acc[r][a], A[i], Bneg[k - 1]);
-          frag_mma<F16, KW>(acc[i][a], A[r], B[i]);
+          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<F16, KW>(acc[i][a], X[r], W[i]);
+          frag_mma<F16, KW>(acc[r][a], Xneg[k - 1], W[i]);
+          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
         } else {
-          frag_mma<F16, KW>(acc[r][a], A[r], B[r]);
-          frag_mma<F16, KW>(acc[i][a], A[r], B[i]);
-          frag_mma<F16, KW>(acc[r][a], A[i], B[i]);
-          frag_mma<F16, KW>(acc[i][a], A[i], Bneg[k - 1]);
+          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<F16, KW>(acc[r][a], X[i], W[i]);
+          frag_mma<F16, KW>(acc[i][a], Xneg[k - 1], W[i]);
         }
       });
     }
   };
 
-  // Per lane: 4 consecutive output channels of one row per o-tile, written as
-  // one contiguous run of 4*T elements (ordinary stores, so L2 merges the
-  // lanes' runs into whole lines).
+  // D = X W^T: lane (g, i) holds output channel ot*16 + i of the pair's rows
+  // 4g .. 4g+3.  The 16 lanes of a lane group write 16 consecutive channels of
+  // one row, a contiguous span of 16*T elements (whole cache lines).
   auto epilogue = [&](int m, int oc) {
-    const int64_t q = (int64_t)m * 64 + 4 * li + rg;
-    if (q >= len) return;
-    const int64_t n = r0 + q;
 #pragma unroll
     for (int a = 0; a < OT; ++a) {
       const int ot = oh * OT + a;
-      const int o4 = oc * OC + ot * 16 + 4 * g;
-      if (oc * OC + ot * 16 >= Co || o4 >= Co) continue;
-      float u[4 * T];
+      if (oc * OC + ot * 16 >= Co) continue;  // uniform across the wave
+      const int o = oc * OC + ot * 16 + li;
+      float bv = 0.0f;
+      if constexpr (!BWD) {
+        if (bp != nullptr && o < Co) bv = (float)bp[o];
+      }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
+        const int64_t q = (int64_t)m * 64 + 4 * (4 * g + r) + rg;
         float Pl[T], ul[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
         irdft<T>(Pl, ul);
-        float bv = 0.0f;
-        if constexpr (!BWD) {
-          if (bp != nullptr && o4 + r < Co) bv = (float)bp[o4 + r];
-        }
 #pragma unroll
-        for (int t = 0; t < T; ++t) u[r * T + t] = ul[t] + bv;
+        for (int t = 0; t < T; ++t) ul[t] += bv;
+        if (q < len && o < Co) store_run<F16, T>(out, ((r0 + q) * Co + o) * T, true, T, ul);
       }
-      const int nvalid = (Co - o4 >= 4 ? 4 : Co - o4) * T;
-      store_run<F16, 4 * T>(out, (n * Co + o4) * T, out_vec, nvalid, u);
     }
   };
 
@@ -439,15 +413,72 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
       for (int a = 0; a < OT; ++a) acc[p][a] = floatx4{0.f, 0.f, 0.f, 0.f};
   };
 
-  // Step protocol (running step s, weights of s in wl[s & 1]):
-  //   publish X(s) to xl; barrier (1): X(s) and W(s) visible
+  int buf = 0;
+  if constexpr (MODE == kStat) {
+    // All weight blocks into LDS once; then a step only exchanges activations:
+    //   publish X(s) to xl[s & 1]; barrier; issue activations of s+1;
+    //   read operands, MFMA(s).
+    // The activations of s+1 are issued before the epilogue that may end step
+    // s, so waiting for them never waits for that epilogue's stores.
+    issue_x(0, 0);
+    {
+      // block b = oc * nks + kc holds planes x OC rows x KSTEP channels; unit
+      // u of the arena is 16 bytes of it.  Four loads in flight per thread.
+      const int n_units = n_oc * nks * NU;
+      for (int u0 = tid; u0 < n_units; u0 += 4 * 512) {
+        u32x4 v[4];
+        int lo[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int u = u0 + 512 * j;
+          lo[j] = -1;
+          if (u < n_units) {
+            const int blk = u / NU;
+            const int in_blk = u - blk * NU;
+            const int boc = blk / nks;
+            const int bkc = blk - boc * nks;
+            const int p = in_blk / (OC * RB / 16);
+            const int rem = in_blk - p * (OC * RB / 16);
+            const int row = rem / (RB / 16);
+            const int ch = rem - row * (RB / 16);
+            const char* src = wbase + p * wplane + ((int64_t)(boc * OC + row) * Ci_pad + bkc * KSTEP) * EB + ch * 16;
+            v[j] = *reinterpret_cast<const u32x4*>(src);
+            lo[j] = blk * WBLK + p * OC * RB + wl_off<RB>(row, ch * 16);
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (lo[j] >= 0) *reinterpret_cast<u32x4*>(wlb + lo[j]) = v[j];
+      }
+    }
+    for (int m = 0; m < rounds; ++m) {
+      for (int oc = 0; oc < n_oc; ++oc) {
+        zero_acc();
+        for (int kc = 0; kc < nks; ++kc) {
+          int noc = oc, nkc = kc + 1, nm = m;
+          if (nkc == nks) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
+          publish_x(buf);
+          __syncthreads();
+          issue_x(nm, nkc);  // past the last round: rows beyond the resource read as zero
+          read_x(buf, bcur);
+          mma_step(oc, oc * nks + kc, bcur);
+          buf ^= 1;
+        }
+        epilogue(m, oc);
+      }
+    }
+    return;
+  }
+
+  // Streamed weights (running step s; weights of s in block s & 1, spectrum
+  // of s in xl[s & 1]):
+  //   publish X(s) to xl[s & 1]; barrier: X(s) and W(s) visible, and every
+  //     wave is done with step s-1, so buffers (s+1) & 1 are free
   //   issue loads W(s+1) -> registers, activations for s+1
-  //   read operands, MFMA(s); W(s+1) -> wl[(s+1) & 1] (last read at step s-1)
-  //   barrier (2): W(s+1) visible next step, xl free again
+  //   read operands, MFMA(s); W(s+1) -> block (s+1) & 1
   issue_w(0, 0);
   issue_x(0, 0);
   store_w(0);
-  int buf = 0;
   for (int m = 0; m < rounds; ++m) {
     for (int oc = 0; oc < n_oc; ++oc) {
       zero_acc();
@@ -457,17 +488,16 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
           int noc = oc, nkc = kc + 1, nm = m;
           if (nkc == NKR) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
           const bool more = nm < rounds;
-          if (oc == 0) publish_x();
+          if (oc == 0) publish_x(buf);
           __syncthreads();
           if (more) issue_w(noc, nkc);
           if (oc == 0) {
             if (kc + 1 < NKR) issue_x(m, kc + 1);
-            else if (m + 1 < rounds) issue_x(m + 1, 0);
-            read_x(xres[kc]);
+            else issue_x(m + 1, 0);
+            read_x(buf, xres[kc]);
           }
           mma_step(oc, buf, xres[kc]);
           if (more) store_w(buf ^ 1);
-          __syncthreads();
           buf ^= 1;
         });
       } else {
@@ -475,16 +505,13 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
           int noc = oc, nkc = kc + 1, nm = m;
           if (nkc == nks) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
           const bool more = nm < rounds;
-          publish_x();
+          publish_x(buf);
           __syncthreads();
-          if (more) {
-            issue_w(noc, nkc);
-            issue_x(nm, nkc);
-          }
-          read_x(bcur);
+          if (more) issue_w(noc, nkc);
+          issue_x(nm, nkc);
+          read_x(buf, bcur);
           mma_step(oc, buf, bcur);
           if (more) store_w(buf ^ 1);
-          __syncthreads();
           buf ^= 1;
         }
       }

@@ -18,26 +18,53 @@ struct GemmPlan {
   int n_ks;        // contraction steps
   int OT, OC;      // o-tiles per wave, channels per chunk
   int n_oc;        // o-chunks
-  bool res;        // spectrum resident across o-chunks
+  int mode;        // GemmMode: 0 streamed weights, 1 + resident spectrum, 2 resident weights
+  bool narrow;     // row stride not a multiple of the wide load: element loads, OT = 1, mode 0
   int Co_pad;      // padded weight rows (n_oc * OC)
+  int lds_bytes;   // dynamic LDS of one workgroup
 };
-inline int gemm_kw(int T, bool f16) {
+constexpr int kLdsBytes = 160 * 1024;
+constexpr int gemm_kw_c(int T, bool f16) {
   const int fit = 128 / (T * (f16 ? 2 : 4));
   if (f16) return fit >= 8 ? 8 : 4;
   return fit >= 8 ? 8 : fit >= 4 ? 4 : fit >= 2 ? 2 : 1;
 }
-// o-tiles per wave: at most 96 accumulator floats per lane (T*OT*4), and the
-// two weight buffers plus the spectrum buffer within 160 KB of LDS.
-constexpr int gemm_otmax_c(int T, int kw, int eb) {
-  const int rb = 4 * kw * eb;
-  const int by_acc = 24 / T > 8 ? 8 : (24 / T < 1 ? 1 : 24 / T);
-  const int by_lds = 163840 / (64 * T * rb) - 1;
-  return by_acc < by_lds ? by_acc : (by_lds < 1 ? 1 : by_lds);
+inline int gemm_kw(int T, bool f16) { return gemm_kw_c(T, f16); }
+constexpr int gemm_rb_c(int T, bool f16) { return 4 * gemm_kw_c(T, f16) * (f16 ? 2 : 4); }
+// LDS of one workgroup with n_wblocks weight blocks: two spectrum buffers of
+// 64*T rows and the blocks of 32*OT*T rows, each row RB bytes.
+constexpr int gemm_lds_c(int T, bool f16, int OT, int n_wblocks) {
+  return (2 * 64 * T + n_wblocks * 32 * OT * T) * gemm_rb_c(T, f16);
 }
-inline int gemm_otmax(int T, bool f16) { return gemm_otmax_c(T, gemm_kw(T, f16), f16 ? 2 : 4); }
+// o-tiles per wave: at most 96 accumulator floats per lane (T*OT*4), and two
+// weight blocks plus the spectrum buffers within the LDS.
+constexpr int gemm_otmax_c(int T, bool f16) {
+  const int by_acc = 24 / T > 8 ? 8 : (24 / T < 1 ? 1 : 24 / T);
+  int by_lds = 1;
+  while (by_lds < 8 && gemm_lds_c(T, f16, by_lds + 1, 2) <= kLdsBytes) ++by_lds;
+  return by_acc < by_lds ? by_acc : by_lds;
+}
+inline int gemm_otmax(int T, bool f16) { return gemm_otmax_c(T, f16); }
 inline int gemm_otres(int T, bool f16) {
   return gemm_otmax(T, f16) / 2 < 1 ? 1 : gemm_otmax(T, f16) / 2;
 }
+// o-tile counts that have a kernel instantiation: 1, 2, 3, 4, 6, 8 up to the maximum.
+constexpr bool gemm_ot_inst(int T, bool f16, int OT) {
+  return OT >= 1 && OT <= gemm_otmax_c(T, f16) && (OT <= 4 || OT == 6 || OT == 8);
+}
+inline int gemm_ot_round(int T, bool f16, int want) {
+  for (int ot = want; ot <= gemm_otmax(T, f16); ++ot)
+    if (gemm_ot_inst(T, f16, ot)) return ot;
+  return gemm_otmax(T, f16);
+}
+// Widest activation load of one lane's run (KW/2 channels x T elements); the
+// row stride Ci*T*EB must be a multiple of it (eql_gemm.h GemmShape::WV).
+constexpr int gemm_wide_load_c(int T, bool f16) {
+  const int nbh = gemm_kw_c(T, f16) / 2 * T * (f16 ? 2 : 4);
+  return nbh % 16 == 0 ? 16 : nbh % 8 == 0 ? 8 : 4;
+}
+// EQL_GEMM_MODE=0/1/2 forces a weight mode where it is valid (tests, A/B timing).
+int gemm_forced_mode();
 inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   GemmPlan p{};
   p.kw = gemm_kw(T, f16);
@@ -45,22 +72,33 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   p.n_ks = (Ci + p.kstep - 1) / p.kstep;
   const int per_wave = ((Co + 15) / 16 + 1) / 2;  // o-tiles per wave for one chunk
   const int otmax = gemm_otmax(T, f16);
+  const bool res_ok = T <= 8 && p.n_ks <= 3 && p.kw * (f16 ? 2 : 4) <= 16;
   if (per_wave <= otmax) {
-    p.OT = per_wave <= 1 ? 1 : per_wave <= 2 ? 2 : (per_wave <= 4 && otmax >= 4) ? 4 : otmax;
-    if (p.OT > otmax) p.OT = otmax;
+    p.OT = gemm_ot_round(T, f16, per_wave);
     p.n_oc = 1;
-    p.res = false;
-  } else if (T <= 8 && p.n_ks <= 3 && p.kw * (f16 ? 2 : 4) <= 16) {
+    p.mode = 0;
+  } else if (res_ok) {
     p.OT = gemm_otres(T, f16);
     p.n_oc = (Co + 32 * p.OT - 1) / (32 * p.OT);
-    p.res = true;
+    p.mode = 1;
   } else {
     p.OT = otmax;
     p.n_oc = (Co + 32 * otmax - 1) / (32 * otmax);
-    p.res = false;
+    p.mode = 0;
+  }
+  // every weight block resident when they all fit
+  if (gemm_lds_c(T, f16, p.OT, p.n_oc * p.n_ks) <= kLdsBytes) p.mode = 2;
+  const int forced = gemm_forced_mode();
+  if (forced == 0 || (forced == 1 && res_ok && p.OT == gemm_otres(T, f16))) p.mode = forced;
+  p.narrow = ((int64_t)Ci * T * (f16 ? 2 : 4)) % gemm_wide_load_c(T, f16) != 0;
+  if (p.narrow) {
+    p.OT = 1;
+    p.n_oc = (Co + 31) / 32;
+    p.mode = 0;
   }
   p.OC = 32 * p.OT;
   p.Co_pad = p.n_oc * p.OC;
+  p.lds_bytes = gemm_lds_c(T, f16, p.OT, p.mode == 2 ? p.n_oc * p.n_ks : 2);
   return p;
 }
 

@@ -18,23 +18,30 @@ hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s)
   return hipGetLastError();
 }
 
-// Persistent grid: one workgroup per resident slot (CUs x occupancy), and no
-// workgroup with fewer than 16 rows.
-template <typename K>
-int persistent_grid(K kernel, int threads, int64_t N, int64_t row_bytes) {
-  static int occ_cache[64];
+// Resident workgroups per CU of one kernel at a given dynamic LDS size,
+// cached per (device, kernel, LDS).
+inline int occupancy(const void* kernel, int threads, int lds) {
+  struct Entry { const void* k; int dev, lds, occ; };
+  static Entry cache[256];
+  static int n_cache = 0;
   int dev = 0;
   (void)hipGetDevice(&dev);
-  int occ = (dev >= 0 && dev < 64) ? occ_cache[dev] : 0;
-  if (occ <= 0) {
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, 0) != hipSuccess || occ <= 0) {
-      (void)hipGetLastError();
-      occ = 1;
-    }
-    if (dev >= 0 && dev < 64) occ_cache[dev] = occ;
+  for (int i = 0; i < n_cache; ++i)
+    if (cache[i].k == kernel && cache[i].dev == dev && cache[i].lds == lds) return cache[i].occ;
+  int occ = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, lds) != hipSuccess || occ <= 0) {
+    (void)hipGetLastError();
+    occ = 1;
   }
-  const int64_t slots = (int64_t)device_cu_count() * occ;
-  const int64_t by_rows = (N + 31) / 32;  // at least 32 rows per workgroup
+  if (n_cache < 256) cache[n_cache++] = Entry{kernel, dev, lds, occ};
+  return occ;
+}
+
+// Persistent grid: one workgroup per resident slot (CUs x occupancy), and no
+// workgroup with fewer than 32 rows.
+inline int persistent_grid(const void* kernel, int threads, int lds, int64_t N, int64_t row_bytes) {
+  const int64_t slots = (int64_t)device_cu_count() * occupancy(kernel, threads, lds);
+  const int64_t by_rows = (N + 31) / 32;
   int64_t g = slots < by_rows ? slots : by_rows;
   if (g < 1) g = 1;
   // each workgroup addresses its rows (plus one round of slack) with 31-bit offsets
@@ -42,40 +49,56 @@ int persistent_grid(K kernel, int threads, int64_t N, int64_t row_bytes) {
   return (int)g;
 }
 
-template <int T, bool F16, bool BWD, int OT, bool RES, int NKR>
+template <int T, bool F16, bool BWD, int OT, int MODE, int NKR, bool NARROW = false>
 hipError_t gemm_variant(const GemmArgs& a) {
-  auto k = eql_gemm_kernel<T, F16, BWD, OT, RES, NKR>;
-  const int grid = persistent_grid(k, 512, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
-  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(512), 0, a.stream, a.in, a.wsp, a.bias, a.out,
+  static_assert(GemmShape<T, F16>::WV == gemm_wide_load_c(T, F16), "host and kernel load widths");
+  auto k = eql_gemm_kernel<T, F16, BWD, OT, MODE, NKR, NARROW>;
+  const int lds = a.plan.lds_bytes;
+  if (lds != gemm_lds_c(T, F16, OT, MODE == kStat ? a.plan.n_oc * a.plan.n_ks : 2) || lds > kLdsBytes)
+    return hipErrorInvalidValue;
+  if (lds > 64 * 1024) {
+    hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return e;
+  }
+  const int grid = persistent_grid((const void*)k, 512, lds, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
+  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(512), lds, a.stream, a.in, a.wsp, a.bias, a.out,
                      a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
   return hipGetLastError();
 }
 
+template <int T, bool F16, bool BWD, int MODE>
+hipError_t gemm_ot(const GemmArgs& a) {
+  hipError_t r = hipErrorInvalidValue;
+  static_for<8>([&](auto oi) {
+    constexpr int OT = decltype(oi)::value + 1;
+    if constexpr (gemm_ot_inst(T, F16, OT)) {
+      if (a.plan.OT == OT) r = gemm_variant<T, F16, BWD, OT, MODE, 0>(a);
+    }
+  });
+  return r;
+}
+
 template <int T, bool F16, bool BWD>
 hipError_t gemm_t(const GemmArgs& a) {
-  constexpr int OTM = gemm_otmax_c(T, GemmShape<T, F16>::KW, F16 ? 2 : 4);
-  constexpr int OTR = OTM / 2 < 1 ? 1 : OTM / 2;
+  constexpr int OTR = gemm_otmax_c(T, F16) / 2 < 1 ? 1 : gemm_otmax_c(T, F16) / 2;
   constexpr bool kResOk = T <= 8 && GemmShape<T, F16>::FB <= 16;
   const GemmPlan& p = a.plan;
-  if (p.res) {
+  if (p.narrow) {
+    if (p.OT != 1 || p.mode != kStream) return hipErrorInvalidValue;
+    return gemm_variant<T, F16, BWD, 1, kStream, 0, true>(a);
+  }
+  if (((int64_t)a.Ci * T * (F16 ? 2 : 4)) % GemmShape<T, F16>::WV != 0) return hipErrorInvalidValue;
+  if (p.mode == kRes) {
     if constexpr (kResOk) {
       if (p.OT != OTR) return hipErrorInvalidValue;
-      if (p.n_ks == 1) return gemm_variant<T, F16, BWD, OTR, true, 1>(a);
-      if (p.n_ks == 2) return gemm_variant<T, F16, BWD, OTR, true, 2>(a);
-      if (p.n_ks == 3) return gemm_variant<T, F16, BWD, OTR, true, 3>(a);
+      if (p.n_ks == 1) return gemm_variant<T, F16, BWD, OTR, kRes, 1>(a);
+      if (p.n_ks == 2) return gemm_variant<T, F16, BWD, OTR, kRes, 2>(a);
+      if (p.n_ks == 3) return gemm_variant<T, F16, BWD, OTR, kRes, 3>(a);
     }
     return hipErrorInvalidValue;
   }
-  if (p.OT == 1) return gemm_variant<T, F16, BWD, 1, false, 0>(a);
-  if constexpr (OTM >= 2) {
-    if (p.OT == 2) return gemm_variant<T, F16, BWD, 2, false, 0>(a);
-  }
-  if constexpr (OTM > 4) {
-    if (p.OT == 4) return gemm_variant<T, F16, BWD, 4, false, 0>(a);
-  }
-  if constexpr (OTM > 2) {
-    if (p.OT == OTM) return gemm_variant<T, F16, BWD, OTM, false, 0>(a);
-  }
+  if (p.mode == kStat) return gemm_ot<T, F16, BWD, kStat>(a);
+  if (p.mode == kStream) return gemm_ot<T, F16, BWD, kStream>(a);
   return hipErrorInvalidValue;
 }
 

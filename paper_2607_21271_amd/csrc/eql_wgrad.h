@@ -27,14 +27,16 @@
 namespace eqk {
 
 // The T elements of one (row, channel), EB bytes each, packed into words
-// (element e in half e%2 of word e/2 for 16-bit data).  vec is the widest
-// aligned load width that every row start allows.
+// (element e in half e%2 of word e/2 for 16-bit data).  Every (row, channel)
+// starts at a multiple of T*EB bytes, so the widest load width dividing T*EB
+// is always aligned; it is fixed at compile time (one load shape per kernel).
 template <int T, int EB>
-__device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t rs, uint32_t off, int vec,
+__device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t rs, uint32_t off,
                                          uint32_t (&w)[(T * EB + 3) / 4]) {
   constexpr int NB = T * EB;
   if constexpr (NB % 4 == 0) {
-    load_raw<NB>(rs, off, 0, vec, w);
+    constexpr int W = NB % 16 == 0 ? 16 : NB % 8 == 0 ? 8 : 4;
+    load_raw<NB, W>(rs, off, 0, w);
   } else {
 #pragma unroll
     for (int q = 0; q < (NB + 3) / 4; ++q) {
@@ -98,10 +100,6 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   const __amdgpu_buffer_rsrc_t drs =
       make_rsrc(reinterpret_cast<const char*>(dy) + n_begin * rowd, (uint32_t)((n_end - n_begin) * rowd));
   constexpr int ITB = T * EB;  // bytes of one (row, channel)
-  const int vx = (rowx % 16 == 0 && ITB % 16 == 0) ? 16 : (rowx % 8 == 0 && ITB % 8 == 0) ? 8
-               : (rowx % 4 == 0 && ITB % 4 == 0) ? 4 : 2;
-  const int vd = (rowd % 16 == 0 && ITB % 16 == 0) ? 16 : (rowd % 8 == 0 && ITB % 8 == 0) ? 8
-               : (rowd % 4 == 0 && ITB % 4 == 0) ? 4 : 2;
 
   uint32_t rx[UX][RAW], rd[UD][RAW];
   // item u of this thread: channel (item % B?), row pair (item / B?)
@@ -116,7 +114,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           uint32_t w[WPR];
-          load_row<T, EB>(xrs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cin + cg) * ITB), vx, w);
+          load_row<T, EB>(xrs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cin + cg) * ITB), w);
 #pragma unroll
           for (int q = 0; q < WPR; ++q) rx[u][h * WPR + q] = w[q];
         }
@@ -134,7 +132,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
           uint32_t w[WPR];
-          load_row<T, EB>(drs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cout + og) * ITB), vd, w);
+          load_row<T, EB>(drs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cout + og) * ITB), w);
 #pragma unroll
           for (int q = 0; q < WPR; ++q) rd[u][h * WPR + q] = w[q];
         }
@@ -158,12 +156,14 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       const int c = item % BC, rp = item / BC;
       float P0[T], P1[T];
       {
-        float v[T];
+        constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
+        float f[RAW * EPW], v[T];
+        raw_to_floats<F16, RAW>(rx[u], f);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rx[u], t);
+        for (int t = 0; t < T; ++t) v[t] = f[t];
         rdft<T>(v, P0);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rx[u] + WPR, t);
+        for (int t = 0; t < T; ++t) v[t] = f[WPR * EPW + t];
         rdft<T>(v, P1);
       }
 #pragma unroll
@@ -180,12 +180,14 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       const int o = item % BO, rp = item / BO;
       float P0[T], P1[T];
       {
-        float v[T];
+        constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
+        float f[RAW * EPW], v[T];
+        raw_to_floats<F16, RAW>(rd[u], f);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rd[u], t);
+        for (int t = 0; t < T; ++t) v[t] = f[t];
         rdft<T>(v, P0);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = raw_elem<F16>(rd[u] + WPR, t);
+        for (int t = 0; t < T; ++t) v[t] = f[WPR * EPW + t];
         rdft<T>(v, P1);
       }
       dbacc[u] += P0[0] + P1[0];

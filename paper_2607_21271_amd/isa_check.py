@@ -1,0 +1,109 @@
+"""Post-build scan of the gfx950 assembly of libeqlinear.so.
+
+The fp16 activation words are unpacked by one inline-asm statement per word
+(``f16x2_to_f32`` in csrc/eql_common.h): a convert of the low half into an
+early-clobber output, then a convert of the high half.  In some kernels this
+toolchain's register allocator once gave that output the input's register (the
+word then reads as already converted), and before the asm form, the same fault
+showed as a word being overwritten between its two half-conversions.  Both
+miscompiles give wrong numbers without any error, so the build scans the
+device assembly for them and refuses to produce a library that has either.
+
+Checks, per kernel:
+  clobbered_unpack   the unpack asm's first convert writes its own input register
+  converted_source   an f16->f32 convert reads a register whose last write in
+                     the same basic block was an fp32 result (a raw word is
+                     never such a value)
+"""
+from __future__ import annotations
+
+import glob
+import os
+import re
+import subprocess
+
+_FUNC = re.compile(r"^(_Z\S+):")
+_BLOCK_END = re.compile(r"^\.LBB|^\s*s_cbranch|^\s*s_branch|^; %bb")
+_CVT = re.compile(r"^\s*v_cvt_f32_f16\S*\s+v(\d+),\s*v(\d+)\b")
+_F32_DEF = re.compile(r"^\s*(v_cvt_f32_f16\S*|v_add_f32\S*|v_sub_f32\S*|v_subrev_f32\S*|v_mul_f32\S*"
+                      r"|v_fma_f32\S*|v_fmac_f32\S*|v_fmamk_f32\S*|v_fmaak_f32\S*)\s+v(\d+),")
+_DEF_RANGE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v\[(\d+):(\d+)\]")
+_DEF_ONE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v(\d+)\b")
+_UNPACK_FIRST = re.compile(r"^\s*v_cvt_f32_f16_e32 v(\d+), v(\d+)\s*$")
+
+
+def scan_lines(lines):
+    """Return a list of (kernel, check, instruction) problems found in assembly lines."""
+    problems = []
+    kernel = None
+    last = {}          # vgpr -> "f32" | "other", within the current basic block
+    in_asm = False
+    asm_first = False
+    for line in lines:
+        m = _FUNC.match(line)
+        if m:
+            kernel, last, in_asm = m.group(1), {}, False
+            continue
+        if "ASMSTART" in line:
+            in_asm, asm_first = True, True
+            continue
+        if "ASMEND" in line:
+            in_asm = False
+            continue
+        if _BLOCK_END.match(line):
+            last = {}
+            continue
+        if in_asm and asm_first:
+            asm_first = False
+            u = _UNPACK_FIRST.match(line)
+            if u and u.group(1) == u.group(2):
+                problems.append((kernel, "clobbered_unpack", line.strip()))
+        c = _CVT.match(line)
+        if c and last.get(int(c.group(2))) == "f32":
+            problems.append((kernel, "converted_source", line.strip()))
+        f = _F32_DEF.match(line)
+        if f:
+            last[int(f.group(2))] = "f32"
+            continue
+        r = _DEF_RANGE.match(line)
+        if r:
+            for k in range(int(r.group(2)), int(r.group(3)) + 1):
+                last[k] = "other"
+            continue
+        d = _DEF_ONE.match(line)
+        if d and not line.strip().startswith("v_cmp"):
+            last[int(d.group(2))] = "other"
+    return problems
+
+
+def scan_file(path):
+    with open(path) as f:
+        return scan_lines(f)
+
+
+def device_asm_files(build_dir):
+    return sorted(glob.glob(os.path.join(build_dir, "*-hip-amdgcn-amd-amdhsa-*.s")))
+
+
+def demangle(names):
+    try:
+        out = subprocess.run(["c++filt"], input="\n".join(names), capture_output=True, text=True).stdout
+        return out.split("\n")[: len(names)]
+    except OSError:
+        return list(names)
+
+
+def check_build(build_dir):
+    """Scan every device assembly file of a build; raise RuntimeError on a problem."""
+    files = device_asm_files(build_dir)
+    if not files:
+        raise RuntimeError("no device assembly found in %s (the build keeps it with -save-temps)" % build_dir)
+    problems = []
+    for path in files:
+        problems += [(os.path.basename(path),) + p for p in scan_file(path)]
+    if problems:
+        names = demangle([p[1] for p in problems])
+        msg = "\n".join("  %s: %s: %s: %s" % (p[0], n, p[2], p[3]) for p, n in zip(problems[:20], names))
+        raise RuntimeError("device code failed the post-build check (%d findings):\n%s"
+                           % (len(problems), msg))
+    return files

@@ -212,3 +212,27 @@ def test_autograd_module_matches_oracle(orc):
     assert rel_err(x.grad.cpu().numpy().reshape(N, Cin, T), ref_dx) <= 1e-5
     assert rel_err(m.weight.grad.cpu().numpy(), ref_dw) <= 1e-5
     assert rel_err(m.bias.grad.cpu().numpy(), ref_db) <= 1e-5
+
+
+# Shapes whose default plan keeps every weight block resident in LDS; the
+# streamed-weight kernels of the same (T, dtype, o-tiles) are forced here so
+# that both instantiations stay under test.
+FORCED = [(3, 64, 64, 1029, True), (4, 24, 96, 2085, False), (4, 96, 24, 700, False),
+          (5, 64, 64, 515, True), (8, 48, 48, 613, True), (12, 64, 64, 257, True),
+          (7, 40, 72, 130, False), (2, 64, 200, 99, True)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", FORCED,
+                         ids=["T%d-%dx%d-N%d" % f[:4] for f in FORCED])
+def test_forced_streamed_weights(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+    say("forced stream", T, Cin, Cout, N, dt)
+    monkeypatch.setenv("EQL_GEMM_MODE", "0")
+    inp = synth.draw(T, Cin, Cout, N, bias, 7000 + 31 * T + Cin + Cout).rounded(dt)
+    g = run_gpu(inp, dt, want=("y", "dx"))
+    errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
+            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w))}
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (T, Cin, Cout, dt, k, v)

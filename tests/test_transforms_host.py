@@ -35,7 +35,8 @@ def txlib():
     src = open(HDR).read()
     a = src.index("namespace eqk {")
     b = src.index("// ---------------------------------------------------------------------------\n// Element types.")
-    body = src[a:b].replace("__device__ __forceinline__", "inline") + "}\n"
+    body = (src[a:b].replace("__host__ __device__ __forceinline__", "inline")
+            .replace("__device__ __forceinline__", "inline") + "}\n")
     d = tempfile.mkdtemp()
     with open(os.path.join(d, "tx.h"), "w") as f:
         f.write("#include <cmath>\n#include <cstdint>\n#include <type_traits>\n#include <utility>\n"
