@@ -229,6 +229,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   a.Co = Co;
   a.stream = (hipStream_t)stream;
   a.plan = eqk::gemm_plan(T, Ci, Co, dtype == EQL_F16);
+  eqk::gemm_plan_rows(a.plan, N, T, dtype == EQL_F16, eqk::device_cu_count());
   if (!bwd) {
     a.wsp = wspec;
     a.Ci_pad = d.CiF;

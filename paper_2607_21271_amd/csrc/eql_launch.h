@@ -102,6 +102,18 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   return p;
 }
 
+// Row-count adjustment at launch: resident weights pay for loading every block
+// up front, which only amortises when a workgroup runs several 64-row rounds;
+// with at most one round per CU the streamed mode overlaps that load with the
+// MFMAs.  Changes only the mode (never OT or the chunking), so the weight
+// spectrum layout is the same either way.
+inline void gemm_plan_rows(GemmPlan& p, int64_t N, int T, bool f16, int cus) {
+  if (p.mode == 2 && gemm_forced_mode() < 0 && N < (int64_t)2 * 64 * cus) {
+    p.mode = 0;
+    p.lds_bytes = gemm_lds_c(T, f16, p.OT, 2);
+  }
+}
+
 // Padded extents of the weight spectrum: rows to the o-chunks of the pass that
 // reads the layout, columns to 32 (a multiple of every contraction step).
 constexpr int kColPad = 32;

@@ -214,25 +214,27 @@ def test_autograd_module_matches_oracle(orc):
     assert rel_err(m.bias.grad.cpu().numpy(), ref_db) <= 1e-5
 
 
-# Shapes whose default plan keeps every weight block resident in LDS; the
-# streamed-weight kernels of the same (T, dtype, o-tiles) are forced here so
-# that both instantiations stay under test.
+# The weight mode is chosen from the shape and the row count; each mode is also
+# forced here on small inputs so that both instantiations of a shape stay under
+# test (0: streamed weights, 2: every weight block resident in LDS, where the
+# blocks fit; elsewhere the plan keeps its own mode).
 FORCED = [(3, 64, 64, 1029, True), (4, 24, 96, 2085, False), (4, 96, 24, 700, False),
           (5, 64, 64, 515, True), (8, 48, 48, 613, True), (12, 64, 64, 257, True),
-          (7, 40, 72, 130, False), (2, 64, 200, 99, True)]
+          (7, 40, 72, 130, False), (2, 64, 200, 99, True), (8, 96, 384, 300, False)]
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("mode", ["0", "2"])
 @pytest.mark.parametrize("dt", ["f32", "f16"])
 @pytest.mark.parametrize("T,Cin,Cout,N,bias", FORCED,
                          ids=["T%d-%dx%d-N%d" % f[:4] for f in FORCED])
-def test_forced_streamed_weights(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
-    say("forced stream", T, Cin, Cout, N, dt)
-    monkeypatch.setenv("EQL_GEMM_MODE", "0")
+def test_forced_weight_mode(orc, monkeypatch, T, Cin, Cout, N, bias, dt, mode):
+    say("forced mode", mode, T, Cin, Cout, N, dt)
+    monkeypatch.setenv("EQL_GEMM_MODE", mode)
     inp = synth.draw(T, Cin, Cout, N, bias, 7000 + 31 * T + Cin + Cout).rounded(dt)
     g = run_gpu(inp, dt, want=("y", "dx"))
     errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
             "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w))}
     say("  ", {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
-        assert v <= TOL[dt], (T, Cin, Cout, dt, k, v)
+        assert v <= TOL[dt], (T, Cin, Cout, dt, mode, k, v)
