@@ -45,7 +45,23 @@ def parse():
                     help="rows of the oracle sample (0: sized to about 15 s of host work)")
     ap.add_argument("--all", action="store_true",
                     help="also time every other workload and dtype (one JSON line each on stderr)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
+                    help="only run a plain device copy of this many MiB, 5 times (reference "
+                         "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
     return ap.parse_args()
+
+
+def calibrate_copy(mib):
+    """A plain copy of known size: the counters it produces turn FETCH_SIZE and
+    WRITE_SIZE readings of the layer's kernels into HBM bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n * 4, "launches": 5}), flush=True)
 
 
 def source_digest() -> str:
@@ -249,6 +265,9 @@ def main():
 
     import synth
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy > 0:
+        calibrate_copy(args.calibrate_copy)
+        return
     digest = source_digest()
     name = args.workload or synth.HEADLINE
     layer = synth.LAYERS[name]

@@ -41,8 +41,8 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
     p.rows_per_split = 0;
   } else {
     // About one workgroup per CU of a 256-CU device, fp32 partials (written
-    // once, read once) at most the bytes of x and dy, at least two row chunks
-    // per split, and each split's rows addressable with 31 bits.
+    // once, read once) at most half the bytes of x and dy, at least two row
+    // chunks per split, and each split's rows addressable with 31 bits.
     const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
     int64_t s = (256 + tiles - 1) / tiles;
     const double eb = f16 ? 2.0 : 4.0;
@@ -53,6 +53,10 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
     const int64_t max_s = (N + 2 * p.KR - 1) / (2 * p.KR);
     if (s > max_s) s = max_s;
     if (s < 1) s = 1;
+    // whole groups of 8 splits: the kernel places the tiles of a split on one
+    // XCD (split % 8), and a partial group would add idle workgroups and push
+    // real ones past the first wave of the grid
+    if (s >= 8) s = s / 8 * 8;
     const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
     while ((double)((N + s - 1) / s + p.KR) * row_bytes >= 2147483648.0) ++s;
     int64_t rows = (N + s - 1) / s;

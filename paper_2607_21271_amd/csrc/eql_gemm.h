@@ -27,6 +27,7 @@
 // one row.
 #pragma once
 #include "eql_common.h"
+#include "eql_config.h"
 
 namespace eqk {
 
@@ -195,7 +196,7 @@ enum GemmMode { kStream = 0, kRes = 1, kStat = 2 };
 template <int T, bool F16, int OT>
 struct GemmLds {
   static constexpr int RB = GemmShape<T, F16>::RB;
-  static constexpr int XBLK = 4 * T * 16 * RB;  // 4 row groups x T planes x 16 rows
+  static constexpr int XBLK = kGemmPairs * T * 16 * RB;  // pairs x T planes x 16 rows
   static constexpr int WBLK = T * 32 * OT * RB; // T planes x OC channels
   static constexpr int bytes(int n_wblocks) { return 2 * XBLK + n_wblocks * WBLK; }
 };
@@ -211,7 +212,7 @@ struct GemmLds {
 // double buffered in LDS: the next block is loaded into registers while the
 // current one feeds the MFMAs, then written to the idle buffer.
 template <int T, bool F16, bool BWD, int OT, int MODE, int NKR, bool NARROW>
-__global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ in,
+__global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __restrict__ in,
                                                        const void* __restrict__ wsp,
                                                        const void* __restrict__ bias,
                                                        void* __restrict__ out, int64_t N, int Ci,
@@ -232,7 +233,8 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   constexpr bool RES = MODE == kRes;
   constexpr int WBLK = GemmLds<T, F16, OT>::WBLK;  // bytes of one weight block
   constexpr int NU = WBLK / 16;         // 16-byte units per block
-  constexpr int UPT = (NU + 511) / 512; // weight units per thread
+  constexpr int NTH = kGemmThreads;
+  constexpr int UPT = (NU + NTH - 1) / NTH; // weight units per thread
   constexpr int XBLK = GemmLds<T, F16, OT>::XBLK;  // bytes of one spectrum buffer
   static_assert(KW >= 2, "contraction split");
 
@@ -251,7 +253,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   const int64_t r0 = (int64_t)blockIdx.x * N / gridDim.x;
   const int64_t r1 = ((int64_t)blockIdx.x + 1) * N / gridDim.x;
   const int64_t len = r1 - r0;
-  const int rounds = (int)((len + 63) / 64);
+  const int rounds = (int)((len + kGemmRoundRows - 1) / kGemmRoundRows);
   const int nks = RES ? NKR : n_ks;
   const int64_t wplane = (int64_t)Co_pad * Ci_pad * EB;
   const char* wbase = reinterpret_cast<const char*>(wsp);
@@ -263,12 +265,16 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
 
   // ---- weight block (oc, kc): global -> registers -> LDS buffer.  Per-thread
   // unit offsets are fixed; a step only moves a uniform base.
-  u32x4 wr[UPT];
+  // register sets of prefetched weight blocks: 2 when streamed (a block is
+  // issued two steps before it is stored to LDS), NKR with a resident
+  // spectrum (block (oc, kc) always uses set kc)
+  constexpr int NWS = RES ? (NKR > 1 ? NKR : 1) : 2;
+  u32x4 wr[NWS][UPT];
   int goff[UPT];
   int loff[UPT];
 #pragma unroll
   for (int u = 0; u < UPT; ++u) {
-    const int unit = tid + 512 * u;
+    const int unit = tid + NTH * u;
     const int p = unit / (OC * RB / 16);
     const int rem = unit - p * (OC * RB / 16);
     const int row = rem / (RB / 16);
@@ -276,16 +282,24 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     goff[u] = (unit < NU) ? (int)(p * wplane + (int64_t)row * Ci_pad * EB + ch * 16) : 0;
     loff[u] = (unit < NU) ? p * OC * RB + wl_off<RB>(row, ch * 16) : 0;
   }
-  auto issue_w = [&](int oc, int kc) {
-    const char* blk = wbase + ((int64_t)oc * OC * Ci_pad + kc * KSTEP) * EB;
+  // Buffer loads: per-thread offsets stay in fixed VGPRs and the block offset
+  // goes in the scalar offset, so issuing a load writes no VGPR before it (an
+  // address computed into the destination registers made the compiler wait
+  // for every load in flight first).  The spectrum is below 2^31 bytes.
+  const __amdgpu_buffer_rsrc_t wrs = make_rsrc(wbase, (uint32_t)((int64_t)T * wplane));
+  auto issue_w = [&](auto set, int oc, int kc) __attribute__((always_inline)) {
+    constexpr int S = decltype(set)::value;
+    const int boff = (oc * OC * Ci_pad + kc * KSTEP) * EB;
 #pragma unroll
     for (int u = 0; u < UPT; ++u)
-      if (NU % 512 == 0 || tid + 512 * u < NU) wr[u] = *reinterpret_cast<const u32x4*>(blk + goff[u]);
+      if (NU % NTH == 0 || tid + NTH * u < NU)
+        wr[S][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, goff[u], boff, 0));
   };
-  auto store_w = [&](int blk) {
+  auto store_w = [&](auto set, int blk) __attribute__((always_inline)) {
+    constexpr int S = decltype(set)::value;
 #pragma unroll
     for (int u = 0; u < UPT; ++u)
-      if (NU % 512 == 0 || tid + 512 * u < NU) *reinterpret_cast<u32x4*>(wlb + blk * WBLK + loff[u]) = wr[u];
+      if (NU % NTH == 0 || tid + NTH * u < NU) *reinterpret_cast<u32x4*>(wlb + blk * WBLK + loff[u]) = wr[S][u];
   };
 
   // ---- raw activations of (round m, step kc): HKW channels of this lane's row.
@@ -294,8 +308,8 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   // because the grid keeps one round of slack.
   uint32_t xr[NBH / 4];
   int xr_valid = 0;  // valid elements in xr (the rest belong to the next row)
-  auto issue_x = [&](int m, int kc) {
-    const int q = m * 64 + 4 * li + rg;
+  auto issue_x = [&](int m, int kc) __attribute__((always_inline)) {
+    const int q = m * kGemmRoundRows + kGemmPairs * li + rg;
     const int c0 = oh * (KSTEP / 2) + g * HKW;  // channel within the step
     const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
     const int cabs = kc * KSTEP + c0;
@@ -303,7 +317,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr);
   };
   // transform and publish this lane's part of the step's operand spectrum
-  auto publish_x = [&](int xb) {
+  auto publish_x = [&](int xb) __attribute__((always_inline)) {
     mask_raw<NBH, EB>(xr_valid, xr);
     float P[T][HKW];
     raw_to_planes<T, F16, HKW>(xr, P);
@@ -382,7 +396,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
   // D = X W^T: lane (g, i) holds output channel ot*16 + i of the pair's rows
   // 4g .. 4g+3.  The 16 lanes of a lane group write 16 consecutive channels of
   // one row, a contiguous span of 16*T elements (whole cache lines).
-  auto epilogue = [&](int m, int oc) {
+  auto epilogue = [&](int m, int oc) __attribute__((always_inline)) {
 #pragma unroll
     for (int a = 0; a < OT; ++a) {
       const int ot = oh * OT + a;
@@ -394,7 +408,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t q = (int64_t)m * 64 + 4 * (4 * g + r) + rg;
+        const int64_t q = (int64_t)m * kGemmRoundRows + kGemmPairs * (4 * g + r) + rg;
         float Pl[T], ul[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
@@ -406,7 +420,7 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     }
   };
 
-  auto zero_acc = [&]() {
+  auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < T; ++p)
 #pragma unroll
@@ -425,12 +439,12 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
       // block b = oc * nks + kc holds planes x OC rows x KSTEP channels; unit
       // u of the arena is 16 bytes of it.  Four loads in flight per thread.
       const int n_units = n_oc * nks * NU;
-      for (int u0 = tid; u0 < n_units; u0 += 4 * 512) {
+      for (int u0 = tid; u0 < n_units; u0 += 4 * NTH) {
         u32x4 v[4];
         int lo[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          const int u = u0 + 512 * j;
+          const int u = u0 + NTH * j;
           lo[j] = -1;
           if (u < n_units) {
             const int blk = u / NU;
@@ -470,52 +484,75 @@ __global__ __launch_bounds__(512) void eql_gemm_kernel(const void* __restrict__ 
     return;
   }
 
-  // Streamed weights (running step s; weights of s in block s & 1, spectrum
-  // of s in xl[s & 1]):
-  //   publish X(s) to xl[s & 1]; barrier: X(s) and W(s) visible, and every
-  //     wave is done with step s-1, so buffers (s+1) & 1 are free
-  //   issue loads W(s+1) -> registers, activations for s+1
-  //   read operands, MFMA(s); W(s+1) -> block (s+1) & 1
-  issue_w(0, 0);
-  issue_x(0, 0);
-  store_w(0);
-  for (int m = 0; m < rounds; ++m) {
-    for (int oc = 0; oc < n_oc; ++oc) {
-      zero_acc();
-      if constexpr (RES) {
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  if constexpr (RES) {
+    // Resident spectrum: per o-chunk, NKR steps with the spectrum of step kc in
+    // xres[kc].  Weight block (oc, kc) lives in register set kc: it is issued
+    // NKR steps ahead, at step (oc - 1, kc), and stored to LDS at the end of
+    // the step before its own.
+    const int total = rounds * n_oc * NKR;
+    int s = 0;
+    static_for<NKR>([&](auto ki) { issue_w(ki, 0, decltype(ki)::value); });
+    issue_x(0, 0);
+    store_w(I0{}, 0);
+    for (int m = 0; m < rounds; ++m) {
+      for (int oc = 0; oc < n_oc; ++oc) {
+        zero_acc();
         static_for<NKR>([&](auto kci) {
           constexpr int kc = decltype(kci)::value;
-          int noc = oc, nkc = kc + 1, nm = m;
-          if (nkc == NKR) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
-          const bool more = nm < rounds;
           if (oc == 0) publish_x(buf);
           __syncthreads();
-          if (more) issue_w(noc, nkc);
+          if (s + NKR < total) issue_w(kci, oc + 1 < n_oc ? oc + 1 : 0, kc);
           if (oc == 0) {
             if (kc + 1 < NKR) issue_x(m, kc + 1);
             else issue_x(m + 1, 0);
             read_x(buf, xres[kc]);
           }
           mma_step(oc, buf, xres[kc]);
-          if (more) store_w(buf ^ 1);
+          if (s + 1 < total) store_w(std::integral_constant<int, (kc + 1) % NKR>{}, buf ^ 1);
           buf ^= 1;
+          ++s;
         });
-      } else {
-        for (int kc = 0; kc < nks; ++kc) {
-          int noc = oc, nkc = kc + 1, nm = m;
-          if (nkc == nks) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
-          const bool more = nm < rounds;
-          publish_x(buf);
-          __syncthreads();
-          if (more) issue_w(noc, nkc);
-          issue_x(nm, nkc);
-          read_x(buf, bcur);
-          mma_step(oc, buf, bcur);
-          if (more) store_w(buf ^ 1);
-          buf ^= 1;
-        }
+        epilogue(m, oc);
       }
-      epilogue(m, oc);
+    }
+  } else {
+    // Streamed weights, step s with coordinates (m, oc, kc); weight block of
+    // step s in register set s & 1 and LDS buffer s & 1, spectrum in xl[s & 1]:
+    //   publish X(s); barrier: X(s), W(s) visible, step s-1 finished everywhere
+    //   issue W(s+2) into set s & 1 (stored to LDS at step s-1), activations
+    //     of s+1; MFMA(s); store W(s+1) (issued at step s-1) to LDS (s+1) & 1
+    // so each weight load has two steps to arrive, and its wait never covers
+    // the stores of an epilogue issued after it.
+    const int total = rounds * n_oc * nks;
+    int s = 0, m = 0, oc = 0, kc = 0;
+    issue_w(I0{}, 0, 0);
+    issue_x(0, 0);
+    if (total > 1) issue_w(I1{}, nks > 1 ? 0 : (n_oc > 1 ? 1 : 0), nks > 1 ? 1 : 0);
+    store_w(I0{}, 0);
+    auto step = [&](auto par) __attribute__((always_inline)) {
+      constexpr int P = decltype(par)::value;
+      if (kc == 0) zero_acc();
+      int m1 = m, oc1 = oc, kc1 = kc + 1;  // step s+1
+      if (kc1 == nks) { kc1 = 0; if (++oc1 == n_oc) { oc1 = 0; ++m1; } }
+      int oc2 = oc1, kc2 = kc1 + 1;        // weight block of step s+2
+      if (kc2 == nks) { kc2 = 0; if (++oc2 == n_oc) oc2 = 0; }
+      publish_x(P);
+      __syncthreads();
+      if (s + 2 < total) issue_w(par, oc2, kc2);
+      issue_x(m1, kc1);
+      read_x(P, bcur);
+      mma_step(oc, P, bcur);
+      if (s + 1 < total) store_w(std::integral_constant<int, 1 - P>{}, 1 - P);
+      if (kc == nks - 1) epilogue(m, oc);
+      m = m1; oc = oc1; kc = kc1; ++s;
+    };
+    while (true) {
+      step(I0{});
+      if (s >= total) break;
+      step(I1{});
+      if (s >= total) break;
     }
   }
 }

@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "eql_config.h"
+
 namespace eqk {
 
 inline int round_up(int v, int m) { return (v + m - 1) / m * m; }
@@ -32,9 +34,9 @@ constexpr int gemm_kw_c(int T, bool f16) {
 inline int gemm_kw(int T, bool f16) { return gemm_kw_c(T, f16); }
 constexpr int gemm_rb_c(int T, bool f16) { return 4 * gemm_kw_c(T, f16) * (f16 ? 2 : 4); }
 // LDS of one workgroup with n_wblocks weight blocks: two spectrum buffers of
-// 64*T rows and the blocks of 32*OT*T rows, each row RB bytes.
+// 16*pairs*T rows and the blocks of 32*OT*T rows, each row RB bytes.
 constexpr int gemm_lds_c(int T, bool f16, int OT, int n_wblocks) {
-  return (2 * 64 * T + n_wblocks * 32 * OT * T) * gemm_rb_c(T, f16);
+  return (2 * kGemmRoundRows * T + n_wblocks * 32 * OT * T) * gemm_rb_c(T, f16);
 }
 // o-tiles per wave: at most 96 accumulator floats per lane (T*OT*4), and two
 // weight blocks plus the spectrum buffers within the LDS.

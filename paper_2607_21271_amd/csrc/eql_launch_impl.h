@@ -11,10 +11,10 @@ namespace eqk {
 template <int T, bool F16>
 hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s) {
   const WspecDims d = wspec_dims(T, Cin, Cout, F16);
-  const int64_t total = (int64_t)d.CoF * d.CiF + (int64_t)d.CinB * d.CoutB;
-  const unsigned blocks = (unsigned)((total + 255) / 256);
-  hipLaunchKernelGGL((eql_wspec_kernel<T, F16>), dim3(blocks), dim3(256), 0, s, w, wspec, Cin,
-                     Cout, d.CoF, d.CiF, d.CinB, d.CoutB);
+  const int omax = d.CoF > d.CoutB ? d.CoF : d.CoutB;  // tiles cover both layouts
+  const int cmax = d.CiF > d.CinB ? d.CiF : d.CinB;
+  hipLaunchKernelGGL((eql_wspec_kernel<T, F16>), dim3((unsigned)(omax / 16), (unsigned)(cmax / 16)),
+                     dim3(256), 0, s, w, wspec, Cin, Cout, d.CoF, d.CiF, d.CinB, d.CoutB);
   return hipGetLastError();
 }
 
@@ -60,8 +60,8 @@ hipError_t gemm_variant(const GemmArgs& a) {
     hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
-  const int grid = persistent_grid((const void*)k, 512, lds, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
-  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(512), lds, a.stream, a.in, a.wsp, a.bias, a.out,
+  const int grid = persistent_grid((const void*)k, kGemmThreads, lds, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
+  hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kGemmThreads), lds, a.stream, a.in, a.wsp, a.bias, a.out,
                      a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
   return hipGetLastError();
 }
@@ -105,10 +105,11 @@ hipError_t gemm_t(const GemmArgs& a) {
 template <int T, bool F16, int WGC, int CT, int OTW>
 hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
   if (p.S > 0) {
-    const int64_t n_tiles = (int64_t)p.S * p.n_ct * p.n_ot;
-    hipLaunchKernelGGL((eql_wgrad_kernel<T, F16, WGC, 8 / WGC, CT, OTW>), dim3((unsigned)n_tiles),
+    // whole groups of 8 splits (see the tile order in eql_wgrad_kernel)
+    const int64_t n_blocks = (int64_t)(p.S + 7) / 8 * 8 * p.n_ct * p.n_ot;
+    hipLaunchKernelGGL((eql_wgrad_kernel<T, F16, WGC, 8 / WGC, CT, OTW>), dim3((unsigned)n_blocks),
                        dim3(512), 0, a.stream, a.x, a.dy, a.part, a.db ? a.dbpart : nullptr, a.N,
-                       a.Cin, a.Cout, p.rows_per_split, p.n_ct, p.n_ot, (int)n_tiles, p.Cin_pad,
+                       a.Cin, a.Cout, p.rows_per_split, p.n_ct, p.n_ot, p.S, p.Cin_pad,
                        p.Cout_pad);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

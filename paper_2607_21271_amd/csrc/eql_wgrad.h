@@ -53,7 +53,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
                                                         float* __restrict__ part,
                                                         float* __restrict__ dbpart, int64_t N,
                                                         int Cin, int Cout, int64_t rows_per_split,
-                                                        int n_ct, int n_ot, int n_tiles, int Cin_pad,
+                                                        int n_ct, int n_ot, int n_splits, int Cin_pad,
                                                         int Cout_pad) {
   using Bn = Bins<T>;
   constexpr int EB = F16 ? 2 : 4;
@@ -76,9 +76,17 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   __shared__ __attribute__((aligned(16))) char ds[T * BO * RB];
   __shared__ float dred[512];
 
+  // XCD-aware tile order: workgroup b runs on XCD b % 8, so the tiles of one
+  // split (which all read the split's rows of x and dy) are given the same
+  // b % 8 and consecutive b / 8; they then share one L2 and the rows are read
+  // from HBM once.  The grid holds whole groups of 8 splits; workgroups past
+  // the last split exit before any barrier.
   const int per_split = n_ct * n_ot;
-  const int split = blockIdx.x / per_split;
-  const int rem = blockIdx.x - split * per_split;
+  const int xcd = blockIdx.x & 7;
+  const int j = blockIdx.x >> 3;
+  const int split = (j / per_split) * 8 + xcd;
+  if (split >= n_splits) return;
+  const int rem = j - (j / per_split) * per_split;
   const int ct = rem / n_ot;
   const int ot = rem - ct * n_ot;
   const int64_t n_begin = (int64_t)split * rows_per_split;
