@@ -2,6 +2,7 @@
 // device checks, workspace planning and dispatch to the gfx950 kernels.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdio.h>
 #include <stdlib.h>
 #include <string.h>
 
@@ -21,8 +22,14 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
                                      {2, 1, 3}, {4, 1, 1}, {4, 1, 2}, {4, 1, 3}};
   WgradPlan p{};
   long best = -1;
+  // EQL_WGRAD_VARIANT=wgc,ct,otw forces one variant where it is valid (A/B timing)
+  int fw = 0, fc = 0, fo = 0;
+  if (const char* e = getenv("EQL_WGRAD_VARIANT")) {
+    if (sscanf(e, "%d,%d,%d", &fw, &fc, &fo) != 3) fw = 0;
+  }
   for (const auto& v : kVariants) {
     const int wgc = v[0], ct = v[1], otw = v[2], wgo = 8 / wgc;
+    if (fw && (wgc != fw || ct != fc || otw != fo)) continue;
     if (ct * otw * T * 4 > 96) continue;
     const int BC = wgc * 16 * ct, BO = wgo * 16 * otw;
     if ((long)T * (BC + BO) * 64 > 160 * 1024 - 4096) continue;
@@ -44,7 +51,9 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
     // once, read once) at most half the bytes of x and dy, at least two row
     // chunks per split, and each split's rows addressable with 31 bits.
     const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
-    int64_t s = (256 + tiles - 1) / tiles;
+    int64_t target = 256;
+    if (const char* e = getenv("EQL_WGRAD_TARGET")) target = atoi(e) > 0 ? atoi(e) : 256;
+    int64_t s = (target + tiles - 1) / tiles;
     const double eb = f16 ? 2.0 : 4.0;
     const double in_bytes = (double)N * (Cin + Cout) * T * eb;
     const double part_per_split = (double)T * p.Cout_pad * p.Cin_pad * 4.0;

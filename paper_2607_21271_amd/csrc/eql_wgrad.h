@@ -47,6 +47,17 @@ __device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t rs, uint32_t off
   }
 }
 
+// Item order of the staging threads: a wave takes 8 channels x 8 row pairs, so
+// each of its loads covers 8 rows x 8 channels (whole 128-byte lines for
+// 16-byte items) and its 64 LDS stores, with the chunk swizzle of wl_off, fall
+// on 64 distinct banks.  B (channels in the tile) is a multiple of 8.
+template <int B>
+__device__ __forceinline__ void wgrad_item(int item, int& ch, int& rp) {
+  const int lo = item & 63, hi = item >> 6;
+  ch = (hi % (B / 8)) * 8 + (lo & 7);
+  rp = (hi / (B / 8)) * 8 + (lo >> 3);
+}
+
 template <int T, bool F16, int WGC, int WGO, int CT, int OTW>
 __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__ x,
                                                         const void* __restrict__ dy,
@@ -65,6 +76,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   static_assert(WGC * WGO == 8, "8 waves");
   constexpr int BC = WGC * 16 * CT;
   constexpr int BO = WGO * 16 * OTW;
+  static_assert((KR / 2) % 8 == 0 && BC % 8 == 0 && BO % 8 == 0, "wgrad_item tiling");
   constexpr int NIX = BC * KR / 2;           // (channel, row pair) items of x per chunk
   constexpr int NID = BO * KR / 2;
   constexpr int UX = (NIX + 511) / 512;
@@ -110,13 +122,14 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   constexpr int ITB = T * EB;  // bytes of one (row, channel)
 
   uint32_t rx[UX][RAW], rd[UD][RAW];
-  // item u of this thread: channel (item % B?), row pair (item / B?)
+  // item u of this thread: (channel, row pair) = wgrad_item(tid + 512 u)
   auto issue = [&](int chunk) {
     const int n0 = chunk * KR;  // row offset within the split
 #pragma unroll
     for (int u = 0; u < UX; ++u) {
       const int item = tid + 512 * u;
-      const int c = item % BC, rp = item / BC;
+      int c, rp;
+      wgrad_item<BC>(item, c, rp);
       const int cg = ct * BC + c;
       if ((NIX % 512 == 0 || item < NIX) && cg < Cin) {
 #pragma unroll
@@ -134,7 +147,8 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 #pragma unroll
     for (int u = 0; u < UD; ++u) {
       const int item = tid + 512 * u;
-      const int o = item % BO, rp = item / BO;
+      int o, rp;
+      wgrad_item<BO>(item, o, rp);
       const int og = ot * BO + o;
       if ((NID % 512 == 0 || item < NID) && og < Cout) {
 #pragma unroll
@@ -161,7 +175,8 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
     for (int u = 0; u < UX; ++u) {
       const int item = tid + 512 * u;
       if (NIX % 512 != 0 && item >= NIX) continue;
-      const int c = item % BC, rp = item / BC;
+      int c, rp;
+      wgrad_item<BC>(item, c, rp);
       float P0[T], P1[T];
       {
         constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
@@ -185,7 +200,8 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
     for (int u = 0; u < UD; ++u) {
       const int item = tid + 512 * u;
       if (NID % 512 != 0 && item >= NID) continue;
-      const int o = item % BO, rp = item / BO;
+      int o, rp;
+      wgrad_item<BO>(item, o, rp);
       float P0[T], P1[T];
       {
         constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
@@ -269,21 +285,25 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
     }
   }
   if (ct == 0 && dbpart != nullptr) {
-    // threads with the same o (item % BO) hold partial sums of different rows
+    // thread q's dbacc[u] belongs to output channel o of item q + 512u
+    // (wgrad_item); thread t < BO sums, in a fixed order, the entries of o = t
+    float dsum = 0.0f;
 #pragma unroll
     for (int u = 0; u < UD; ++u) {
       __syncthreads();
       dred[tid] = dbacc[u];
       __syncthreads();
-      if (tid < BO && (NID % 512 == 0 || tid + 512 * u < NID)) {
-        float s = 0.0f;
-        for (int q = tid; q < 512; q += BO)
-          if (NID % 512 == 0 || q + 512 * u < NID) s += dred[q];
-        const int o = (tid + 512 * u) % BO;
-        if (u == 0) dbpart[(int64_t)split * Cout_pad + ot * BO + o] = s;
-        else dbpart[(int64_t)split * Cout_pad + ot * BO + o] += s;
+      if (tid < BO) {
+        for (int w = 0; w < 8; ++w) {
+          if ((w + 8 * u) % (BO / 8) != (tid >> 3)) continue;
+          for (int rl = 0; rl < 8; ++rl) {
+            const int q = w * 64 + rl * 8 + (tid & 7);
+            if (NID % 512 == 0 || q + 512 * u < NID) dsum += dred[q];
+          }
+        }
       }
     }
+    if (tid < BO) dbpart[(int64_t)split * Cout_pad + ot * BO + tid] = dsum;
   }
 }
 
