@@ -84,9 +84,17 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   constexpr int WPR = (T * EB + 3) / 4;      // words of one (row, channel)
   constexpr int RAW = 2 * WPR;               // words of one item (two rows)
 
-  __shared__ __attribute__((aligned(16))) char xs[T * BC * RB];
-  __shared__ __attribute__((aligned(16))) char ds[T * BO * RB];
-  __shared__ float dred[512];
+  // Staging: spectra of one chunk, x planes [p][c][row] then dy planes
+  // [p][o][row].  Double buffered when two copies fit in LDS (DB): then the
+  // transform of chunk ch+1 and the MFMAs of chunk ch run between the same two
+  // barriers, the two waves that share a SIMD in opposite order, so one's VALU
+  // work overlaps the other's MFMAs.  The bias sums reuse the area afterwards.
+  constexpr int XSB = T * BC * RB, DSB = T * BO * RB;
+  constexpr bool DB = 2 * (XSB + DSB) <= 160 * 1024;
+  constexpr int SMEM = (DB ? 2 : 1) * (XSB + DSB);
+  static_assert(SMEM >= 512 * 4, "bias scratch");
+  __shared__ __attribute__((aligned(16))) char smem[SMEM];
+  float* const dred = reinterpret_cast<float*>(smem);
 
   // XCD-aware tile order: workgroup b runs on XCD b % 8, so the tiles of one
   // split (which all read the split's rows of x and dy) are given the same
@@ -123,7 +131,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 
   uint32_t rx[UX][RAW], rd[UD][RAW];
   // item u of this thread: (channel, row pair) = wgrad_item(tid + 512 u)
-  auto issue = [&](int chunk) {
+  auto issue = [&](int chunk) __attribute__((always_inline)) {
     const int n0 = chunk * KR;  // row offset within the split
 #pragma unroll
     for (int u = 0; u < UX; ++u) {
@@ -170,7 +178,9 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
   for (int u = 0; u < UD; ++u) dbacc[u] = 0.0f;
 
   // transform the prefetched items and stage their planes (two rows each)
-  auto publish = [&]() {
+  auto publish = [&](int buf) __attribute__((always_inline)) {
+    char* const xs = smem + buf * (XSB + DSB);
+    char* const ds = xs + XSB;
 #pragma unroll
     for (int u = 0; u < UX; ++u) {
       const int item = tid + 512 * u;
@@ -232,7 +242,9 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 #pragma unroll
       for (int b = 0; b < OTW; ++b) acc[p][a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  auto mma_chunk = [&]() {
+  auto mma_chunk = [&](int buf) __attribute__((always_inline)) {
+    const char* const xs = smem + buf * (XSB + DSB);
+    const char* const ds = xs + XSB;
 #pragma unroll
     for (int b = 0; b < OTW; ++b) {
       const int ol = (wo * OTW + b) * 16 + li;
@@ -260,13 +272,40 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
     }
   };
 
-  if (nchunks > 0) issue(0);
-  for (int ch = 0; ch < nchunks; ++ch) {
-    publish();
-    __syncthreads();                       // spectra of chunk ch visible
-    if (ch + 1 < nchunks) issue(ch + 1);   // in flight during the MFMAs
-    mma_chunk();
-    __syncthreads();                       // xs / ds free for the next chunk
+  if constexpr (DB) {
+    // chunk ch staged in buffer ch & 1; raw loads run two chunks ahead of the MFMAs
+    if (nchunks > 0) {
+      issue(0);
+      publish(0);
+    }
+    if (nchunks > 1) issue(1);
+    const bool transform_first = wave < 4;
+    for (int ch = 0; ch < nchunks; ++ch) {
+      __syncthreads();  // chunk ch staged; every wave done with chunk ch-1's buffer
+      const bool more = ch + 1 < nchunks;
+      if (transform_first) {
+        if (more) {
+          publish((ch + 1) & 1);
+          if (ch + 2 < nchunks) issue(ch + 2);
+        }
+        mma_chunk(ch & 1);
+      } else {
+        mma_chunk(ch & 1);
+        if (more) {
+          publish((ch + 1) & 1);
+          if (ch + 2 < nchunks) issue(ch + 2);
+        }
+      }
+    }
+  } else {
+    if (nchunks > 0) issue(0);
+    for (int ch = 0; ch < nchunks; ++ch) {
+      publish(0);
+      __syncthreads();                       // spectra of chunk ch visible
+      if (ch + 1 < nchunks) issue(ch + 1);   // in flight during the MFMAs
+      mma_chunk(0);
+      __syncthreads();                       // staging free for the next chunk
+    }
   }
 
   // ---- partials: part[split][p][c/4][o][c%4]
