@@ -76,16 +76,26 @@ __host__ __device__ __forceinline__ void static_for(F&& f) {
   static_for_impl(f, std::make_integer_sequence<int, N>{});
 }
 
+// Arithmetic of the transforms, as a policy: F32Ops holds one value per
+// element in fp32 (H2Ops, with the element types below, holds two independent
+// signals in the halves of a packed fp16 register).
+struct F32Ops {
+  using V = float;
+  static __device__ __forceinline__ V zero() { return 0.0f; }
+  static __device__ __forceinline__ V fma(float c, V x, V y) { return __builtin_fmaf(c, x, y); }
+  static __device__ __forceinline__ V mul(float c, V x) { return c * x; }
+};
+
 // acc += C * v for a compile-time constant C; terms with C = 0 vanish and
 // C = +-1 become an add or a subtract.
-template <float C>
-__device__ __forceinline__ void axpy_c(float& acc, float v) {
+template <float C, typename A = F32Ops>
+__device__ __forceinline__ void axpy_c(typename A::V& acc, typename A::V v) {
   if constexpr (C == 1.0f) {
     acc += v;
   } else if constexpr (C == -1.0f) {
     acc -= v;
   } else if constexpr (C != 0.0f) {
-    acc = __builtin_fmaf(C, v, acc);
+    acc = A::fma(C, v, acc);
   }
 }
 
@@ -95,22 +105,23 @@ __device__ __forceinline__ void axpy_c(float& acc, float v) {
 // that each bin takes about T/2 multiply-adds:
 //   Re X_k = v_0 + (-1)^k v_{T/2} + sum_s e_s cos(2 pi k s/T)
 //   Im X_k = -sum_s d_s sin(2 pi k s/T)
-template <int T>
-__device__ __forceinline__ void rdft_direct(const float (&v)[T], float (&P)[T]) {
+template <int T, typename A = F32Ops>
+__device__ __forceinline__ void rdft_direct(const typename A::V (&v)[T], typename A::V (&P)[T]) {
+  using V = typename A::V;
   using B = Bins<T>;
   constexpr int S = B::S;
-  float e[S + 1], d[S + 1];
+  V e[S + 1], d[S + 1];
   static_for<S>([&](auto si) {
     constexpr int s = decltype(si)::value + 1;
     e[s] = v[s] + v[T - s];
     d[s] = v[s] - v[T - s];
   });
-  float a = v[0];
+  V a = v[0];
   static_for<S>([&](auto si) { a += e[decltype(si)::value + 1]; });
   if constexpr (B::kEven) a += v[T / 2];
   P[0] = a;
   if constexpr (B::kEven) {
-    float b = v[0];
+    V b = v[0];
     static_for<S>([&](auto si) {
       constexpr int s = decltype(si)::value + 1;
       if constexpr (s & 1) b -= e[s]; else b += e[s];
@@ -120,12 +131,12 @@ __device__ __forceinline__ void rdft_direct(const float (&v)[T], float (&P)[T]) 
   }
   static_for<B::K>([&](auto ki) {
     constexpr int k = decltype(ki)::value + 1;
-    float re = v[0];
-    float im = 0.0f;
+    V re = v[0];
+    V im = A::zero();
     static_for<S>([&](auto si) {
       constexpr int s = decltype(si)::value + 1;
-      axpy_c<(float)cos2pi((long)k * s, T)>(re, e[s]);
-      axpy_c<(float)-sin2pi((long)k * s, T)>(im, d[s]);
+      axpy_c<(float)cos2pi((long)k * s, T), A>(re, e[s]);
+      axpy_c<(float)-sin2pi((long)k * s, T), A>(im, d[s]);
     });
     if constexpr (B::kEven) {
       if constexpr (k & 1) re -= v[T / 2]; else re += v[T / 2];
@@ -181,8 +192,9 @@ __device__ __forceinline__ void irdft_direct(const float (&P)[T], float (&u)[T])
 // FFT forms for T = 4, 8, 16 (same planes, same results up to rounding order).
 //
 // T = 4: two length-2 butterflies.  Planes: 0 X0, 1 X2, 2 Re X1, 3 Im X1.
-__device__ __forceinline__ void rdft4(const float (&v)[4], float (&P)[4]) {
-  const float a0 = v[0] + v[2], a1 = v[1] + v[3];
+template <typename A = F32Ops>
+__device__ __forceinline__ void rdft4(const typename A::V (&v)[4], typename A::V (&P)[4]) {
+  const typename A::V a0 = v[0] + v[2], a1 = v[1] + v[3];
   P[0] = a0 + a1;
   P[1] = a0 - a1;
   P[2] = v[0] - v[2];
@@ -200,19 +212,21 @@ __device__ __forceinline__ void irdft4(const float (&P)[4], float (&u)[4]) {
 // twiddled DFT4 of the differences for the odd bins.
 // Planes: 0 X0, 1 X4, 2/3 Re/Im X1, 4/5 Re/Im X2, 6/7 Re/Im X3.
 constexpr float kR2 = 0.70710678118654752440f;  // 1/sqrt(2)
-__device__ __forceinline__ void rdft8(const float (&v)[8], float (&P)[8]) {
-  const float a0 = v[0] + v[4], a1 = v[1] + v[5], a2 = v[2] + v[6], a3 = v[3] + v[7];
-  const float b0 = v[0] - v[4], b1 = v[1] - v[5], b2 = v[2] - v[6], b3 = v[3] - v[7];
-  const float s02 = a0 + a2, s13 = a1 + a3;
+template <typename A = F32Ops>
+__device__ __forceinline__ void rdft8(const typename A::V (&v)[8], typename A::V (&P)[8]) {
+  using V = typename A::V;
+  const V a0 = v[0] + v[4], a1 = v[1] + v[5], a2 = v[2] + v[6], a3 = v[3] + v[7];
+  const V b0 = v[0] - v[4], b1 = v[1] - v[5], b2 = v[2] - v[6], b3 = v[3] - v[7];
+  const V s02 = a0 + a2, s13 = a1 + a3;
   P[0] = s02 + s13;
   P[1] = s02 - s13;
   P[4] = a0 - a2;
   P[5] = a3 - a1;
-  const float p = b1 - b3, q = b1 + b3;
-  P[2] = __builtin_fmaf(kR2, p, b0);
-  P[6] = __builtin_fmaf(-kR2, p, b0);
-  P[3] = __builtin_fmaf(-kR2, q, -b2);
-  P[7] = __builtin_fmaf(-kR2, q, b2);
+  const V p = b1 - b3, q = b1 + b3;
+  P[2] = A::fma(kR2, p, b0);
+  P[6] = A::fma(-kR2, p, b0);
+  P[3] = A::fma(-kR2, q, -b2);
+  P[7] = A::fma(-kR2, q, b2);
 }
 // Inverse: even outputs from X0+X4, Re X2 and the sums/differences of bins 1
 // and 3; odd outputs from X0-X4, Im X2 and bins 1, 3 rotated by e^{i pi/4}.
@@ -237,12 +251,14 @@ __device__ __forceinline__ void irdft8(const float (&P)[8], float (&u)[8]) {
 // T = 16: two DFT8 of the even and odd samples, combined with the twiddles
 // w^k = e^{-i pi k/8}: X_k = E_k + w^k O_k and X_{8-k} = conj(E_k - w^k O_k).
 // Planes: 0 X0, 1 X8, 2k/2k+1 Re/Im X_k for k = 1..7.
-__device__ __forceinline__ void rdft16(const float (&v)[16], float (&P)[16]) {
-  float ve[8], vo[8], E[8], O[8];
+template <typename A = F32Ops>
+__device__ __forceinline__ void rdft16(const typename A::V (&v)[16], typename A::V (&P)[16]) {
+  using V = typename A::V;
+  V ve[8], vo[8], E[8], O[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) { ve[i] = v[2 * i]; vo[i] = v[2 * i + 1]; }
-  rdft8(ve, E);
-  rdft8(vo, O);
+  rdft8<A>(ve, E);
+  rdft8<A>(vo, O);
   // E, O planes: 0 X0, 1 X4, 2/3 X1, 4/5 X2, 6/7 X3 (length-8 spectra)
   P[0] = E[0] + O[0];
   P[1] = E[0] - O[0];
@@ -252,22 +268,22 @@ __device__ __forceinline__ void rdft16(const float (&v)[16], float (&P)[16]) {
   constexpr float c1 = 0.92387953251128675613f, s1 = 0.38268343236508977173f;  // cos, sin(pi/8)
   // k = 1: Z = w O1 = (c - i s)(Or + i Oi)
   {
-    const float zr = __builtin_fmaf(c1, O[2], s1 * O[3]);
-    const float zi = __builtin_fmaf(c1, O[3], -s1 * O[2]);
+    const V zr = A::fma(c1, O[2], A::mul(s1, O[3]));
+    const V zi = A::fma(c1, O[3], A::mul(-s1, O[2]));
     P[2] = E[2] + zr; P[3] = E[3] + zi;      // X1
     P[14] = E[2] - zr; P[15] = zi - E[3];    // X7 = conj(E1 - Z)
   }
   // k = 2: w^2 = (1 - i)/sqrt2, uses E2/O2 planes 4/5
   {
-    const float zr = kR2 * (O[4] + O[5]);
-    const float zi = kR2 * (O[5] - O[4]);
+    const V zr = A::mul(kR2, O[4] + O[5]);
+    const V zi = A::mul(kR2, O[5] - O[4]);
     P[4] = E[4] + zr; P[5] = E[5] + zi;      // X2
     P[12] = E[4] - zr; P[13] = zi - E[5];    // X6
   }
   // k = 3: w^3 = (s - i c), uses E3/O3 planes 6/7
   {
-    const float zr = __builtin_fmaf(s1, O[6], c1 * O[7]);
-    const float zi = __builtin_fmaf(s1, O[7], -c1 * O[6]);
+    const V zr = A::fma(s1, O[6], A::mul(c1, O[7]));
+    const V zi = A::fma(s1, O[7], A::mul(-c1, O[6]));
     P[6] = E[6] + zr; P[7] = E[7] + zi;      // X3
     P[10] = E[6] - zr; P[11] = zi - E[7];    // X5
   }
@@ -315,12 +331,12 @@ __device__ __forceinline__ void irdft16(const float (&P)[16], float (&u)[16]) {
 }
 
 // Dispatch: FFT forms where written, the symmetric direct form otherwise.
-template <int T>
-__device__ __forceinline__ void rdft(const float (&v)[T], float (&P)[T]) {
-  if constexpr (T == 4) rdft4(v, P);
-  else if constexpr (T == 8) rdft8(v, P);
-  else if constexpr (T == 16) rdft16(v, P);
-  else rdft_direct<T>(v, P);
+template <int T, typename A = F32Ops>
+__device__ __forceinline__ void rdft(const typename A::V (&v)[T], typename A::V (&P)[T]) {
+  if constexpr (T == 4) rdft4<A>(v, P);
+  else if constexpr (T == 8) rdft8<A>(v, P);
+  else if constexpr (T == 16) rdft16<A>(v, P);
+  else rdft_direct<T, A>(v, P);
 }
 template <int T>
 __device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
@@ -331,7 +347,9 @@ __device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
 }
 
 // ---------------------------------------------------------------------------
-// Element types.  F16 tensors hold IEEE binary16; arithmetic is fp32.
+// Element types.  F16 tensors hold IEEE binary16.  Their forward transforms
+// run in packed fp16 arithmetic (H2Ops); products accumulate in fp32 and the
+// inverse transforms and the weight spectrum are computed in fp32.
 template <bool F16>
 struct Elem;
 template <>
@@ -346,6 +364,30 @@ struct Elem<false> {
 };
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+
+// Transform arithmetic on two independent signals held in the two halves of
+// packed fp16 registers (v_pk_add/v_pk_fma_f16), twiddles rounded to fp16.
+struct H2Ops {
+  using V = half2v;
+  static __device__ __forceinline__ V zero() { return V{(_Float16)0.0f, (_Float16)0.0f}; }
+  static __device__ __forceinline__ V fma(float c, V x, V y) {
+    const _Float16 h = (_Float16)c;
+    return __builtin_elementwise_fma(V{h, h}, x, y);
+  }
+  static __device__ __forceinline__ V mul(float c, V x) {
+    const _Float16 h = (_Float16)c;
+    return V{h, h} * x;
+  }
+};
+
+// One packed register from two fp16 words: half ha of word a in the low half,
+// half hb of word b in the high half.
+template <int ha, int hb>
+__device__ __forceinline__ half2v pair_halves(uint32_t a, uint32_t b) {
+  constexpr uint32_t sel = (ha ? 0x0302u : 0x0100u) | ((hb ? 0x0706u : 0x0504u) << 16);
+  return __builtin_bit_cast(half2v, __builtin_amdgcn_perm(b, a, sel));
+}
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));

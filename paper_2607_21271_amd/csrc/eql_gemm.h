@@ -182,6 +182,27 @@ __device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (F16
   }
 }
 
+// fp16: the HKW channels of one lane taken in pairs (2j, 2j+1), element t of
+// both in one packed register, and transformed together in fp16 arithmetic;
+// W[p][j] is then plane p of the pair, the word that is staged.  Element t of
+// channel c is half (c*T + t) % 2 of raw word (c*T + t) / 2.
+template <int T, int HKW>
+__device__ __forceinline__ void raw_to_packed_planes(const uint32_t (&r)[HKW * T / 2],
+                                                     uint32_t (&W)[T][HKW / 2]) {
+  static_for<HKW / 2>([&](auto ji) {
+    constexpr int j = decltype(ji)::value;
+    half2v v[T], P[T];
+    static_for<T>([&](auto ti) {
+      constexpr int t = decltype(ti)::value;
+      constexpr int ia = (2 * j) * T + t, ib = (2 * j + 1) * T + t;
+      v[t] = pair_halves<ia % 2, ib % 2>(r[ia / 2], r[ib / 2]);
+    });
+    rdft<T, H2Ops>(v, P);
+#pragma unroll
+    for (int p = 0; p < T; ++p) W[p][j] = __builtin_bit_cast(uint32_t, P[p]);
+  });
+}
+
 // How the weight blocks reach LDS (MODE):
 //   kStream  two block buffers; the block of the next step is prefetched into
 //            registers while the current one feeds the MFMAs
@@ -245,7 +266,7 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: branches on it stay scalar
   const int rg = wave >> 1;
   const int oh = wave & 1;
   const int g = lane >> 4;
@@ -319,19 +340,23 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   // transform and publish this lane's part of the step's operand spectrum
   auto publish_x = [&](int xb) __attribute__((always_inline)) {
     mask_raw<NBH, EB>(xr_valid, xr);
+    const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
+    if constexpr (F16) {
+      uint32_t W[T][HKW / 2];
+      raw_to_packed_planes<T, HKW>(xr, W);
+#pragma unroll
+      for (int p = 0; p < T; ++p) {
+        char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
+        if constexpr (HKW == 4) *reinterpret_cast<u32x2*>(dst) = u32x2{W[p][0], W[p][1]};
+        else *reinterpret_cast<uint32_t*>(dst) = W[p][0];
+      }
+      return;
+    }
     float P[T][HKW];
     raw_to_planes<T, F16, HKW>(xr, P);
-    const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
 #pragma unroll
     for (int p = 0; p < T; ++p) {
-      if constexpr (F16) {
-        uint32_t w[HKW / 2];
-#pragma unroll
-        for (int j = 0; j < HKW / 2; ++j) w[j] = pack2<true>(P[p][2 * j], P[p][2 * j + 1]);
-        char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
-        if constexpr (HKW == 4) *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
-        else *reinterpret_cast<uint32_t*>(dst) = w[0];
-      } else {
+      {
         char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
         if constexpr (HKW == 4) {
           *reinterpret_cast<u32x4*>(dst) = u32x4{__builtin_bit_cast(uint32_t, P[p][0]), __builtin_bit_cast(uint32_t, P[p][1]),
@@ -412,9 +437,9 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
         float Pl[T], ul[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
+        // a constant added to every group position is T times it added to bin 0
+        Pl[0] = __builtin_fmaf((float)T, bv, Pl[0]);
         irdft<T>(Pl, ul);
-#pragma unroll
-        for (int t = 0; t < T; ++t) ul[t] += bv;
         if (q < len && o < Co) store_run<F16, T>(out, ((r0 + q) * Co + o) * T, true, T, ul);
       }
     }

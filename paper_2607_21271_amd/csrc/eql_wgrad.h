@@ -47,6 +47,33 @@ __device__ __forceinline__ void load_row(__amdgpu_buffer_rsrc_t rs, uint32_t off
   }
 }
 
+// Spectra of the two rows of one item.  fp16: element t of both rows in one
+// packed register (row 0 low), transformed together in fp16 arithmetic, so
+// plane p comes out as the staged word (row 0, row 1).  fp32: one transform
+// per row.  Each row's element t sits in raw word t / 2 (fp16, half t % 2) or
+// t (fp32) of its WPR words.
+template <int T>
+__device__ __forceinline__ void transform_pair(const uint32_t (&r)[2 * ((2 * T + 3) / 4)], half2v (&P)[T]) {
+  constexpr int WPR = (2 * T + 3) / 4;
+  half2v v[T];
+  static_for<T>([&](auto ti) {
+    constexpr int t = decltype(ti)::value;
+    v[t] = pair_halves<t % 2, t % 2>(r[t / 2], r[WPR + t / 2]);
+  });
+  rdft<T, H2Ops>(v, P);
+}
+template <int T>
+__device__ __forceinline__ void transform_rows(const uint32_t (&r)[2 * T], float (&P0)[T], float (&P1)[T]) {
+  float v0[T], v1[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    v0[t] = __builtin_bit_cast(float, r[t]);
+    v1[t] = __builtin_bit_cast(float, r[T + t]);
+  }
+  rdft<T>(v0, P0);
+  rdft<T>(v1, P1);
+}
+
 // Item order of the staging threads: a wave takes 8 channels x 8 row pairs, so
 // each of its loads covers 8 rows x 8 channels (whole 128-byte lines for
 // 16-byte items) and its 64 LDS stores, with the chunk swizzle of wl_off, fall
@@ -187,23 +214,19 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       if (NIX % 512 != 0 && item >= NIX) continue;
       int c, rp;
       wgrad_item<BC>(item, c, rp);
-      float P0[T], P1[T];
-      {
-        constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
-        float f[RAW * EPW], v[T];
-        raw_to_floats<F16, RAW>(rx[u], f);
+      if constexpr (F16) {
+        half2v P[T];
+        transform_pair<T>(rx[u], P);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = f[t];
-        rdft<T>(v, P0);
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<uint32_t*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) = __builtin_bit_cast(uint32_t, P[p]);
+      } else {
+        float P0[T], P1[T];
+        transform_rows<T>(rx[u], P0, P1);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = f[WPR * EPW + t];
-        rdft<T>(v, P1);
-      }
-#pragma unroll
-      for (int p = 0; p < T; ++p) {
-        char* dst = &xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)];
-        if constexpr (F16) *reinterpret_cast<uint32_t*>(dst) = pack2<true>(P0[p], P1[p]);
-        else *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<u32x2*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) =
+              u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
       }
     }
 #pragma unroll
@@ -212,24 +235,22 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       if (NID % 512 != 0 && item >= NID) continue;
       int o, rp;
       wgrad_item<BO>(item, o, rp);
-      float P0[T], P1[T];
-      {
-        constexpr int EPW = F16 ? 2 : 1;  // elements per raw word
-        float f[RAW * EPW], v[T];
-        raw_to_floats<F16, RAW>(rd[u], f);
+      if constexpr (F16) {
+        half2v P[T];
+        transform_pair<T>(rd[u], P);
+        // bin 0 of both rows, summed in fp32
+        dbacc[u] = __builtin_amdgcn_fdot2(P[0], half2v{(_Float16)1.0f, (_Float16)1.0f}, dbacc[u], false);
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = f[t];
-        rdft<T>(v, P0);
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<uint32_t*>(&ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)]) = __builtin_bit_cast(uint32_t, P[p]);
+      } else {
+        float P0[T], P1[T];
+        transform_rows<T>(rd[u], P0, P1);
+        dbacc[u] += P0[0] + P1[0];
 #pragma unroll
-        for (int t = 0; t < T; ++t) v[t] = f[WPR * EPW + t];
-        rdft<T>(v, P1);
-      }
-      dbacc[u] += P0[0] + P1[0];
-#pragma unroll
-      for (int p = 0; p < T; ++p) {
-        char* dst = &ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)];
-        if constexpr (F16) *reinterpret_cast<uint32_t*>(dst) = pack2<true>(P0[p], P1[p]);
-        else *reinterpret_cast<u32x2*>(dst) = u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<u32x2*>(&ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)]) =
+              u32x2{__builtin_bit_cast(uint32_t, P0[p]), __builtin_bit_cast(uint32_t, P1[p])};
       }
     }
   };
