@@ -114,6 +114,44 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
 
+// One lane's L contiguous output elements through a buffer resource, at byte
+// offset off; a lane passes kDropOffset (past any resource) to store nothing.
+// No branch skips a store, so every path through a loop issues the same
+// memory operations and the compiler's memory-counter waits stay exact.
+constexpr uint32_t kDropOffset = 0x80000000u;
+template <bool F16, int L>
+__device__ __forceinline__ void store_run_rsrc(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float (&v)[L]) {
+  using E = typename Elem<F16>::T;
+  constexpr int EBY = Elem<F16>::bytes;
+  constexpr int NB = L * EBY;
+  constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
+  constexpr int PER = VEC / EBY;
+#pragma unroll
+  for (int s = 0; s < L / PER; ++s) {
+    E tmp[PER];
+#pragma unroll
+    for (int q = 0; q < PER; ++q) tmp[q] = (E)v[s * PER + q];
+    const uint32_t o = off + s * VEC;
+    if constexpr (VEC == 16) {
+      u32x4 w;
+      __builtin_memcpy(&w, tmp, 16);
+      __builtin_amdgcn_raw_buffer_store_b128(w, rs, o, 0, 0);
+    } else if constexpr (VEC == 8) {
+      u32x2 w;
+      __builtin_memcpy(&w, tmp, 8);
+      __builtin_amdgcn_raw_buffer_store_b64(w, rs, o, 0, 0);
+    } else if constexpr (VEC == 4) {
+      uint32_t w;
+      __builtin_memcpy(&w, tmp, 4);
+      __builtin_amdgcn_raw_buffer_store_b32(w, rs, o, 0, 0);
+    } else {
+      uint16_t w;
+      __builtin_memcpy(&w, tmp, 2);
+      __builtin_amdgcn_raw_buffer_store_b16(w, rs, o, 0, 0);
+    }
+  }
+}
+
 // Raw bytes of one lane for one step: NB bytes at byte offset off (+ soff) of
 // the resource, with loads of W bytes (W = 2: 16-bit loads paired into words).
 // The width is a compile-time constant so that every kernel has a single load
@@ -259,7 +297,8 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   constexpr int XBLK = GemmLds<T, F16, OT>::XBLK;  // bytes of one spectrum buffer
   static_assert(KW >= 2, "contraction split");
 
-  // dynamic LDS: xl[2][XBLK], then the weight blocks (2, or n_oc * n_ks for kStat)
+  // dynamic LDS: xl[2][XBLK], then the weight blocks (2 streamed, 2 * NKR with a
+  // resident spectrum, n_oc * n_ks resident)
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char* const xlb = smem;
   char* const wlb = smem + 2 * XBLK;
@@ -327,23 +366,28 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   // Issued unconditionally, also for the round after the last one (those rows
   // lie past the buffer resource and read as zero); offsets stay below 2^31
   // because the grid keeps one round of slack.
-  uint32_t xr[NBH / 4];
-  int xr_valid = 0;  // valid elements in xr (the rest belong to the next row)
-  auto issue_x = [&](int m, int kc) __attribute__((always_inline)) {
+  // raw activation sets (compile-time index): one per contraction step with
+  // a resident spectrum (a round's loads are issued together), else one
+  constexpr int NXS = RES ? NKR : 1;
+  uint32_t xr[NXS][NBH / 4];
+  int xr_valid[NXS];  // valid elements per set (the rest belong to the next row)
+  auto issue_x = [&](auto set, int m, int kc) __attribute__((always_inline)) {
+    constexpr int X = decltype(set)::value;
     const int q = m * kGemmRoundRows + kGemmPairs * li + rg;
     const int c0 = oh * (KSTEP / 2) + g * HKW;  // channel within the step
     const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
     const int cabs = kc * KSTEP + c0;
-    xr_valid = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
-    load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr);
+    xr_valid[X] = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
+    load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr[X]);
   };
   // transform and publish this lane's part of the step's operand spectrum
-  auto publish_x = [&](int xb) __attribute__((always_inline)) {
-    mask_raw<NBH, EB>(xr_valid, xr);
+  auto publish_x = [&](auto set, int xb) __attribute__((always_inline)) {
+    constexpr int X = decltype(set)::value;
+    mask_raw<NBH, EB>(xr_valid[X], xr[X]);
     const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
     if constexpr (F16) {
       uint32_t W[T][HKW / 2];
-      raw_to_packed_planes<T, HKW>(xr, W);
+      raw_to_packed_planes<T, HKW>(xr[X], W);
 #pragma unroll
       for (int p = 0; p < T; ++p) {
         char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
@@ -353,7 +397,7 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
       return;
     }
     float P[T][HKW];
-    raw_to_planes<T, F16, HKW>(xr, P);
+    raw_to_planes<T, F16, HKW>(xr[X], P);
 #pragma unroll
     for (int p = 0; p < T; ++p) {
       {
@@ -375,9 +419,18 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   };
 
   floatx4 acc[T][OT];
+  // With a resident spectrum the subtracted product of each complex bin has
+  // its own accumulator (difference taken in the epilogue) instead of a
+  // negated operand, which would stay live across o-chunks.
+  constexpr int NXA = RES && Bn::K > 0 ? Bn::K : 1;
+  floatx4 accx[NXA][OT];
   FR xres[RES ? NKR : 1][T];
   FR bcur[T];
-  const E* bp = reinterpret_cast<const E*>(bias);
+  const E* __restrict__ bp = reinterpret_cast<const E*>(bias);
+  // output rows of this workgroup as a buffer resource, below 2^31 bytes (the
+  // launcher sizes the grid so)
+  const __amdgpu_buffer_rsrc_t ors =
+      make_rsrc(reinterpret_cast<char*>(out) + r0 * Co * T * EB, (uint32_t)(len * Co * T * EB));
 
   // One step: weights of (oc, kc) in LDS block blk, X the activation spectrum.
   // The sign of each complex product sits on a negated copy of one X plane
@@ -385,11 +438,13 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   //   forward:  Re += Wr Xr + Wi (-Xi),   Im += Wi Xr + Wr Xi
   //   backward: Re += Wr Dr + Wi Di,      Im += Wr Di + Wi (-Dr)
   auto mma_step = [&](int oc, int blk, FR (&X)[T]) {
-    FR Xneg[Bn::K > 0 ? Bn::K : 1];
-    static_for<Bn::K>([&](auto ki) {
-      constexpr int k = decltype(ki)::value + 1;
-      Xneg[k - 1] = frag_neg<F16, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
-    });
+    FR Xneg[Bn::K > 0 && !RES ? Bn::K : 1];
+    if constexpr (!RES) {
+      static_for<Bn::K>([&](auto ki) {
+        constexpr int k = decltype(ki)::value + 1;
+        Xneg[k - 1] = frag_neg<F16, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
+      });
+    }
 #pragma unroll
     for (int a = 0; a < OT; ++a) {
       const int ot = oh * OT + a;                 // o-tile within the chunk
@@ -403,7 +458,17 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
         constexpr int k = decltype(ki)::value + 1;
         constexpr int r = Bn::re(k);
         constexpr int i = Bn::im(k);
-        if constexpr (!BWD) {
+        if constexpr (RES && !BWD) {
+          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<F16, KW>(acc[i][a], X[r], W[i]);
+          frag_mma<F16, KW>(accx[k - 1][a], X[i], W[i]);   // subtracted from Re
+          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
+        } else if constexpr (RES) {
+          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<F16, KW>(acc[r][a], X[i], W[i]);
+          frag_mma<F16, KW>(accx[k - 1][a], X[r], W[i]);   // subtracted from Im
+        } else if constexpr (!BWD) {
           frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
           frag_mma<F16, KW>(acc[i][a], X[r], W[i]);
           frag_mma<F16, KW>(acc[r][a], Xneg[k - 1], W[i]);
@@ -421,45 +486,76 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   // D = X W^T: lane (g, i) holds output channel ot*16 + i of the pair's rows
   // 4g .. 4g+3.  The 16 lanes of a lane group write 16 consecutive channels of
   // one row, a contiguous span of 16*T elements (whole cache lines).
-  auto epilogue = [&](int m, int oc) __attribute__((always_inline)) {
+  // Tiles past Co (zero accumulators) run too, with every store dropped.
+  // With active false the inverse transforms are skipped and the same
+  // stores are issued, all dropped (one wave group of the resident-spectrum
+  // loop runs its epilogue at another point of the iteration than the other;
+  // identical memory operations on both keep the waits exact).
+  auto epilogue_if = [&](int m, int oc, bool active) __attribute__((always_inline)) {
 #pragma unroll
     for (int a = 0; a < OT; ++a) {
       const int ot = oh * OT + a;
-      if (oc * OC + ot * 16 >= Co) continue;  // uniform across the wave
       const int o = oc * OC + ot * 16 + li;
       float bv = 0.0f;
       if constexpr (!BWD) {
-        if (bp != nullptr && o < Co) bv = (float)bp[o];
+        // (a uniform branch; waiting for this load also waits for every
+        // memory operation issued before it)
+        if (bp != nullptr) bv = (float)bp[o < Co ? o : Co - 1];
       }
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t q = (int64_t)m * kGemmRoundRows + kGemmPairs * (4 * g + r) + rg;
-        float Pl[T], ul[T];
+        const int q = m * kGemmRoundRows + kGemmPairs * (4 * g + r) + rg;
+        float ul[T];
 #pragma unroll
-        for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
-        // a constant added to every group position is T times it added to bin 0
-        Pl[0] = __builtin_fmaf((float)T, bv, Pl[0]);
-        irdft<T>(Pl, ul);
-        if (q < len && o < Co) store_run<F16, T>(out, ((r0 + q) * Co + o) * T, true, T, ul);
+        for (int t = 0; t < T; ++t) ul[t] = 0.0f;
+        if (active) {  // uniform across the wave
+          float Pl[T];
+#pragma unroll
+          for (int p = 0; p < T; ++p) Pl[p] = acc[p][a][r];
+          if constexpr (RES) {
+            static_for<Bn::K>([&](auto ki) {
+              constexpr int k = decltype(ki)::value + 1;
+              constexpr int pl = BWD ? Bn::im(k) : Bn::re(k);
+              Pl[pl] -= accx[k - 1][a][r];
+            });
+          }
+          // a constant added to every group position is T times it added to bin 0
+          Pl[0] = __builtin_fmaf((float)T, bv, Pl[0]);
+          irdft<T>(Pl, ul);
+        }
+        const uint32_t off = (active && q < len && o < Co) ? (uint32_t)((q * Co + o) * T * EB) : kDropOffset;
+        store_run_rsrc<F16, T>(ors, off, ul);
       }
     }
   };
+  auto epilogue = [&](int m, int oc) __attribute__((always_inline)) { epilogue_if(m, oc, true); };
 
   auto zero_acc = [&]() __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < T; ++p)
 #pragma unroll
       for (int a = 0; a < OT; ++a) acc[p][a] = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int k = 0; k < NXA; ++k)
+#pragma unroll
+      for (int a = 0; a < OT; ++a) accx[k][a] = floatx4{0.f, 0.f, 0.f, 0.f};
   };
 
+  // Pipelining.  Every global load is issued right after a barrier and
+  // consumed in the same loop iteration, after that step's MFMAs: the
+  // compiler's memory-counter waits are exact only for loads whose issue and
+  // use lie on one straight path (across a loop back edge or around a branch
+  // that issues other memory operations it falls back to waiting for nearly
+  // everything in flight).  Epilogue stores come last in an iteration, so no
+  // wait of that iteration covers them.
   int buf = 0;
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
   if constexpr (MODE == kStat) {
     // All weight blocks into LDS once; then a step only exchanges activations:
-    //   publish X(s) to xl[s & 1]; barrier; issue activations of s+1;
-    //   read operands, MFMA(s).
-    // The activations of s+1 are issued before the epilogue that may end step
-    // s, so waiting for them never waits for that epilogue's stores.
-    issue_x(0, 0);
+    //   barrier; issue activations of s+1; read operands, MFMA(s);
+    //   publish X(s+1) to xl[(s+1) & 1]; epilogue if s ends an o-chunk.
+    issue_x(I0{}, 0, 0);
     {
       // block b = oc * nks + kc holds planes x OC rows x KSTEP channels; unit
       // u of the arena is 16 bytes of it.  Four loads in flight per thread.
@@ -490,17 +586,18 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
           if (lo[j] >= 0) *reinterpret_cast<u32x4*>(wlb + lo[j]) = v[j];
       }
     }
+    publish_x(I0{}, 0);
     for (int m = 0; m < rounds; ++m) {
       for (int oc = 0; oc < n_oc; ++oc) {
         zero_acc();
         for (int kc = 0; kc < nks; ++kc) {
-          int noc = oc, nkc = kc + 1, nm = m;
-          if (nkc == nks) { nkc = 0; ++noc; if (noc == n_oc) { noc = 0; ++nm; } }
-          publish_x(buf);
+          int nkc = kc + 1, nm = m;
+          if (nkc == nks) { nkc = 0; if (oc + 1 == n_oc) ++nm; }
           __syncthreads();
-          issue_x(nm, nkc);  // past the last round: rows beyond the resource read as zero
+          issue_x(I0{}, nm, nkc);  // past the last round: rows beyond the resource read as zero
           read_x(buf, bcur);
           mma_step(oc, oc * nks + kc, bcur);
+          publish_x(I0{}, buf ^ 1);
           buf ^= 1;
         }
         epilogue(m, oc);
@@ -509,37 +606,47 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     return;
   }
 
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
   if constexpr (RES) {
-    // Resident spectrum: per o-chunk, NKR steps with the spectrum of step kc in
-    // xres[kc].  Weight block (oc, kc) lives in register set kc: it is issued
-    // NKR steps ahead, at step (oc - 1, kc), and stored to LDS at the end of
-    // the step before its own.
-    const int total = rounds * n_oc * NKR;
-    int s = 0;
+    // Resident spectrum: the NKR weight blocks of an o-chunk sit together in
+    // one of two LDS regions (block kc of region r at LDS block r * NKR + kc).
+    // Iteration (m, oc):
+    //   oc == 0: the round's raw activations are issued together (for the
+    //     first round in the prologue), then published and read into xres one
+    //     step per barrier; else one barrier
+    //   issue the next o-chunk's blocks (register set kc for block kc); the
+    //   NKR steps run from the current region; the next blocks go to the
+    //   other region.
     static_for<NKR>([&](auto ki) { issue_w(ki, 0, decltype(ki)::value); });
-    issue_x(0, 0);
-    store_w(I0{}, 0);
+    static_for<NKR>([&](auto ki) { issue_x(ki, 0, decltype(ki)::value); });
+    static_for<NKR>([&](auto ki) { store_w(ki, decltype(ki)::value); });
+    int reg = 0;
     for (int m = 0; m < rounds; ++m) {
       for (int oc = 0; oc < n_oc; ++oc) {
+        if (oc == 0) {
+          if (m > 0) static_for<NKR>([&](auto ki) { issue_x(ki, m, decltype(ki)::value); });
+          static_for<NKR>([&](auto kci) {
+            constexpr int kc = decltype(kci)::value;
+            publish_x(kci, buf);
+            __syncthreads();
+            read_x(buf, xres[kc]);
+            buf ^= 1;
+          });
+        } else {
+          __syncthreads();
+        }
+        const int noc = oc + 1 < n_oc ? oc + 1 : 0;
+        static_for<NKR>([&](auto ki) { issue_w(ki, noc, decltype(ki)::value); });
         zero_acc();
         static_for<NKR>([&](auto kci) {
           constexpr int kc = decltype(kci)::value;
-          if (oc == 0) publish_x(buf);
-          __syncthreads();
-          if (s + NKR < total) issue_w(kci, oc + 1 < n_oc ? oc + 1 : 0, kc);
-          if (oc == 0) {
-            if (kc + 1 < NKR) issue_x(m, kc + 1);
-            else issue_x(m + 1, 0);
-            read_x(buf, xres[kc]);
-          }
-          mma_step(oc, buf, xres[kc]);
-          if (s + 1 < total) store_w(std::integral_constant<int, (kc + 1) % NKR>{}, buf ^ 1);
-          buf ^= 1;
-          ++s;
+          mma_step(oc, reg * NKR + kc, xres[kc]);
+          // keep each step's operand reads with its MFMAs (hoisting all of
+          // them ahead would need more registers than two waves per SIMD have)
+          __builtin_amdgcn_sched_barrier(0);
         });
+        static_for<NKR>([&](auto ki) { store_w(ki, (reg ^ 1) * NKR + decltype(ki)::value); });
         epilogue(m, oc);
+        reg ^= 1;
       }
     }
   } else {
@@ -548,12 +655,11 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     //   publish X(s); barrier: X(s), W(s) visible, step s-1 finished everywhere
     //   issue W(s+2) into set s & 1 (stored to LDS at step s-1), activations
     //     of s+1; MFMA(s); store W(s+1) (issued at step s-1) to LDS (s+1) & 1
-    // so each weight load has two steps to arrive, and its wait never covers
-    // the stores of an epilogue issued after it.
+    // so each weight load has two steps to arrive.
     const int total = rounds * n_oc * nks;
     int s = 0, m = 0, oc = 0, kc = 0;
     issue_w(I0{}, 0, 0);
-    issue_x(0, 0);
+    issue_x(I0{}, 0, 0);
     if (total > 1) issue_w(I1{}, nks > 1 ? 0 : (n_oc > 1 ? 1 : 0), nks > 1 ? 1 : 0);
     store_w(I0{}, 0);
     auto step = [&](auto par) __attribute__((always_inline)) {
@@ -563,10 +669,10 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
       if (kc1 == nks) { kc1 = 0; if (++oc1 == n_oc) { oc1 = 0; ++m1; } }
       int oc2 = oc1, kc2 = kc1 + 1;        // weight block of step s+2
       if (kc2 == nks) { kc2 = 0; if (++oc2 == n_oc) oc2 = 0; }
-      publish_x(P);
+      publish_x(I0{}, P);
       __syncthreads();
       if (s + 2 < total) issue_w(par, oc2, kc2);
-      issue_x(m1, kc1);
+      issue_x(I0{}, m1, kc1);
       read_x(P, bcur);
       mma_step(oc, P, bcur);
       if (s + 1 < total) store_w(std::integral_constant<int, 1 - P>{}, 1 - P);

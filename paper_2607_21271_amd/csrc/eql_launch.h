@@ -65,6 +65,11 @@ constexpr int gemm_wide_load_c(int T, bool f16) {
   const int nbh = gemm_kw_c(T, f16) / 2 * T * (f16 ? 2 : 4);
   return nbh % 16 == 0 ? 16 : nbh % 8 == 0 ? 8 : 4;
 }
+// Weight blocks held in LDS: two streamed blocks, two regions of n_ks blocks
+// (resident spectrum), or every block (resident weights).
+constexpr int gemm_wblocks(int mode, int n_oc, int n_ks) {
+  return mode == 2 ? n_oc * n_ks : mode == 1 ? 2 * n_ks : 2;
+}
 // EQL_GEMM_MODE=0/1/2 forces a weight mode where it is valid (tests, A/B timing).
 int gemm_forced_mode();
 inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
@@ -74,7 +79,9 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   p.n_ks = (Ci + p.kstep - 1) / p.kstep;
   const int per_wave = ((Co + 15) / 16 + 1) / 2;  // o-tiles per wave for one chunk
   const int otmax = gemm_otmax(T, f16);
-  const bool res_ok = T <= 8 && p.n_ks <= 3 && p.kw * (f16 ? 2 : 4) <= 16;
+  // resident spectrum: two LDS regions of n_ks weight blocks each
+  const bool res_ok = T <= 8 && p.n_ks <= 3 && p.kw * (f16 ? 2 : 4) <= 16 &&
+                      gemm_lds_c(T, f16, gemm_otres(T, f16), 2 * p.n_ks) <= kLdsBytes;
   if (per_wave <= otmax) {
     p.OT = gemm_ot_round(T, f16, per_wave);
     p.n_oc = 1;
@@ -100,7 +107,7 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   }
   p.OC = 32 * p.OT;
   p.Co_pad = p.n_oc * p.OC;
-  p.lds_bytes = gemm_lds_c(T, f16, p.OT, p.mode == 2 ? p.n_oc * p.n_ks : 2);
+  p.lds_bytes = gemm_lds_c(T, f16, p.OT, gemm_wblocks(p.mode, p.n_oc, p.n_ks));
   return p;
 }
 
@@ -112,7 +119,7 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
 inline void gemm_plan_rows(GemmPlan& p, int64_t N, int T, bool f16, int cus) {
   if (p.mode == 2 && gemm_forced_mode() < 0 && N < (int64_t)2 * 64 * cus) {
     p.mode = 0;
-    p.lds_bytes = gemm_lds_c(T, f16, p.OT, 2);
+    p.lds_bytes = gemm_lds_c(T, f16, p.OT, gemm_wblocks(0, p.n_oc, p.n_ks));
   }
 }
 

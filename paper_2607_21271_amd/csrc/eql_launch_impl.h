@@ -54,13 +54,16 @@ hipError_t gemm_variant(const GemmArgs& a) {
   static_assert(GemmShape<T, F16>::WV == gemm_wide_load_c(T, F16), "host and kernel load widths");
   auto k = eql_gemm_kernel<T, F16, BWD, OT, MODE, NKR, NARROW>;
   const int lds = a.plan.lds_bytes;
-  if (lds != gemm_lds_c(T, F16, OT, MODE == kStat ? a.plan.n_oc * a.plan.n_ks : 2) || lds > kLdsBytes)
+  if (lds != gemm_lds_c(T, F16, OT, gemm_wblocks(MODE, a.plan.n_oc, a.plan.n_ks)) || lds > kLdsBytes ||
+      (MODE == kRes && a.plan.n_ks != NKR))
     return hipErrorInvalidValue;
   if (lds > 64 * 1024) {
     hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     if (e != hipSuccess) return e;
   }
-  const int grid = persistent_grid((const void*)k, kGemmThreads, lds, a.N, (int64_t)a.Ci * T * (F16 ? 2 : 4));
+  // input and output rows are addressed with 31-bit offsets per workgroup
+  const int grid = persistent_grid((const void*)k, kGemmThreads, lds, a.N,
+                                   (int64_t)(a.Ci > a.Co ? a.Ci : a.Co) * T * (F16 ? 2 : 4));
   hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kGemmThreads), lds, a.stream, a.in, a.wsp, a.bias, a.out,
                      a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
   return hipGetLastError();
