@@ -121,27 +121,50 @@ class Workload:
         self.stream = torch.cuda.current_stream()
         self.events = []
 
-    def step(self, i, record):
+    def step(self, i, record, stream=None):
         import torch
         l, ops = self.layer, self.ops
+        st = stream if stream is not None else self.stream
         x, dy, y, dx = self.sets[i % len(self.sets)]
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
         if record:
-            ev[0].record(self.stream)
-        ops.weight_spectrum(self.w, out=self.wspec, stream=self.stream)
+            ev[0].record(st)
+        ops.weight_spectrum(self.w, out=self.wspec, stream=st)
         if record:
-            ev[1].record(self.stream)
-        ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=self.stream)
+            ev[1].record(st)
+        ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=st)
         if record:
-            ev[2].record(self.stream)
-        ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=self.stream)
+            ev[2].record(st)
+        ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=st)
         if record:
-            ev[3].record(self.stream)
+            ev[3].record(st)
         ops.backward_weight(x, dy, l.T, l.Cin, l.Cout, with_bias=l.bias, dw=self.dw, db=self.db,
-                            workspace=self.ws, stream=self.stream)
+                            workspace=self.ws, stream=st)
         if record:
-            ev[4].record(self.stream)
+            ev[4].record(st)
             self.events.append(ev)
+
+    def run_graph(self, steps, warmup):
+        """Whole-step time with each input set's step (the same five launches)
+        captured once in a HIP graph and replayed; exactly ``steps`` steps are
+        timed, bracketed by device synchronisation."""
+        import torch
+        graphs = []
+        for r in range(len(self.sets)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                self.step(r, False, stream=torch.cuda.current_stream())
+            graphs.append(g)
+        for i in range(warmup):
+            graphs[i % len(graphs)].replay()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            graphs[(warmup + i) % len(graphs)].replay()
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        del graphs
+        return (t1 - t0) / steps
 
     def run(self, steps, warmup):
         import torch
@@ -175,10 +198,12 @@ def cpu_baseline(layer, dt, inp, rows_req):
     macs_per_row = 3 * l.T * l.T * l.Cin * l.Cout
     if rows_req <= 0:
         # calibrate on a small slice, then size the sample to about 15 s
-        n0 = max(8, min(l.N, int(2e8 // macs_per_row)))
+        n0 = max(8, min(l.N, int(6e8 // macs_per_row)))
         t0 = time.perf_counter()
         orc.forward(inp.x[:n0], inp.w, inp.b)
-        rate = n0 / max(time.perf_counter() - t0, 1e-6) / 3.0
+        orc.backward_input(inp.dy[:n0], inp.w)
+        orc.backward_weight(inp.x[:n0], inp.dy[:n0], with_bias=inp.b is not None)
+        rate = n0 / max(time.perf_counter() - t0, 1e-6)
         rows_req = int(rate * 15.0)
     n = max(1, min(l.N, rows_req))
     reps = max(1, rows_req // n) if n == l.N else 1
@@ -203,7 +228,10 @@ def measure(layer, dt, args, digest, with_cpu):
     from paper_2607_21271_amd import roofline as rf
     l = layer
     wl = Workload(l, dt, max(1, args.rotate))
-    sec, per = wl.run(args.steps, args.warmup)
+    # eager steps with events between the passes (per-pass times, roofline),
+    # then the same steps replayed from HIP graphs (the step time reported)
+    sec_eager, per = wl.run(args.steps, args.warmup)
+    sec = wl.run_graph(args.steps, args.warmup)
     N = l.N
     flops = 3 * rf.pass_flops(N, l.T, l.Cin, l.Cout)
     dense = 3 * rf.dense_equiv_flops(N, l.T, l.Cin, l.Cout)
@@ -242,6 +270,10 @@ def measure(layer, dt, args, digest, with_cpu):
         "mfma_util_pct": round(100 * flops / sec / (rf.PEAK_MFMA_TFLOPS[dt] * 1e12), 2),
         "tflops_actual": round(flops / sec / 1e12, 2),
         "tflops_dense_equiv": round(dense / sec / 1e12, 2),
+        "timing": "step = one replay of a HIP graph holding that input set's five launches "
+                  "(weight spectrum, forward, input gradient, weight gradient + reduce); "
+                  "pass_us and roofline from an eager run with events between the passes",
+        "eager_ms_per_step": round(sec_eager * 1e3, 4),
         "pass_us": {k: round(v, 2) for k, v in per.items()},
         "pass_hbm_gbs": {k: round(nbytes[k] / (per[k] * 1e-6) / 1e9, 1) for k in per},
         "roofline": roof,
