@@ -13,20 +13,60 @@
 
 namespace eqk {
 
+// Split count of one variant: about one workgroup per CU of a 256-CU device,
+// fp32 partials (written once, read once) at most half the bytes of x and dy,
+// at least two row chunks per split, and each split's rows addressable with
+// 31 bits.  Returns the rows per split (0 when N <= 0) and sets S.
+static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool f16, int KR, int64_t tiles,
+                            int Cin_pad, int Cout_pad, int& S) {
+  if (N <= 0) {
+    S = 0;
+    return 0;
+  }
+  int64_t target = 256;
+  if (const char* e = getenv("EQL_WGRAD_TARGET")) target = atoi(e) > 0 ? atoi(e) : 256;
+  int64_t s = (target + tiles - 1) / tiles;
+  const double eb = f16 ? 2.0 : 4.0;
+  const double in_bytes = (double)N * (Cin + Cout) * T * eb;
+  const double part_per_split = (double)T * Cout_pad * Cin_pad * 4.0;
+  const int64_t s_budget = (int64_t)(in_bytes / (2.0 * part_per_split));
+  if (s > s_budget) s = s_budget;
+  const int64_t max_s = (N + 2 * KR - 1) / (2 * KR);
+  if (s > max_s) s = max_s;
+  if (s < 1) s = 1;
+  // whole groups of 8 splits: the kernel places the tiles of a split on one
+  // XCD (split % 8), and a partial group would add idle workgroups and push
+  // real ones past the first wave of the grid
+  if (s >= 8) s = s / 8 * 8;
+  const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
+  while ((double)((N + s - 1) / s + KR) * row_bytes >= 2147483648.0) ++s;
+  int64_t rows = (N + s - 1) / s;
+  rows = (rows + KR - 1) / KR * KR;
+  S = (int)((N + rows - 1) / rows);
+  return rows;
+}
+
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   // Variants (wave grid rows, c-tiles, o-tiles per wave) with at most 96
-  // accumulator floats per lane: CT * OTW * T * 4 <= 96.  Pick the one that
-  // transforms the fewest (row, channel) pairs per row of input:
-  // n_ct * n_ot * (BC + BO); ties go to fewer workgroup tiles.
+  // accumulator floats per lane: CT * OTW * T * 4 <= 96.  Pick the one with the
+  // smallest estimated time: HBM bytes (x and dy once, the partials written
+  // and read back), plus a quarter of the bytes that the channel tiles re-read
+  // from L2 (x once per o-tile, dy once per c-tile), or the MFMA time of the
+  // padded tiles if larger, divided by the fraction of a 256-CU device the
+  // workgroups fill.  Ties go to fewer workgroup tiles.
   static const int kVariants[][3] = {{2, 1, 1}, {2, 2, 1}, {2, 3, 1}, {2, 1, 2},
                                      {2, 1, 3}, {4, 1, 1}, {4, 1, 2}, {4, 1, 3}};
   WgradPlan p{};
-  long best = -1;
+  double best = -1.0;
   // EQL_WGRAD_VARIANT=wgc,ct,otw forces one variant where it is valid (A/B timing)
   int fw = 0, fc = 0, fo = 0;
   if (const char* e = getenv("EQL_WGRAD_VARIANT")) {
     if (sscanf(e, "%d,%d,%d", &fw, &fc, &fo) != 3) fw = 0;
   }
+  const int KR = f16 ? 32 : 16;
+  const double eb = f16 ? 2.0 : 4.0;
+  const int R = 1 + (T % 2 == 0), K = (T - 1) / 2;
+  const double n = (double)(N > 0 ? N : 0);
   for (const auto& v : kVariants) {
     const int wgc = v[0], ct = v[1], otw = v[2], wgo = 8 / wgc;
     if (fw && (wgc != fw || ct != fc || otw != fo)) continue;
@@ -34,45 +74,29 @@ WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
     const int BC = wgc * 16 * ct, BO = wgo * 16 * otw;
     if ((long)T * (BC + BO) * 64 > 160 * 1024 - 4096) continue;
     const int nct = (Cin + BC - 1) / BC, not_ = (Cout + BO - 1) / BO;
-    const long cost = (long)nct * not_ * (BC + BO) * 1024 + nct * not_;
+    const int64_t tiles = (int64_t)nct * not_;
+    int S = 0;
+    wgrad_splits(N, T, Cin, Cout, f16, KR, tiles, nct * BC, not_ * BO, S);
+    const double part = (double)S * T * (nct * BC) * (not_ * BO) * 4.0;
+    const double hbm = n * (Cin + Cout) * T * eb + 2.0 * part;
+    const double l2 = n * T * eb * ((double)Cin * not_ + (double)Cout * nct);
+    const double flops = 2.0 * (R + 4 * K) * n * (nct * BC) * (not_ * BO);
+    const double mfma_bytes = flops / (f16 ? 2.5e15 : 1.573e14) * 8.0e12;  // as HBM-time bytes
+    double mem = hbm + 0.25 * l2;
+    if (mfma_bytes > mem) mem = mfma_bytes;
+    double fill = (double)S * tiles / 256.0;
+    if (fill > 1.0 || fill <= 0.0) fill = 1.0;
+    const double cost = mem / fill * (1.0 + 1e-9 * tiles);
     if (best < 0 || cost < best) {
       best = cost;
       p.wgc = wgc; p.ct = ct; p.otw = otw; p.BC = BC; p.BO = BO; p.n_ct = nct; p.n_ot = not_;
     }
   }
-  p.KR = f16 ? 32 : 16;
+  p.KR = KR;
   p.Cin_pad = p.n_ct * p.BC;
   p.Cout_pad = p.n_ot * p.BO;
-  if (N <= 0) {
-    p.S = 0;
-    p.rows_per_split = 0;
-  } else {
-    // About one workgroup per CU of a 256-CU device, fp32 partials (written
-    // once, read once) at most half the bytes of x and dy, at least two row
-    // chunks per split, and each split's rows addressable with 31 bits.
-    const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
-    int64_t target = 256;
-    if (const char* e = getenv("EQL_WGRAD_TARGET")) target = atoi(e) > 0 ? atoi(e) : 256;
-    int64_t s = (target + tiles - 1) / tiles;
-    const double eb = f16 ? 2.0 : 4.0;
-    const double in_bytes = (double)N * (Cin + Cout) * T * eb;
-    const double part_per_split = (double)T * p.Cout_pad * p.Cin_pad * 4.0;
-    const int64_t s_budget = (int64_t)(in_bytes / (2.0 * part_per_split));
-    if (s > s_budget) s = s_budget;
-    const int64_t max_s = (N + 2 * p.KR - 1) / (2 * p.KR);
-    if (s > max_s) s = max_s;
-    if (s < 1) s = 1;
-    // whole groups of 8 splits: the kernel places the tiles of a split on one
-    // XCD (split % 8), and a partial group would add idle workgroups and push
-    // real ones past the first wave of the grid
-    if (s >= 8) s = s / 8 * 8;
-    const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
-    while ((double)((N + s - 1) / s + p.KR) * row_bytes >= 2147483648.0) ++s;
-    int64_t rows = (N + s - 1) / s;
-    rows = (rows + p.KR - 1) / p.KR * p.KR;
-    p.rows_per_split = rows;
-    p.S = (int)((N + rows - 1) / rows);
-  }
+  p.rows_per_split = wgrad_splits(N, T, Cin, Cout, f16, KR, (int64_t)p.n_ct * p.n_ot, p.Cin_pad,
+                                  p.Cout_pad, p.S);
   p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
   p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
   return p;

@@ -3,6 +3,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdlib.h>
 
 #include "eql_config.h"
 
@@ -152,6 +153,25 @@ struct WgradPlan {
   size_t part_bytes, dbpart_bytes;
 };
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16);
+
+// Shape of the partial reduction (1024 threads): runs of IPW = 16 items (256
+// bytes per split and plane) where that still gives 128 workgroups, else 8
+// or 4; G = 1024 / (IPW * T) split groups (at most 32).  Measured on the
+// bench workloads, 16-item runs were as fast as or faster than 4..64.
+// EQL_RED_IPW forces IPW (A/B timing).
+inline void wgrad_reduce_shape(int T, int64_t items, int& ipw, int& G) {
+  int forced = 0;
+  if (const char* e = getenv("EQL_RED_IPW")) forced = atoi(e);
+  if (forced == 4 || forced == 8 || forced == 16 || (forced == 32 && 32 * T <= 1024) ||
+      (forced == 64 && 64 * T <= 1024)) {
+    ipw = forced;
+  } else {
+    for (ipw = 16; ipw > 4; ipw /= 2)
+      if ((items + ipw - 1) / ipw >= 128) break;
+  }
+  G = 1024 / (ipw * T);
+  if (G > 32) G = 32;
+}
 
 struct GemmArgs {
   const void* in;

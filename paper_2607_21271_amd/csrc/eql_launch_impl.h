@@ -117,12 +117,15 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // one workgroup per 64/T (4-channel group, o) items, plus one for the bias gradient
-  constexpr int IPW = 64 / T > 0 ? 64 / T : 1;
-  const int64_t items = (int64_t)(p.Cin_pad / 4) * a.Cout;
-  const unsigned blocks = (unsigned)((items + IPW - 1) / IPW + (a.db ? 1 : 0));
-  hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3(blocks), dim3(256), 0, a.stream,
-                     a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad);
+  // items per workgroup and split groups of eql_wgrad_reduce_kernel
+  const int64_t items = (int64_t)(p.Cin_pad / 4) * p.Cout_pad;
+  int ipw = 0, G = 0;
+  wgrad_reduce_shape(T, items, ipw, G);
+  const int NS = 1024 / G;
+  const unsigned blocks =
+      (unsigned)((items + ipw - 1) / ipw + (a.db ? (a.Cout + NS - 1) / NS : 0));
+  hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3(blocks), dim3(1024), 0, a.stream,
+                     a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
   return hipGetLastError();
 }
 

@@ -369,63 +369,106 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 
 // Fixed-order sum of the S split partials, then the inverse transform over
 // the planes (the same inverse as the forward epilogue).  An item is one
-// 16-byte run of the partial layout: four consecutive input channels of one
-// output channel.  A workgroup takes IPW = 64/T items x T planes = 64 slots and
-// splits the splits four ways: thread (q, e) sums splits q, q+4, ... of slot e,
-// the four group sums are added in a fixed order through LDS, and one thread
-// per (item, channel) transforms the planes and writes dw.  The extra last
-// workgroup sums the bias-gradient partials.
+// 16-byte run of the partial layout: four consecutive input channels c of one
+// padded output channel o, flat index cq * Cout_pad + o, so consecutive items
+// are contiguous within a plane.  A workgroup of 1024 threads takes IPW
+// consecutive items with all T planes (IPW * T slots) and splits the splits G
+// ways (IPW * T * G <= 1024): thread (q, e) reads slot e = p * IPW + i (plane p
+// of item i, so a plane's IPW items are one contiguous run of IPW * 16 bytes)
+// of splits q, q+G, q+2G, ...  Its loads are issued in batches of 8 before any
+// of them is added, so each thread keeps up to 8 loads in flight.  The G group
+// sums are added in a fixed order through LDS, and one thread per (item,
+// channel) transforms the planes and writes dw.  Workgroups past the items sum
+// the bias-gradient partials, 1024 / G output channels each, the same way.
+// Every summation order depends only on (S, G), so results are bitwise
+// reproducible.
+constexpr int kRedThreads = 1024;
+constexpr int kRedBatch = 8;
+template <int NB>
+__device__ __forceinline__ floatx4 sum_splits(const float* src, int64_t stride, int first, int step, int S) {
+  floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int sp = first; sp < S; sp += NB * step) {
+    floatx4 v[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const int s2 = sp + b * step;
+      v[b] = s2 < S ? *reinterpret_cast<const floatx4*>(src + s2 * stride) : floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int b = 0; b < NB; ++b) acc += v[b];
+  }
+  return acc;
+}
+
 template <int T, bool F16>
-__global__ __launch_bounds__(256) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
-                                                               const float* __restrict__ dbpart,
-                                                               void* __restrict__ dw,
-                                                               void* __restrict__ db, int S,
-                                                               int Cin, int Cout, int Cin_pad,
-                                                               int Cout_pad) {
+__global__ __launch_bounds__(kRedThreads) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
+                                                                       const float* __restrict__ dbpart,
+                                                                       void* __restrict__ dw,
+                                                                       void* __restrict__ db, int S,
+                                                                       int Cin, int Cout, int Cin_pad,
+                                                                       int Cout_pad, int IPW, int G) {
   using E = typename Elem<F16>::T;
-  constexpr int IPW = 64 / T > 0 ? 64 / T : 1;  // items per workgroup
-  constexpr int SLOTS = IPW * T;
-  __shared__ floatx4 red[4][64];
+  __shared__ floatx4 red[kRedThreads];
+  const int NS = kRedThreads / G;  // slot lanes (>= IPW * T)
   const int CQ = Cin_pad / 4;
-  const int64_t items = (int64_t)CQ * Cout;
+  const int64_t items = (int64_t)CQ * Cout_pad;
   const int64_t nblk = (items + IPW - 1) / IPW;
   const int tid = threadIdx.x;
-  if ((int64_t)blockIdx.x == nblk) {  // bias gradient
+  const int q = tid / NS;          // split group
+  const int e = tid - q * NS;      // slot lane
+  if ((int64_t)blockIdx.x >= nblk) {  // bias gradient: NS output channels per workgroup
     if (db == nullptr) return;
-    for (int o = tid; o < Cout; o += 256) {
-      float s = 0.0f;
-      for (int sp = 0; sp < S; ++sp) s += dbpart[(int64_t)sp * Cout_pad + o];
-      reinterpret_cast<E*>(db)[o] = (E)s;
+    const int o = (int)((int64_t)blockIdx.x - nblk) * NS + e;
+    float s = 0.0f;
+    if (q < G && o < Cout) {
+      for (int sp = q; sp < S; sp += kRedBatch * G) {
+        float v[kRedBatch];
+#pragma unroll
+        for (int b = 0; b < kRedBatch; ++b) {
+          const int s2 = sp + b * G;
+          v[b] = s2 < S ? dbpart[(int64_t)s2 * Cout_pad + o] : 0.0f;
+        }
+#pragma unroll
+        for (int b = 0; b < kRedBatch; ++b) s += v[b];
+      }
+    }
+    float* const rs = reinterpret_cast<float*>(red);
+    rs[tid] = s;
+    __syncthreads();
+    if (q == 0 && o < Cout) {
+      float t = rs[e];
+      for (int g = 1; g < G; ++g) t += rs[g * NS + e];
+      reinterpret_cast<E*>(db)[o] = (E)t;
     }
     return;
   }
-  const int q = tid >> 6;     // split group
-  const int e = tid & 63;     // slot: item e / T, plane e % T
-  const int64_t plane_stride = (int64_t)CQ * Cout_pad * 4;
+  const int64_t plane_stride = items * 4;
   const int64_t split_stride = (int64_t)T * plane_stride;
+  const int64_t it0 = (int64_t)blockIdx.x * IPW;
   floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
-  const int64_t item = (int64_t)blockIdx.x * IPW + e / T;
-  if (e < SLOTS && item < items) {
-    const int cq = (int)(item / Cout);
-    const int o = (int)(item - (int64_t)cq * Cout);
-    const float* src = part + (e % T) * plane_stride + ((int64_t)cq * Cout_pad + o) * 4;
-    for (int sp = q; sp < S; sp += 4) acc += *reinterpret_cast<const floatx4*>(src + sp * split_stride);
+  if (q < G && e < IPW * T) {
+    const int p = e / IPW;
+    const int64_t it = it0 + (e - p * IPW);
+    if (it < items) acc = sum_splits<kRedBatch>(part + p * plane_stride + it * 4, split_stride, q, G, S);
   }
-  red[q][e] = acc;
-  __syncthreads();
-  if (tid < SLOTS) red[0][tid] = ((red[0][tid] + red[1][tid]) + red[2][tid]) + red[3][tid];
+  red[tid] = acc;
   __syncthreads();
   if (tid < IPW * 4) {
     const int il = tid >> 2, ce = tid & 3;
-    const int64_t it = (int64_t)blockIdx.x * IPW + il;
+    const int64_t it = it0 + il;
     if (it < items) {
-      const int cq = (int)(it / Cout);
-      const int o = (int)(it - (int64_t)cq * Cout);
+      const int cq = (int)(it / Cout_pad);
+      const int o = (int)(it - (int64_t)cq * Cout_pad);
       const int c = cq * 4 + ce;
-      if (c < Cin) {
+      if (o < Cout && c < Cin) {
         float Pl[T], u[T];
 #pragma unroll
-        for (int p = 0; p < T; ++p) Pl[p] = red[0][il * T + p][ce];
+        for (int p = 0; p < T; ++p) {
+          const int sl = p * IPW + il;
+          float v = red[sl][ce];
+          for (int g = 1; g < G; ++g) v += red[g * NS + sl][ce];
+          Pl[p] = v;
+        }
         irdft<T>(Pl, u);
         E* d = reinterpret_cast<E*>(dw);
 #pragma unroll

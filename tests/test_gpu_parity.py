@@ -238,3 +238,27 @@ def test_forced_weight_mode(orc, monkeypatch, T, Cin, Cout, N, bias, dt, mode):
     say("  ", {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
         assert v <= TOL[dt], (T, Cin, Cout, dt, mode, k, v)
+
+
+# The weight-gradient reduction reads IPW consecutive partial items per plane
+# and splits the row splits over G thread groups (both chosen on the host from
+# T and the item count); every run length is forced here, with the bias
+# gradient, across group orders and split counts.
+RED_CASES = [(3, 64, 64, 3000, True), (8, 96, 384, 900, True), (16, 64, 64, 1500, True),
+             (5, 24, 40, 70, True)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("ipw", ["4", "8", "16", "32", "64"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", RED_CASES,
+                         ids=["T%d-%dx%d-N%d" % f[:4] for f in RED_CASES])
+def test_wgrad_reduce_run_length(orc, monkeypatch, T, Cin, Cout, N, bias, ipw):
+    say("reduce run length", ipw, T, Cin, Cout, N)
+    monkeypatch.setenv("EQL_RED_IPW", ipw)
+    inp = synth.draw(T, Cin, Cout, N, bias, 7700 + 31 * T + Cin + Cout).rounded("f32")
+    g = run_gpu(inp, "f32", want=("dw",))
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy)
+    errs = {"dw": rel_err(g["dw"], ref_dw), "db": rel_err(g["db"], ref_db)}
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL["f32"], (T, Cin, Cout, ipw, k, v)
