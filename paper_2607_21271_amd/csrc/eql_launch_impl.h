@@ -13,7 +13,9 @@ hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s)
   const WspecDims d = wspec_dims(T, Cin, Cout, F16);
   const int omax = d.CoF > d.CoutB ? d.CoF : d.CoutB;  // tiles cover both layouts
   const int cmax = d.CiF > d.CinB ? d.CiF : d.CinB;
-  hipLaunchKernelGGL((eql_wspec_kernel<T, F16>), dim3((unsigned)(omax / 16), (unsigned)(cmax / 16)),
+  constexpr int WO = 256 * (F16 ? 8 : 4) / kWsC;  // output channels per tile (eql_wspec_kernel)
+  hipLaunchKernelGGL((eql_wspec_kernel<T, F16>),
+                     dim3((unsigned)((omax + WO - 1) / WO), (unsigned)((cmax + kWsC - 1) / kWsC)),
                      dim3(256), 0, s, w, wspec, Cin, Cout, d.CoF, d.CiF, d.CinB, d.CoutB);
   return hipGetLastError();
 }

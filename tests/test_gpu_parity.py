@@ -262,3 +262,25 @@ def test_wgrad_reduce_run_length(orc, monkeypatch, T, Cin, Cout, N, bias, ipw):
     say("  ", {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
         assert v <= TOL["f32"], (T, Cin, Cout, ipw, k, v)
+
+
+# The weight spectrum reads 16-byte runs of input channels where the weight
+# base and row stride allow it and single elements elsewhere; both paths give
+# the same bits.
+@pytest.mark.gpu
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout", [(8, 96, 384), (3, 64, 64), (16, 40, 24), (5, 7, 33)])
+def test_weight_spectrum_unaligned_base(T, Cin, Cout, dt):
+    from paper_2607_21271_amd import ops
+    say("weight spectrum offset base", T, Cin, Cout, dt)
+    tdt = torch.float16 if dt == "f16" else torch.float32
+    w = (torch.randn(T, Cout, Cin, generator=torch.Generator().manual_seed(T * 1000 + Cin)) /
+         np.sqrt(T * Cin)).to(tdt).cuda()
+    buf = torch.empty(w.numel() + 1, dtype=tdt, device="cuda")
+    w_off = buf[1:].view(T, Cout, Cin)
+    w_off.copy_(w)
+    assert w_off.data_ptr() % 16 != 0
+    a = ops.weight_spectrum(w)
+    b = ops.weight_spectrum(w_off)
+    torch.cuda.synchronize()
+    assert torch.equal(a.cpu(), b.cpu())
