@@ -284,3 +284,29 @@ def test_weight_spectrum_unaligned_base(T, Cin, Cout, dt):
     b = ops.weight_spectrum(w_off)
     torch.cuda.synchronize()
     assert torch.equal(a.cpu(), b.cpu())
+
+
+# Layers whose contraction fits in at most three MFMA steps and whose output
+# spans several o-chunks run the resident-spectrum mode (the activation
+# spectrum of a round stays in registers across o-chunks); covered across
+# group orders, both passes (the input gradient of the Cin > Cout cases), odd
+# and even o-chunk counts and one to three contraction steps.
+RES_CASES = [(8, 96, 384, 300, False), (8, 40, 200, 333, True), (8, 384, 96, 260, True),
+             (4, 24, 200, 517, False), (4, 200, 24, 300, True), (3, 64, 400, 1029, True),
+             (5, 48, 300, 260, True), (7, 32, 256, 130, False), (6, 64, 200, 200, True),
+             (2, 96, 512, 99, True), (1, 96, 1024, 77, True)]
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", RES_CASES,
+                         ids=["T%d-%dx%d-N%d" % f[:4] for f in RES_CASES])
+def test_resident_spectrum_mode(orc, T, Cin, Cout, N, bias, dt):
+    say("resident spectrum", T, Cin, Cout, N, dt)
+    inp = synth.draw(T, Cin, Cout, N, bias, 7900 + 31 * T + Cin + Cout).rounded(dt)
+    g = run_gpu(inp, dt, want=("y", "dx"))
+    errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
+            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w))}
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (T, Cin, Cout, dt, k, v)
