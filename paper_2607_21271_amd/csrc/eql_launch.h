@@ -154,22 +154,27 @@ struct WgradPlan {
 };
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16);
 
-// Shape of the partial reduction (1024 threads): runs of IPW = 16 items (256
-// bytes per split and plane) where that still gives 128 workgroups, else 8
-// or 4; G = 1024 / (IPW * T) split groups (at most 32).  Measured on the
-// bench workloads, 16-item runs were as fast as or faster than 4..64.
+// Shape of the partial reduction: NTHR threads per workgroup, runs of IPW
+// items (IPW * 16 bytes per split and plane), G = NTHR / (IPW * T) split
+// groups (at most 32).  Up to 64 splits: 256 threads and IPW = min(16, 64/T)
+// (the headline's 40 splits: 8 items x 4 groups, 10 splits per thread in two
+// batches; 10.8 us against 12.1 us with 1024 threads); more splits: 1024
+// threads and IPW = 16 where that still gives 128 workgroups, else 8 or 4
+// (16-item runs measured as fast as or faster than 4..64).
 // EQL_RED_IPW forces IPW (A/B timing).
-inline void wgrad_reduce_shape(int T, int64_t items, int& ipw, int& G) {
+inline void wgrad_reduce_shape(int T, int S, int64_t items, int& nthr, int& ipw, int& G) {
   int forced = 0;
   if (const char* e = getenv("EQL_RED_IPW")) forced = atoi(e);
-  if (forced == 4 || forced == 8 || forced == 16 || (forced == 32 && 32 * T <= 1024) ||
-      (forced == 64 && 64 * T <= 1024)) {
+  nthr = S <= 64 ? 256 : 1024;
+  if ((forced == 4 || forced == 8 || forced == 16 || forced == 32 || forced == 64) && forced * T <= nthr) {
     ipw = forced;
+  } else if (nthr == 256) {
+    ipw = 64 / T < 1 ? 1 : (64 / T > 16 ? 16 : 64 / T);
   } else {
     for (ipw = 16; ipw > 4; ipw /= 2)
       if ((items + ipw - 1) / ipw >= 128) break;
   }
-  G = 1024 / (ipw * T);
+  G = nthr / (ipw * T);
   if (G > 32) G = 32;
 }
 

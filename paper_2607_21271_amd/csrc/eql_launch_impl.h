@@ -119,15 +119,19 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  // items per workgroup and split groups of eql_wgrad_reduce_kernel
+  // threads, items per workgroup and split groups of eql_wgrad_reduce_kernel
   const int64_t items = (int64_t)(p.Cin_pad / 4) * p.Cout_pad;
-  int ipw = 0, G = 0;
-  wgrad_reduce_shape(T, items, ipw, G);
-  const int NS = 1024 / G;
+  int nthr = 0, ipw = 0, G = 0;
+  wgrad_reduce_shape(T, p.S, items, nthr, ipw, G);
+  const int NS = nthr / G;
   const unsigned blocks =
       (unsigned)((items + ipw - 1) / ipw + (a.db ? (a.Cout + NS - 1) / NS : 0));
-  hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16>), dim3(blocks), dim3(1024), 0, a.stream,
-                     a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
+  if (nthr == 256)
+    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16, 256>), dim3(blocks), dim3(256), 0, a.stream,
+                       a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
+  else
+    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16, 1024>), dim3(blocks), dim3(1024), 0, a.stream,
+                       a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
   return hipGetLastError();
 }
 

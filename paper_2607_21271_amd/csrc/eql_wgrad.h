@@ -371,18 +371,17 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 // the planes (the same inverse as the forward epilogue).  An item is one
 // 16-byte run of the partial layout: four consecutive input channels c of one
 // padded output channel o, flat index cq * Cout_pad + o, so consecutive items
-// are contiguous within a plane.  A workgroup of 1024 threads takes IPW
-// consecutive items with all T planes (IPW * T slots) and splits the splits G
-// ways (IPW * T * G <= 1024): thread (q, e) reads slot e = p * IPW + i (plane p
+// are contiguous within a plane.  A workgroup of NTHR threads (256 or 1024)
+// takes IPW consecutive items with all T planes (IPW * T slots) and splits the
+// splits G ways (IPW * T * G <= NTHR): thread (q, e) reads slot e = p * IPW + i (plane p
 // of item i, so a plane's IPW items are one contiguous run of IPW * 16 bytes)
 // of splits q, q+G, q+2G, ...  Its loads are issued in batches of 8 before any
 // of them is added, so each thread keeps up to 8 loads in flight.  The G group
 // sums are added in a fixed order through LDS, and one thread per (item,
 // channel) transforms the planes and writes dw.  Workgroups past the items sum
-// the bias-gradient partials, 1024 / G output channels each, the same way.
+// the bias-gradient partials, NTHR / G output channels each, the same way.
 // Every summation order depends only on (S, G), so results are bitwise
 // reproducible.
-constexpr int kRedThreads = 1024;
 constexpr int kRedBatch = 8;
 template <int NB>
 __device__ __forceinline__ floatx4 sum_splits(const float* src, int64_t stride, int first, int step, int S) {
@@ -400,16 +399,16 @@ __device__ __forceinline__ floatx4 sum_splits(const float* src, int64_t stride, 
   return acc;
 }
 
-template <int T, bool F16>
-__global__ __launch_bounds__(kRedThreads) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
+template <int T, bool F16, int NTHR>
+__global__ __launch_bounds__(NTHR) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
                                                                        const float* __restrict__ dbpart,
                                                                        void* __restrict__ dw,
                                                                        void* __restrict__ db, int S,
                                                                        int Cin, int Cout, int Cin_pad,
                                                                        int Cout_pad, int IPW, int G) {
   using E = typename Elem<F16>::T;
-  __shared__ floatx4 red[kRedThreads];
-  const int NS = kRedThreads / G;  // slot lanes (>= IPW * T)
+  __shared__ floatx4 red[NTHR];
+  const int NS = NTHR / G;         // slot lanes (>= IPW * T)
   const int CQ = Cin_pad / 4;
   const int64_t items = (int64_t)CQ * Cout_pad;
   const int64_t nblk = (items + IPW - 1) / IPW;
@@ -448,7 +447,8 @@ __global__ __launch_bounds__(kRedThreads) void eql_wgrad_reduce_kernel(const flo
   floatx4 acc = floatx4{0.f, 0.f, 0.f, 0.f};
   if (q < G && e < IPW * T) {
     const int p = e / IPW;
-    const int64_t it = it0 + (e - p * IPW);
+    const int i = e - p * IPW;
+    const int64_t it = it0 + i;
     if (it < items) acc = sum_splits<kRedBatch>(part + p * plane_stride + it * 4, split_stride, q, G, S);
   }
   red[tid] = acc;
