@@ -241,11 +241,13 @@ def test_forced_weight_mode(orc, monkeypatch, T, Cin, Cout, N, bias, dt, mode):
 
 
 # The weight-gradient reduction reads IPW consecutive partial items per plane
-# and splits the row splits over G thread groups (both chosen on the host from
-# T and the item count); every run length is forced here, with the bias
-# gradient, across group orders and split counts.
+# and splits the row splits over G thread groups, in workgroups of 256 threads
+# (up to 64 splits) or 1024 (more); all three are chosen on the host from T,
+# the split count and the item count.  Every run length that fits the
+# workgroup is forced here, with the bias gradient, across group orders and
+# split counts on both sides of 64 (the T = 3, N = 20000 case has 125).
 RED_CASES = [(3, 64, 64, 3000, True), (8, 96, 384, 900, True), (16, 64, 64, 1500, True),
-             (5, 24, 40, 70, True)]
+             (5, 24, 40, 70, True), (3, 64, 64, 20000, True)]
 
 
 @pytest.mark.gpu
