@@ -188,8 +188,10 @@ class Workload:
 
 def cpu_baseline(layer, dt, inp, rows_req):
     """Time the fp64 oracle (fwd + dx + dw) on the host cores: the first rows of
-    the same draw when the whole workload would take longer than about 15 s,
-    else the whole workload repeated until about 15 s have passed."""
+    the same draw when the whole workload would take longer than about 20 s,
+    else the whole workload repeated until about 20 s have passed (sized from
+    a calibration slice of about 2 G multiply-adds, large enough that thread
+    start-up does not dominate it)."""
     threads = len(os.sched_getaffinity(0))
     os.environ.setdefault("OMP_NUM_THREADS", str(threads))
     import oracle
@@ -197,14 +199,14 @@ def cpu_baseline(layer, dt, inp, rows_req):
     l = layer
     macs_per_row = 3 * l.T * l.T * l.Cin * l.Cout
     if rows_req <= 0:
-        # calibrate on a small slice, then size the sample to about 15 s
-        n0 = max(8, min(l.N, int(6e8 // macs_per_row)))
+        # calibrate on a slice, then size the sample to about 20 s
+        n0 = max(8, min(l.N, int(2e9 // macs_per_row)))
         t0 = time.perf_counter()
         orc.forward(inp.x[:n0], inp.w, inp.b)
         orc.backward_input(inp.dy[:n0], inp.w)
         orc.backward_weight(inp.x[:n0], inp.dy[:n0], with_bias=inp.b is not None)
         rate = n0 / max(time.perf_counter() - t0, 1e-6)
-        rows_req = int(rate * 15.0)
+        rows_req = int(rate * 20.0)
     n = max(1, min(l.N, rows_req))
     reps = max(1, rows_req // n) if n == l.N else 1
     xs, dys = inp.x[:n], inp.dy[:n]
