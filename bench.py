@@ -42,7 +42,7 @@ def parse():
     ap.add_argument("--rotate", type=int, default=4, help="input sets used in turn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=0,
-                    help="rows of the oracle sample (0: sized to about 15 s of host work)")
+                    help="rows of the oracle sample (0: sized to about 20 s of host work)")
     ap.add_argument("--all", action="store_true",
                     help="also time every other workload and dtype (one JSON line each on stderr)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
