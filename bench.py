@@ -5,7 +5,8 @@ One step = the whole hot path for one batch: weight spectrum, forward (rDFT ->
 per-bin MFMA GEMMs -> irDFT + bias), input gradient and weight gradient, all
 through the C ABI of libeqlinear.so.  Default workload: the EQ-ViT-B MLP
 up-projection, T = 8, Cin = 96 -> Cout = 384 per group element, N = 64*197 =
-12608 tokens, fp16 storage with fp32 transforms and accumulation.
+12608 tokens, fp16 storage; packed-fp16 forward transforms of x and dy, fp32
+weight spectrum, accumulation, inverse transforms and bias.
 
 Inputs are seeded synthetic tensors already resident in HBM.  ``--rotate``
 input sets (default 4, about 0.8 GB for the default workload) are used in
@@ -119,79 +120,113 @@ class Workload:
         nws = ops.workspace_bytes(l.N, l.T, l.Cin, l.Cout, tdt)
         self.ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
         self.stream = torch.cuda.current_stream()
-        self.events = []
 
-    def step(self, i, record, stream=None):
-        import torch
+    def step(self, i, stream=None):
+        """One training step of the layer on input set i: weight spectrum,
+        forward, input gradient, weight and bias gradients."""
         l, ops = self.layer, self.ops
         st = stream if stream is not None else self.stream
         x, dy, y, dx = self.sets[i % len(self.sets)]
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)] if record else None
-        if record:
-            ev[0].record(st)
         ops.weight_spectrum(self.w, out=self.wspec, stream=st)
-        if record:
-            ev[1].record(st)
         ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=st)
-        if record:
-            ev[2].record(st)
         ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=st)
-        if record:
-            ev[3].record(st)
         ops.backward_weight(x, dy, l.T, l.Cin, l.Cout, with_bias=l.bias, dw=self.dw, db=self.db,
                             workspace=self.ws, stream=st)
-        if record:
-            ev[4].record(st)
-            self.events.append(ev)
+
+    def _graph(self, fn):
+        import torch
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn(torch.cuda.current_stream())
+        return g
 
     def run_graph(self, steps, warmup):
-        """Whole-step time with each input set's step (the same five launches)
-        captured once in a HIP graph and replayed; exactly ``steps`` steps are
-        timed, bracketed by device synchronisation."""
+        """Whole-step time with each input set's step (the same launches as the
+        eager path) captured once in a HIP graph and replayed.  Exactly
+        ``steps`` steps are timed, bracketed by device synchronisation (their
+        mean is the reported step time); HIP events around every replay, on
+        the stream the replays run on, give the per-step distribution."""
         import torch
-        graphs = []
-        for r in range(len(self.sets)):
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g):
-                self.step(r, False, stream=torch.cuda.current_stream())
-            graphs.append(g)
+        graphs = [self._graph(lambda st, r=r: self.step(r, stream=st))
+                  for r in range(len(self.sets))]
         for i in range(warmup):
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
+        st = torch.cuda.current_stream()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
         t0 = time.perf_counter()
+        ev[0].record(st)
         for i in range(steps):
             graphs[(warmup + i) % len(graphs)].replay()
+            ev[i + 1].record(st)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
+        per = [ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(steps)]  # us
         del graphs
-        return (t1 - t0) / steps
-
-    def run(self, steps, warmup):
-        import torch
-        for i in range(warmup):
-            self.step(i, False)
-        torch.cuda.synchronize()
-        self.events = []
-        t0 = time.perf_counter()
-        for i in range(steps):
-            self.step(warmup + i, True)
-        torch.cuda.synchronize()
-        t1 = time.perf_counter()
-        names = ["wspec", "fwd", "dx", "dw"]
-        per = {n: 0.0 for n in names}
-        for ev in self.events:
-            for k, n in enumerate(names):
-                per[n] += ev[k].elapsed_time(ev[k + 1]) * 1e3  # us
-        per = {n: v / steps for n, v in per.items()}
         return (t1 - t0) / steps, per
+
+    def run_passes(self, reps):
+        """Average duration of one launch of each entry point: per pass, one HIP
+        graph holds one call per input set back to back (no host time between
+        the launches) and is replayed until ``reps`` calls have run; HIP
+        events on the replay stream bracket all of them."""
+        import torch
+        l, ops = self.layer, self.ops
+        R = len(self.sets)
+
+        def launch(kind, r, st):
+            x, dy, y, dx = self.sets[r]
+            if kind == "wspec":
+                ops.weight_spectrum(self.w, out=self.wspec, stream=st)
+            elif kind == "fwd":
+                ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=st)
+            elif kind == "dx":
+                ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=st)
+            else:
+                ops.backward_weight(x, dy, l.T, l.Cin, l.Cout, with_bias=l.bias, dw=self.dw,
+                                    db=self.db, workspace=self.ws, stream=st)
+
+        ops.weight_spectrum(self.w, out=self.wspec)
+        out = {}
+        for kind in ("wspec", "fwd", "dx", "dw"):
+            g = self._graph(lambda st: [launch(kind, r, st) for r in range(R)])
+            n = max(1, reps // R)
+            g.replay()
+            torch.cuda.synchronize()
+            st = torch.cuda.current_stream()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(st)
+            for _ in range(n):
+                g.replay()
+            e1.record(st)
+            torch.cuda.synchronize()
+            out[kind] = e0.elapsed_time(e1) * 1e3 / (n * R)
+            del g
+        return out
+
+
+def _pct(v, q):
+    import numpy as np
+    return float(np.percentile(np.asarray(v), q))
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(layer, dt, inp, rows_req):
-    """Time the fp64 oracle (fwd + dx + dw) on the host cores: the first rows of
-    the same draw when the whole workload would take longer than about 20 s,
-    else the whole workload repeated until about 20 s have passed (sized from
-    a calibration slice of about 2 G multiply-adds, large enough that thread
-    start-up does not dominate it)."""
+    """Time the fp64 oracle (fwd, dx, dw each timed) on the host cores: the first
+    rows of the same draw when the whole workload would take longer than
+    about 20 s, else the whole workload repeated until about 20 s have passed
+    (sized from a calibration slice of about 2 G multiply-adds, large enough
+    that thread start-up does not dominate it)."""
     threads = len(os.sched_getaffinity(0))
     os.environ.setdefault("OMP_NUM_THREADS", str(threads))
     import oracle
@@ -210,18 +245,32 @@ def cpu_baseline(layer, dt, inp, rows_req):
     n = max(1, min(l.N, rows_req))
     reps = max(1, rows_req // n) if n == l.N else 1
     xs, dys = inp.x[:n], inp.dy[:n]
-    t0 = time.perf_counter()
+    per = {"fwd": 0.0, "dx": 0.0, "dw": 0.0}
     for _ in range(reps):
+        t0 = time.perf_counter()
         orc.forward(xs, inp.w, inp.b)
+        t1 = time.perf_counter()
         orc.backward_input(dys, inp.w)
+        t2 = time.perf_counter()
         orc.backward_weight(xs, dys, with_bias=inp.b is not None)
-    t = time.perf_counter() - t0
+        t3 = time.perf_counter()
+        per["fwd"] += t1 - t0
+        per["dx"] += t2 - t1
+        per["dw"] += t3 - t2
+    t = sum(per.values())
     what = ("first %d of %d rows" % (n, l.N)) if n < l.N else ("all %d rows, %d times" % (n, reps))
     return {"value": n * reps / t, "unit": "tokens/s", "cores": int(os.environ["OMP_NUM_THREADS"]),
             "kind": "oracle",
             "sample": "%s of the same seeded %s draw, fwd + dx + dw in fp64 (direct circular-"
                       "convolution sums), %.1f s" % (what, dt, t),
-            "seconds": t}
+            "seconds": t, "cpu_model": cpu_model(),
+            "pass_tokens_per_s": {k: round(n * reps / v, 1) for k, v in per.items()}}
+
+
+KERNELS = {"wspec": "eqlinear_weight_spectrum (eql_wspec_kernel)",
+           "fwd": "eqlinear_forward (eql_gemm_kernel, forward)",
+           "dx": "eqlinear_backward_input (eql_gemm_kernel, input gradient)",
+           "dw": "eqlinear_backward_weight (eql_wgrad_kernel + eql_wgrad_reduce_kernel)"}
 
 
 def measure(layer, dt, args, digest, with_cpu):
@@ -230,18 +279,18 @@ def measure(layer, dt, args, digest, with_cpu):
     from paper_2607_21271_amd import roofline as rf
     l = layer
     wl = Workload(l, dt, max(1, args.rotate))
-    # eager steps with events between the passes (per-pass times, roofline),
-    # then the same steps replayed from HIP graphs (the step time reported)
-    sec_eager, per = wl.run(args.steps, args.warmup)
-    sec = wl.run_graph(args.steps, args.warmup)
+    # the step: HIP-graph replays of whole steps (reported step time and its
+    # distribution); the passes: back-to-back launches of each entry point
+    sec, per_step = wl.run_graph(args.steps, args.warmup)
+    per = wl.run_passes(max(args.steps, 4 * max(1, args.rotate)))
     N = l.N
     flops = 3 * rf.pass_flops(N, l.T, l.Cin, l.Cout)
     dense = 3 * rf.dense_equiv_flops(N, l.T, l.Cin, l.Cout)
     nbytes = {k: rf.pass_bytes(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
               for k in ("wspec", "fwd", "dx", "dw")}
     dom = max(("fwd", "dx", "dw"), key=lambda k: per[k])
-    bound = "hbm" if dt == "f16" or rf.pass_bytes(dom, N, l.T, l.Cin, l.Cout, dt) / (
-        rf.PEAK_HBM_GBS * 1e9) > rf.pass_flops(N, l.T, l.Cin, l.Cout) / (
+    bound = "hbm" if rf.pass_bytes(dom, N, l.T, l.Cin, l.Cout, dt) / (
+        rf.PEAK_HBM_GBS * 1e9) >= rf.pass_flops(N, l.T, l.Cin, l.Cout) / (
         rf.PEAK_MFMA_TFLOPS[dt] * 1e12) else "mfma"
     t_dom = per[dom] * 1e-6
     if bound == "hbm":
@@ -252,10 +301,7 @@ def measure(layer, dt, args, digest, with_cpu):
         peak, unit = rf.PEAK_MFMA_TFLOPS[dt], "TFLOP/s"
     traffic = stored_traffic(l.name, dt, dom, digest)
     roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": {
-                "fwd": "eqlinear_forward (eql_gemm_kernel, forward)",
-                "dx": "eqlinear_backward_input (eql_gemm_kernel, input gradient)",
-                "dw": "eqlinear_backward_weight (eql_wgrad_kernel + eql_wgrad_reduce_kernel)"}[dom],
+            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": KERNELS[dom],
             "algorithmic_bytes_per_launch": nbytes[dom], "avg_launch_us": round(per[dom], 2)}
     roof_all = sum(rf.roofline_time_s(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
                    for k in ("wspec", "fwd", "dx", "dw"))
@@ -272,10 +318,14 @@ def measure(layer, dt, args, digest, with_cpu):
         "mfma_util_pct": round(100 * flops / sec / (rf.PEAK_MFMA_TFLOPS[dt] * 1e12), 2),
         "tflops_actual": round(flops / sec / 1e12, 2),
         "tflops_dense_equiv": round(dense / sec / 1e12, 2),
-        "timing": "step = one replay of a HIP graph holding that input set's five launches "
-                  "(weight spectrum, forward, input gradient, weight gradient + reduce); "
-                  "pass_us and roofline from an eager run with events between the passes",
-        "eager_ms_per_step": round(sec_eager * 1e3, 4),
+        "step_us": {"mean": round(sec * 1e6, 2), "median": round(_pct(per_step, 50), 2),
+                    "p10": round(_pct(per_step, 10), 2), "p90": round(_pct(per_step, 90), 2)},
+        "timing": "step = one replay of a HIP graph holding one input set's launches (weight "
+                  "spectrum, forward, input gradient, weight gradient); ms_per_step is the mean "
+                  "over the timed replays (host clock around all of them), step_us its "
+                  "distribution from HIP events around each replay; pass_us = average launch "
+                  "of each entry point, timed with HIP events around graph replays of "
+                  "back-to-back launches on the replay stream",
         "pass_us": {k: round(v, 2) for k, v in per.items()},
         "pass_hbm_gbs": {k: round(nbytes[k] / (per[k] * 1e-6) / 1e9, 1) for k in per},
         "roofline": roof,

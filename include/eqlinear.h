@@ -18,9 +18,16 @@
  * axis: w[j] = W_paper[(T - j) mod T].
  *
  * Common rules for every entry point:
- *   - dtype is EQL_F32 or EQL_F16 and applies to every tensor of the call;
- *     FP16 tensors are IEEE binary16, every transform and accumulation is fp32,
- *     and each output is rounded once (round-to-nearest-even).
+ *   - dtype is EQL_F32 or EQL_F16 and applies to every tensor of the call.
+ *     EQL_F32: every transform, product and accumulation is fp32.
+ *     EQL_F16 (IEEE binary16): the forward real DFTs of the activations x and
+ *     of the output gradients dy run in packed fp16 arithmetic (two signals per
+ *     register, twiddles rounded to fp16), since their results are fp16 MFMA
+ *     operands; the weight spectrum, every product's accumulation, the inverse
+ *     transforms and the bias are fp32.  db sums each pair of rows' fp16 bin 0
+ *     into fp32.  A transform partial sum above 65504 in magnitude overflows
+ *     to +-inf, so |x| and |dy| must stay below about 65504 / T.
+ *     Each output is rounded once (round-to-nearest-even).
  *   - All pointers are device pointers owned by the caller.  The library never
  *     allocates, frees or synchronises; work is enqueued on `stream` (a
  *     hipStream_t passed as void*, NULL = the null stream) and the call returns
@@ -38,8 +45,10 @@
  *   - Outputs are overwritten, never accumulated into.
  *   - Results are bitwise reproducible for the same inputs, shape, dtype and
  *     device model: no atomics, fixed summation orders.
- *   - Calls are thread-safe; concurrent calls that share no output buffer may
- *     run on different streams.
+ *   - Calls are thread-safe: the library's only shared state is a per-device
+ *     property cache filled once and a kernel-occupancy cache guarded by a
+ *     mutex.  Concurrent calls that share no output buffer may run on
+ *     different streams.
  */
 #ifndef EQLINEAR_H
 #define EQLINEAR_H

@@ -1,7 +1,8 @@
 """Build libeqlinear.so (gfx950) in-tree with hipcc.
 
 Each translation unit is compiled in its own hipcc process (in parallel), then
-linked into ``paper_2607_21271_amd/libeqlinear.so``.  Always rebuilds.  The
+linked into ``paper_2607_21271_amd/libeqlinear.so``.  The kernel instantiations
+are one object per (group order T, dtype): ``eql_inst.hip`` compiled 32 times.  Always rebuilds.  The
 device assembly is kept (-save-temps) and scanned by isa_check before the
 library is installed; a finding fails the build.
 Usage: ``python -m paper_2607_21271_amd.build`` or ``build()``.
@@ -19,7 +20,12 @@ CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libeqlinear.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 
-SOURCES = ["eql_api.cpp", "eql_f32.hip", "eql_f16.hip"]
+HOST_SOURCES = ["eql_api.cpp", "eql_dispatch.cpp"]
+MAX_T = 16
+# (source, object stem, extra defines)
+UNITS = [(s, os.path.splitext(s)[0], []) for s in HOST_SOURCES] + [
+    ("eql_inst.hip", "inst_%s_t%02d" % ("f16" if f16 else "f32", t), ["-DEQK_T=%d" % t, "-DEQK_F16=%d" % f16])
+    for t in range(MAX_T, 0, -1) for f16 in (1, 0)]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -32,12 +38,15 @@ COMMON_FLAGS = ["-O3", "-std=c++20", "-fPIC", "-Wall", "-Wno-unused-function",
                 "-I" + os.path.join(os.path.dirname(HERE), "include")]
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
+def _compile(unit) -> str:
+    src, stem, defs = unit
+    wd = os.path.join(BUILD_DIR, stem)   # -save-temps names its files after the source
+    os.makedirs(wd, exist_ok=True)
+    obj = os.path.join(wd, stem + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON_FLAGS, "-save-temps", *lang, "-c", os.path.join(CSRC, src),
-           "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD_DIR)
+    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON_FLAGS, *defs, "-save-temps", *lang, "-c",
+           os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=wd)
     if r.returncode != 0:
         raise RuntimeError("hipcc failed for %s:\n%s\n%s" % (src, " ".join(cmd), r.stderr[-20000:]))
     return obj
@@ -46,9 +55,9 @@ def _compile(src: str) -> str:
 def build(verbose: bool = True) -> str:
     shutil.rmtree(BUILD_DIR, ignore_errors=True)
     os.makedirs(BUILD_DIR, exist_ok=True)
-    jobs = min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4)))
+    jobs = min(len(UNITS), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4)))
     with cf.ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        objs = list(ex.map(_compile, UNITS))
     from . import isa_check
     isa_check.check_build(BUILD_DIR)
     tmp = OUT + ".tmp%d" % os.getpid()

@@ -233,8 +233,7 @@ int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cou
   if (any_overlap(r, 2)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   hipStream_t s = (hipStream_t)stream;
-  return launched(dtype == EQL_F16 ? eqk::launch_wspec_f16(T, w, wspec, Cin, Cout, s)
-                                   : eqk::launch_wspec_f32(T, w, wspec, Cin, Cout, s));
+  return launched(eqk::launch_wspec(dtype == EQL_F16, T, w, wspec, Cin, Cout, s));
 }
 
 static int gemm_common(const void* in, const void* wspec, const void* bias, void* out, int64_t N,
@@ -274,8 +273,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
     a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
     a.Ci_pad = d.CoutB;
   }
-  return launched(dtype == EQL_F16 ? eqk::launch_gemm_f16(T, bwd, a)
-                                   : eqk::launch_gemm_f32(T, bwd, a));
+  return launched(eqk::launch_gemm(dtype == EQL_F16, T, bwd, a));
 }
 
 int eqlinear_forward(const void* x, const void* wspec, const void* bias, void* y, int64_t N,
@@ -326,8 +324,7 @@ int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbia
   a.Cin = Cin;
   a.Cout = Cout;
   a.stream = (hipStream_t)stream;
-  return launched(dtype == EQL_F16 ? eqk::launch_wgrad_f16(T, a, p)
-                                   : eqk::launch_wgrad_f32(T, a, p));
+  return launched(eqk::launch_wgrad(dtype == EQL_F16, T, a, p));
 }
 
 }  // extern "C"

@@ -201,11 +201,18 @@ struct WgradArgs {
   hipStream_t stream;
 };
 
-hipError_t launch_wspec_f32(int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
-hipError_t launch_wspec_f16(int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
-hipError_t launch_gemm_f32(int T, bool bwd, const GemmArgs& a);
-hipError_t launch_gemm_f16(int T, bool bwd, const GemmArgs& a);
-hipError_t launch_wgrad_f32(int T, const WgradArgs& a, const WgradPlan& p);
-hipError_t launch_wgrad_f16(int T, const WgradArgs& a, const WgradPlan& p);
+// Launches of one group order and element type (eql_inst.hip, one object per
+// (T, dtype) so the instantiations build in parallel).
+template <int T, bool F16>
+struct Inst {
+  static hipError_t wspec(const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
+  static hipError_t gemm(bool bwd, const GemmArgs& a);
+  static hipError_t wgrad(const WgradArgs& a, const WgradPlan& p);
+};
+
+// Dispatch over T (eql_dispatch.cpp).
+hipError_t launch_wspec(bool f16, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
+hipError_t launch_gemm(bool f16, int T, bool bwd, const GemmArgs& a);
+hipError_t launch_wgrad(bool f16, int T, const WgradArgs& a, const WgradPlan& p);
 
 }  // namespace eqk

@@ -1,6 +1,8 @@
-// eql_launch_impl.h -- tile choice and launches for one element type.  Included
-// by exactly one instantiation unit per dtype (EQK_F16 = 0 or 1).
+// eql_launch_impl.h -- tile choice and launches for one group order and element
+// type.  Included only by eql_inst.hip, which is compiled once per (T, dtype).
 #pragma once
+#include <mutex>
+
 #include "eql_gemm.h"
 #include "eql_kernels.h"
 #include "eql_wgrad.h"
@@ -21,21 +23,27 @@ hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s)
 }
 
 // Resident workgroups per CU of one kernel at a given dynamic LDS size,
-// cached per (device, kernel, LDS).
+// cached per (device, kernel, LDS).  The cache is shared by every host thread:
+// lookups and inserts hold one mutex (an entry never changes once written).
 inline int occupancy(const void* kernel, int threads, int lds) {
   struct Entry { const void* k; int dev, lds, occ; };
-  static Entry cache[256];
+  static std::mutex mu;
+  static Entry cache[512];
   static int n_cache = 0;
   int dev = 0;
   (void)hipGetDevice(&dev);
-  for (int i = 0; i < n_cache; ++i)
-    if (cache[i].k == kernel && cache[i].dev == dev && cache[i].lds == lds) return cache[i].occ;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    for (int i = 0; i < n_cache; ++i)
+      if (cache[i].k == kernel && cache[i].dev == dev && cache[i].lds == lds) return cache[i].occ;
+  }
   int occ = 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, lds) != hipSuccess || occ <= 0) {
     (void)hipGetLastError();
     occ = 1;
   }
-  if (n_cache < 256) cache[n_cache++] = Entry{kernel, dev, lds, occ};
+  std::lock_guard<std::mutex> lock(mu);
+  if (n_cache < 512) cache[n_cache++] = Entry{kernel, dev, lds, occ};
   return occ;
 }
 
@@ -155,26 +163,5 @@ hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
 #undef EQK_WG
   return hipErrorInvalidValue;
 }
-
-#define EQK_T_SWITCH(T_, CALL)       \
-  switch (T_) {                      \
-    case 1: return CALL(1);          \
-    case 2: return CALL(2);          \
-    case 3: return CALL(3);          \
-    case 4: return CALL(4);          \
-    case 5: return CALL(5);          \
-    case 6: return CALL(6);          \
-    case 7: return CALL(7);          \
-    case 8: return CALL(8);          \
-    case 9: return CALL(9);          \
-    case 10: return CALL(10);        \
-    case 11: return CALL(11);        \
-    case 12: return CALL(12);        \
-    case 13: return CALL(13);        \
-    case 14: return CALL(14);        \
-    case 15: return CALL(15);        \
-    case 16: return CALL(16);        \
-    default: return hipErrorInvalidValue; \
-  }
 
 }  // namespace eqk

@@ -14,6 +14,15 @@ Checks, per kernel:
   converted_source   an f16->f32 convert reads a register whose last write in
                      the same basic block was an fp32 result (a raw word is
                      never such a value)
+  mfma_dst_overlap   an MFMA whose result spans more than four registers has a
+                     destination that partially overlaps its accumulator
+                     input (srcC).  The gfx950 assembler refuses exactly this
+                     form ("source 2 operand must not partially overlap with
+                     dst") and accepts partial overlap for four-register
+                     results, which the compiler emits for the 16x16 MFMAs
+                     of these kernels; the check keeps a build from carrying
+                     the refused form in code that bypassed the assembler's
+                     operand validation.
 """
 from __future__ import annotations
 
@@ -30,6 +39,7 @@ _F32_DEF = re.compile(r"^\s*(v_cvt_f32_f16\S*|v_add_f32\S*|v_sub_f32\S*|v_subrev
 _DEF_RANGE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v\[(\d+):(\d+)\]")
 _DEF_ONE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v(\d+)\b")
 _UNPACK_FIRST = re.compile(r"^\s*v_cvt_f32_f16_e32 v(\d+), v(\d+)\s*$")
+_MFMA = re.compile(r"^\s*v_mfma\S*\s+([va])\[(\d+):(\d+)\],\s*[^,]+,\s*[^,]+,\s*([va])\[(\d+):(\d+)\]")
 
 
 def scan_lines(lines):
@@ -58,6 +68,12 @@ def scan_lines(lines):
             u = _UNPACK_FIRST.match(line)
             if u and u.group(1) == u.group(2):
                 problems.append((kernel, "clobbered_unpack", line.strip()))
+        mf = _MFMA.match(line)
+        if mf:
+            d0, d1, c0, c1 = (int(mf.group(i)) for i in (2, 3, 5, 6))
+            if (mf.group(1) == mf.group(4) and d1 - d0 + 1 > 4 and (d0, d1) != (c0, c1)
+                    and d0 <= c1 and c0 <= d1):
+                problems.append((kernel, "mfma_dst_overlap", line.strip()))
         c = _CVT.match(line)
         if c and last.get(int(c.group(2))) == "f32":
             problems.append((kernel, "converted_source", line.strip()))
@@ -82,7 +98,7 @@ def scan_file(path):
 
 
 def device_asm_files(build_dir):
-    return sorted(glob.glob(os.path.join(build_dir, "*-hip-amdgcn-amd-amdhsa-*.s")))
+    return sorted(glob.glob(os.path.join(build_dir, "**", "*-hip-amdgcn-amd-amdhsa-*.s"), recursive=True))
 
 
 def demangle(names):

@@ -6,8 +6,19 @@ here (plumbing) unless the caller passes them in.
 
 Tensor layouts: x [..., Cin, T] (leading dims flattened to N rows),
 w [T, Cout, Cin], bias [Cout]; see include/eqlinear.h.
+
+The C ABI receives raw device addresses only, so every check that needs the
+tensors themselves happens here, before any launch: all tensors of a call live
+on one GPU and share one dtype (float32 or float16), outputs that the caller
+passes in are contiguous with exactly the expected shape, and a weight
+spectrum is a contiguous uint8 buffer of exactly
+``eqlinear_weight_spectrum_bytes`` bytes for the call's (T, Cin, Cout, dtype)
+(an fp32 spectrum is twice the size of an fp16 one, so a spectrum of the wrong
+dtype is refused).
 """
 from __future__ import annotations
+
+import weakref
 
 import torch
 
@@ -33,20 +44,62 @@ def _stream(stream):
 
 
 def _check_dev(*ts):
+    dev = None
     for t in ts:
-        if t is not None and not t.is_cuda:
+        if t is None:
+            continue
+        if not t.is_cuda:
             raise ValueError("eqlinear tensors must live on the GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("eqlinear tensors of one call must be on one device (%s vs %s)"
+                             % (dev, t.device))
+
+
+def _check_same_dtype(ref: torch.Tensor, **named):
+    for name, t in named.items():
+        if t is not None and t.dtype != ref.dtype:
+            raise TypeError("%s has dtype %s, expected %s (one dtype per call)"
+                            % (name, t.dtype, ref.dtype))
+
+
+def _check_out(name: str, t, shape, dtype):
+    if t is None:
+        return
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(shape)))
+    if t.dtype != dtype:
+        raise TypeError("%s has dtype %s, expected %s" % (name, t.dtype, dtype))
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def spectrum_bytes(T: int, Cin: int, Cout: int, dtype: torch.dtype) -> int:
+    return _lib.eqlinear_weight_spectrum_bytes(T, Cin, Cout, _DT[dtype])
+
+
+def _check_wspec(wspec: torch.Tensor, T, Cin, Cout, dtype):
+    need = spectrum_bytes(T, Cin, Cout, dtype)
+    if wspec.dtype != torch.uint8 or wspec.dim() != 1 or not wspec.is_contiguous():
+        raise TypeError("a weight spectrum is a contiguous 1-d uint8 buffer")
+    if wspec.numel() != need:
+        raise ValueError("weight spectrum has %d bytes; (T=%d, Cin=%d, Cout=%d, %s) needs exactly %d"
+                         % (wspec.numel(), T, Cin, Cout, dtype, need))
 
 
 def weight_spectrum(w: torch.Tensor, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """Opaque weight-spectrum buffer (uint8 tensor) for w [T, Cout, Cin]."""
-    _check_dev(w)
+    if w.dim() != 3:
+        raise ValueError("w must be [T, Cout, Cin], got shape %s" % (tuple(w.shape),))
     T, Cout, Cin = w.shape
     dt = _dtype_code(w)
+    if out is not None:
+        _check_wspec(out, T, Cin, Cout, w.dtype)
+    _check_dev(w, out)
     nbytes = _lib.eqlinear_weight_spectrum_bytes(T, Cin, Cout, dt)
     if out is None:
         out = torch.empty(nbytes, dtype=torch.uint8, device=w.device)
-    assert out.numel() >= nbytes
     w = w.contiguous()
     _lib.check(_lib.eqlinear_weight_spectrum(_ptr(w), _ptr(out), T, Cin, Cout, dt, _stream(stream)),
                "eqlinear_weight_spectrum")
@@ -55,30 +108,41 @@ def weight_spectrum(w: torch.Tensor, out: torch.Tensor | None = None, stream=Non
 
 def forward(x: torch.Tensor, wspec: torch.Tensor, bias: torch.Tensor | None, T: int, Cin: int,
             Cout: int, out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    _check_dev(x, wspec, bias)
+    dt = _dtype_code(x)
+    _check_same_dtype(x, bias=bias)
+    if tuple(x.shape[-2:]) != (Cin, T):
+        raise ValueError("x must be [..., Cin=%d, T=%d], got %s" % (Cin, T, tuple(x.shape)))
+    if bias is not None and tuple(bias.shape) != (Cout,):
+        raise ValueError("bias must be [Cout=%d], got %s" % (Cout, tuple(bias.shape)))
+    _check_wspec(wspec, T, Cin, Cout, x.dtype)
     lead = x.shape[:-2]
-    assert tuple(x.shape[-2:]) == (Cin, T), (x.shape, Cin, T)
+    _check_out("out", out, tuple(lead) + (Cout, T), x.dtype)
+    _check_dev(x, wspec, bias, out)
     x = x.contiguous()
+    bias = None if bias is None else bias.contiguous()
     N = x.numel() // (Cin * T)
     if out is None:
         out = torch.empty(*lead, Cout, T, dtype=x.dtype, device=x.device)
     _lib.check(_lib.eqlinear_forward(_ptr(x), _ptr(wspec), _ptr(bias), _ptr(out), N, T, Cin, Cout,
-                                     _dtype_code(x), _stream(stream)), "eqlinear_forward")
+                                     dt, _stream(stream)), "eqlinear_forward")
     return out
 
 
 def backward_input(dy: torch.Tensor, wspec: torch.Tensor, T: int, Cin: int, Cout: int,
                    out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
-    _check_dev(dy, wspec)
+    dt = _dtype_code(dy)
+    if tuple(dy.shape[-2:]) != (Cout, T):
+        raise ValueError("dy must be [..., Cout=%d, T=%d], got %s" % (Cout, T, tuple(dy.shape)))
+    _check_wspec(wspec, T, Cin, Cout, dy.dtype)
     lead = dy.shape[:-2]
-    assert tuple(dy.shape[-2:]) == (Cout, T), (dy.shape, Cout, T)
+    _check_out("out", out, tuple(lead) + (Cin, T), dy.dtype)
+    _check_dev(dy, wspec, out)
     dy = dy.contiguous()
     N = dy.numel() // (Cout * T)
     if out is None:
         out = torch.empty(*lead, Cin, T, dtype=dy.dtype, device=dy.device)
     _lib.check(_lib.eqlinear_backward_input(_ptr(dy), _ptr(wspec), _ptr(out), N, T, Cin, Cout,
-                                            _dtype_code(dy), _stream(stream)),
-               "eqlinear_backward_input")
+                                            dt, _stream(stream)), "eqlinear_backward_input")
     return out
 
 
@@ -91,19 +155,32 @@ def backward_weight(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int, Cout: i
                     db: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
                     stream=None):
     """(dw [T, Cout, Cin], db [Cout] or None)."""
-    _check_dev(x, dy)
+    dt = _dtype_code(x)
+    _check_same_dtype(x, dy=dy)
+    if tuple(x.shape[-2:]) != (Cin, T) or tuple(dy.shape[-2:]) != (Cout, T):
+        raise ValueError("x must be [..., %d, %d] and dy [..., %d, %d], got %s and %s"
+                         % (Cin, T, Cout, T, tuple(x.shape), tuple(dy.shape)))
+    N = x.numel() // (Cin * T)
+    if dy.numel() != N * Cout * T:
+        raise ValueError("x and dy must have the same number of rows")
+    if not with_bias:
+        db = None
+    _check_out("dw", dw, (T, Cout, Cin), x.dtype)
+    _check_out("db", db, (Cout,), x.dtype)
+    need = _lib.eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dt)
+    if workspace is not None:
+        if workspace.dim() != 1 or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous 1-d buffer")
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError("workspace has %d bytes, needs %d"
+                             % (workspace.numel() * workspace.element_size(), need))
+    _check_dev(x, dy, dw, db, workspace)
     x = x.contiguous()
     dy = dy.contiguous()
-    N = x.numel() // (Cin * T)
-    assert dy.numel() == N * Cout * T
-    dt = _dtype_code(x)
     if dw is None:
         dw = torch.empty(T, Cout, Cin, dtype=x.dtype, device=x.device)
     if with_bias and db is None:
         db = torch.empty(Cout, dtype=x.dtype, device=x.device)
-    if not with_bias:
-        db = None
-    need = _lib.eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dt)
     if workspace is None and need > 0:
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
     wsb = 0 if workspace is None else workspace.numel() * workspace.element_size()
@@ -113,13 +190,31 @@ def backward_weight(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int, Cout: i
     return dw, db
 
 
+# Weight spectra of the autograd path, per weight tensor: reused while the
+# weight's storage, version counter (bumped by every in-place update, e.g. an
+# optimizer step) and the current stream are unchanged.
+_SPEC_CACHE: "weakref.WeakKeyDictionary[torch.Tensor, tuple]" = weakref.WeakKeyDictionary()
+
+
+def cached_weight_spectrum(w: torch.Tensor) -> torch.Tensor:
+    stream = torch.cuda.current_stream(w.device).cuda_stream
+    key = (w.data_ptr(), w._version, tuple(w.shape), w.dtype, stream)
+    ent = _SPEC_CACHE.get(w)
+    if ent is not None and ent[0] == key:
+        return ent[1]
+    spec = weight_spectrum(w)
+    _SPEC_CACHE[w] = (key, spec)
+    return spec
+
+
 class EQLinearFunction(torch.autograd.Function):
     """Autograd wrapper: forward through the spectrum, gradients w.r.t. x, w and b."""
 
     @staticmethod
     def forward(ctx, x, w, b):
+        _check_same_dtype(x, w=w, b=b)
         T, Cout, Cin = w.shape
-        wspec = weight_spectrum(w)
+        wspec = cached_weight_spectrum(w)
         ctx.save_for_backward(x, w)
         ctx.wspec = wspec
         ctx.has_bias = b is not None

@@ -71,4 +71,20 @@ def test_current_build_is_clean():
     if not files:
         pytest.skip("no kept device assembly (library not built in this tree)")
     assert isa_check.check_build(B.BUILD_DIR) == files
-    assert any("eql_f16" in os.path.basename(f) for f in files)
+    assert any("inst_f16" in f for f in files)
+
+
+def test_flags_partial_overlap_of_wide_mfma_result():
+    probs = _scan("""
+\tv_mfma_f32_32x32x16_f16 v[4:19], v[30:33], v[34:37], v[0:15]
+""")
+    assert [p[1] for p in probs] == ["mfma_dst_overlap"]
+
+
+def test_passes_in_place_and_four_register_mfma():
+    probs = _scan("""
+\tv_mfma_f32_32x32x16_f16 v[0:15], v[30:33], v[34:37], v[0:15]
+\tv_mfma_f32_16x16x32_f16 v[52:55], v[158:161], v[208:211], v[54:57]
+\tv_mfma_f32_16x16x32_f16 v[0:3], v[10:13], v[14:17], 0
+""")
+    assert probs == []
