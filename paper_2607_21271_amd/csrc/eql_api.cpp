@@ -46,7 +46,100 @@ static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool f16, int K
   return rows;
 }
 
+// Plan of the register-direct kernel: the (CT, OT) block tile and split count
+// with the smallest estimated time.  One workgroup (kRdWaves waves, one per
+// SIMD) per CU, S splits x tiles workgroups; the estimate is the largest of
+// the HBM time (x and dy once plus the partials written and read back), the
+// L2-to-CU time and the transform (VALU) time of every workgroup loading its
+// rows for its channel tile, and the MFMA time, each spread over the CUs the
+// grid occupies.
+static WgradPlan wgrad_plan_rd(int64_t N, int T, int Cin, int Cout, bool f16) {
+  static const int kTiles[][2] = {{1, 1}, {1, 2}, {2, 1}, {2, 2}, {2, 4}, {4, 2}};
+  const int cus = 256;
+  const int KR = f16 ? 32 : 16;
+  const double eb = f16 ? 2.0 : 4.0;
+  const int R = 1 + (T % 2 == 0), K = (T - 1) / 2;
+  const double n = (double)(N > 0 ? N : 0);
+  // VALU cycles per transformed element (packed fp16: two rows per operation)
+  const double log2t = T <= 1 ? 1.0 : (T <= 2 ? 1.0 : (T <= 4 ? 2.0 : (T <= 8 ? 3.0 : 4.0)));
+  const double cyc = (f16 ? 0.05 : 0.10) * (log2t + 1.0);
+  int fc = 0, fo = 0;
+  if (const char* e = getenv("EQL_WGRAD_TILE")) {
+    if (sscanf(e, "%d,%d", &fc, &fo) != 2) fc = 0;
+  }
+  WgradPlan p{};
+  p.kind = 1;
+  double best = -1.0;
+  for (const auto& v : kTiles) {
+    const int ct = v[0], ot = v[1];
+    if (!rd_fits(T, ct, ot)) continue;
+    if (fc && (ct != fc || ot != fo)) continue;
+    const int BC = 16 * ct, BO = 16 * ot;
+    const int nct = (Cin + BC - 1) / BC, not_ = (Cout + BO - 1) / BO;
+    const int64_t tiles = (int64_t)nct * not_;
+    int64_t S = tiles >= cus ? 1 : cus / tiles;
+    const int64_t max_s = (N + (int64_t)kRdWaves * KR - 1) / ((int64_t)kRdWaves * KR);
+    if (S > max_s) S = max_s;
+    if (S < 1) S = 1;
+    const double part = (double)S * T * (nct * BC) * (not_ * BO) * 4.0;
+    const double hbm = (n * (Cin + Cout) * T * eb + 2.0 * part) / 5.5e12;
+    const double busy = (double)(S * tiles < cus ? S * tiles : cus);
+    const double vals = n * T * ((double)nct * BC * not_ + (double)not_ * BO * nct);
+    const double l2 = vals * eb / (busy * 154e9);
+    const double valu = vals * cyc / (busy * 4.0 * 2.4e9);
+    const double mfma = 2.0 * (R + 4 * K) * n * (nct * BC) * (not_ * BO) / ((f16 ? 2.5e15 : 1.573e14) * busy / cus);
+    double t = hbm;
+    if (l2 > t) t = l2;
+    if (valu > t) t = valu;
+    if (mfma > t) t = mfma;
+    const double cost = t * (1.0 + 1e-9 * tiles);
+    if (best < 0 || cost < best) {
+      best = cost;
+      p.ct = ct; p.otw = ot; p.BC = BC; p.BO = BO; p.n_ct = nct; p.n_ot = not_; p.S = (int)S;
+    }
+  }
+  p.KR = KR;
+  p.Cin_pad = p.n_ct * p.BC;
+  p.Cout_pad = p.n_ot * p.BO;
+  // rows per split: whole chunks, and each split's rows plus the chunks a
+  // wave prefetches past its last one addressable with 31-bit offsets
+  const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
+  int64_t S = p.S;
+  while ((double)((N + S - 1) / S + (kRdWaves + 1) * KR) * row_bytes >= 2147483648.0) ++S;
+  int64_t rows = N > 0 ? (N + S - 1) / S : 0;
+  rows = (rows + KR - 1) / KR * KR;
+  p.S = N > 0 ? (int)((N + rows - 1) / rows) : 0;
+  p.rows_per_split = rows;
+  p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
+  p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
+  return p;
+}
+
+// Which weight-gradient kernel: EQL_WGRAD_KIND=0/1 forces one (tests, A/B timing).
+static int wgrad_forced_kind() {
+  const char* v = getenv("EQL_WGRAD_KIND");
+  return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
+}
+
+static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16);
+
+// Kernel choice.  The register-direct kernel writes few partials but reads
+// every row once per channel tile and transforms it there; the staged kernel
+// transforms each row once per workgroup tile but needs many row splits to
+// fill the device.  Measured on MI355X (bench.py, all workloads): the
+// register-direct kernel is faster for layers of at most 48 x 48 channels per
+// group element (EQ-ViT-S projection 12.9 vs 22.0 us fp16, 20.3 vs 30.8 us
+// fp32; the 16 x 16 layer 7.5 vs 15.0 us), level at 96 x 384, and slower on
+// the larger-row-count layers (Swin stage 1, the 64 x 64 sweep), so it is
+// used up to 48 x 48.
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+  const int forced = wgrad_forced_kind();
+  if (forced == 1 || (forced < 0 && (int64_t)Cin * Cout <= 48 * 48))
+    return wgrad_plan_rd(N, T, Cin, Cout, f16);
+  return wgrad_plan_staged(N, T, Cin, Cout, f16);
+}
+
+static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16) {
   // Variants (wave grid rows, c-tiles, o-tiles per wave) with at most 96
   // accumulator floats per lane: CT * OTW * T * 4 <= 96.  Pick the one with the
   // smallest estimated time: HBM bytes (x and dy once, the partials written

@@ -138,11 +138,18 @@ inline WspecDims wspec_dims(int T, int Cin, int Cout, bool f16) {
 // Compute units of the current device (cached); 256 if unknown.
 int device_cu_count();
 
-// Plan of the split-row weight gradient: workgroup tile (a WGC x WGO wave grid
-// of CT x OTW tiles of 16 channels per wave), split count and the padded
-// partial extents.  Depends only on the problem, not on the device, so results
-// are reproducible across devices of the same model.
+// Plan of the split-row weight gradient: kernel, workgroup tile, split count
+// and the padded partial extents.  kind 0: eql_wgrad_kernel (operands staged
+// in LDS, a WGC x WGO wave grid of CT x OTW blocks of 16 x 16 channels per
+// wave); kind 1: eql_wgrad_rd_kernel (register-direct operands, kRdWaves
+// waves on one tile of CT x OTW blocks).  Depends only on the problem, not on
+// the device, so results are reproducible across devices of the same model.
+constexpr int kRdWaves = 4;
+// Register-direct variants whose accumulators and two raw chunk buffers fit
+// one wave per SIMD: 4T (CT*OT + 2 (CT + OT)) <= 400 registers.
+constexpr bool rd_fits(int T, int CT, int OT) { return 4 * T * (CT * OT + 2 * (CT + OT)) <= 400; }
 struct WgradPlan {
+  int kind;
   int wgc, ct, otw; // variant: wave grid rows (WGO = 8 / wgc), tiles per wave
   int BC, BO;       // channel tile of one workgroup
   int KR;           // rows per chunk

@@ -6,6 +6,7 @@
 #include "eql_gemm.h"
 #include "eql_kernels.h"
 #include "eql_wgrad.h"
+#include "eql_wgrad_rd.h"
 #include "eql_launch.h"
 
 namespace eqk {
@@ -115,6 +116,33 @@ hipError_t gemm_t(const GemmArgs& a) {
   return hipErrorInvalidValue;
 }
 
+// The split-partial reduction (both weight-gradient kernels write the same
+// partial layout).
+template <int T, bool F16>
+hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p);
+
+template <int T, bool F16, int CT, int OT>
+hipError_t wgrad_rd_variant(const WgradArgs& a, const WgradPlan& p) {
+  if (p.S > 0) {
+    constexpr int NW = kRdWaves;
+    const int lds = (NW - 1) * rd_wave_acc_bytes<T, CT, OT>() + NW * OT * 16 * 4;
+    auto k = eql_wgrad_rd_kernel<T, F16, CT, OT, NW>;
+    if (lds > kLdsBytes) return hipErrorInvalidValue;
+    if (lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+      if (e != hipSuccess) return e;
+    }
+    const int64_t G = (int64_t)p.S * p.n_ct * p.n_ot;
+    const int64_t blocks = (G + 7) / 8 * 8;  // whole groups of 8 (one per XCD)
+    hipLaunchKernelGGL(k, dim3((unsigned)blocks), dim3(64 * NW), lds, a.stream, a.x, a.dy, a.part,
+                       a.db ? a.dbpart : nullptr, a.N, a.Cin, a.Cout, p.rows_per_split, p.n_ct,
+                       p.n_ot, p.S, p.Cin_pad, p.Cout_pad);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return wgrad_reduce<T, F16>(a, p);
+}
+
 template <int T, bool F16, int WGC, int CT, int OTW>
 hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
   if (p.S > 0) {
@@ -127,6 +155,11 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  return wgrad_reduce<T, F16>(a, p);
+}
+
+template <int T, bool F16>
+hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p) {
   // threads, items per workgroup and split groups of eql_wgrad_reduce_kernel
   const int64_t items = (int64_t)(p.Cin_pad / 4) * p.Cout_pad;
   int nthr = 0, ipw = 0, G = 0;
@@ -145,6 +178,20 @@ hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
 
 template <int T, bool F16>
 hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
+  if (p.kind == 1) {
+#define EQK_RD(C_, O_)                                             \
+  if constexpr (rd_fits(T, C_, O_)) {                              \
+    if (p.ct == (C_) && p.otw == (O_)) return wgrad_rd_variant<T, F16, C_, O_>(a, p); \
+  }
+    EQK_RD(1, 1)
+    EQK_RD(1, 2)
+    EQK_RD(2, 1)
+    EQK_RD(2, 2)
+    EQK_RD(2, 4)
+    EQK_RD(4, 2)
+#undef EQK_RD
+    return hipErrorInvalidValue;
+  }
   // the variants of wgrad_plan whose accumulators fit (CT * OTW * T * 4 <= 96)
 #define EQK_WG(W_, C_, O_)                                                                    \
   if constexpr ((C_) * (O_) * T * 4 <= 96 &&                                                 \

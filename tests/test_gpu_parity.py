@@ -357,3 +357,43 @@ def test_two_host_threads_bitwise():
             for key in ref:
                 if ref[key] is not None:
                     assert np.array_equal(g[key], ref[key]), (dt, key)
+
+
+# Both weight-gradient kernels, forced: the staged kernel (EQL_WGRAD_KIND=0)
+# and the register-direct one (=1) with each of its channel tiles
+# (EQL_WGRAD_TILE=CT,OT blocks of 16 x 16) that fits the group order; ragged
+# channel counts, row counts that are not whole chunks, and a row count
+# smaller than one chunk per wave.
+WG_CASES = [(8, 96, 384, 700, False), (4, 24, 96, 1111, False), (3, 64, 64, 517, True),
+            (16, 40, 24, 300, True), (5, 7, 33, 45, True), (12, 64, 64, 257, True),
+            (1, 33, 17, 80, True), (8, 48, 48, 13, True)]
+WG_MODES = ["staged", "rd:1,1", "rd:1,2", "rd:2,1", "rd:2,2", "rd:2,4", "rd:4,2"]
+
+
+def _rd_fits(T, ct, ot):
+    return 4 * T * (ct * ot + 2 * (ct + ot)) <= 400
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("mode", WG_MODES)
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", WG_CASES, ids=["T%d-%dx%d-N%d" % f[:4] for f in WG_CASES])
+def test_wgrad_kernel_forced(orc, monkeypatch, T, Cin, Cout, N, bias, dt, mode):
+    if mode == "staged":
+        monkeypatch.setenv("EQL_WGRAD_KIND", "0")
+    else:
+        ct, ot = (int(v) for v in mode[3:].split(","))
+        if not _rd_fits(T, ct, ot):
+            pytest.skip("tile does not fit this group order")
+        monkeypatch.setenv("EQL_WGRAD_KIND", "1")
+        monkeypatch.setenv("EQL_WGRAD_TILE", "%d,%d" % (ct, ot))
+    say("weight gradient", mode, T, Cin, Cout, N, dt)
+    inp = synth.draw(T, Cin, Cout, N, bias, 7300 + 31 * T + Cin + Cout).rounded(dt)
+    g = run_gpu(inp, dt, want=("dw",))
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy, with_bias=bias)
+    errs = {"dw": rel_err(g["dw"], ref_dw)}
+    if bias:
+        errs["db"] = rel_err(g["db"], ref_db)
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (T, Cin, Cout, dt, mode, k, v)
