@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 1
+#define EQLINEAR_ABI_VERSION 2
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
@@ -72,8 +72,14 @@ typedef enum {
   EQL_ERR_ALIGNMENT = 3,
   EQL_ERR_WORKSPACE = 4,
   EQL_ERR_NO_DEVICE = 5,
-  EQL_ERR_LAUNCH = 6
+  EQL_ERR_LAUNCH = 6,
+  EQL_ERR_SCRATCH = 7
 } eql_status_t;
+
+/* Bytes of the static device scratch array that
+ * eqlinear_backward_weight_noalloc uses in place of a workspace (per GPU,
+ * held until the process ends). */
+#define EQLINEAR_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
 
 /* EQLINEAR_ABI_VERSION of the built library. */
 int eqlinear_abi_version(void);
@@ -137,6 +143,24 @@ size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int C
 int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
                              size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
                              void* stream);
+
+/* eqlinear_backward_weight without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid allocation).  Same operation, arguments (minus the
+ * workspace), kernels and bits as eqlinear_backward_weight; the fp32 split
+ * partials live in a file-scope static device array of
+ * EQLINEAR_STATIC_SCRATCH_BYTES per GPU instead, and the call performs no
+ * allocation of any kind.  A problem whose partials need more than that
+ * (eqlinear_backward_weight_workspace_bytes() >
+ * EQLINEAR_STATIC_SCRATCH_BYTES) returns EQL_ERR_SCRATCH before any HIP call.
+ * Every call on one GPU uses that GPU's one array, and every partial a call
+ * reads it first writes in the same call, so nothing carries over between
+ * calls; but two calls whose executions overlap on one GPU (different
+ * streams, or host threads without ordering) race on the array and give
+ * wrong results.  The first call on a device resolves the array's address
+ * on that device once (EQL_ERR_LAUNCH if the runtime cannot). */
+int eqlinear_backward_weight_noalloc(const void* x, const void* dy, void* dw, void* dbias, int64_t N,
+                                     int T, int Cin, int Cout, int dtype, void* stream);
 
 #ifdef __cplusplus
 }

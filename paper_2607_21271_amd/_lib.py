@@ -23,6 +23,11 @@ EQL_ERR_ALIGNMENT = 3
 EQL_ERR_WORKSPACE = 4
 EQL_ERR_NO_DEVICE = 5
 EQL_ERR_LAUNCH = 6
+EQL_ERR_SCRATCH = 7
+
+# Bytes of the static device scratch of eqlinear_backward_weight_noalloc
+# (EQLINEAR_STATIC_SCRATCH_BYTES in include/eqlinear.h).
+STATIC_SCRATCH_BYTES = 64 << 20
 
 # Every function the header declares, with (restype, argtypes).
 _vp, _i, _i64, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t
@@ -35,6 +40,7 @@ SIGNATURES = {
     "eqlinear_backward_input": (_i, [_vp, _vp, _vp, _i64, _i, _i, _i, _i, _vp]),
     "eqlinear_backward_weight_workspace_bytes": (_sz, [_i64, _i, _i, _i, _i]),
     "eqlinear_backward_weight": (_i, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i, _i, _i, _i, _vp]),
+    "eqlinear_backward_weight_noalloc": (_i, [_vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _vp]),
 }
 
 
@@ -107,3 +113,7 @@ def eqlinear_backward_weight(x, dy, dw, dbias, workspace, workspace_bytes, N, T,
                              stream) -> int:
     return lib().eqlinear_backward_weight(x, dy, dw, dbias, workspace, workspace_bytes, N, T, Cin,
                                           Cout, dtype, stream)
+
+
+def eqlinear_backward_weight_noalloc(x, dy, dw, dbias, N, T, Cin, Cout, dtype, stream) -> int:
+    return lib().eqlinear_backward_weight_noalloc(x, dy, dw, dbias, N, T, Cin, Cout, dtype, stream)

@@ -302,6 +302,7 @@ const char* eqlinear_status_string(int status) {
     case EQL_ERR_WORKSPACE: return "workspace too small or missing";
     case EQL_ERR_NO_DEVICE: return "no HIP device available";
     case EQL_ERR_LAUNCH: return "kernel launch failed";
+    case EQL_ERR_SCRATCH: return "problem needs more than the static device scratch of the allocation-free entry point";
     default: return "unknown status";
   }
 }
@@ -385,9 +386,58 @@ size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int C
   return align256(p.part_bytes) + align256(p.dbpart_bytes);
 }
 
+static int backward_weight_impl(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
+                                size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
+                                void* stream, bool static_scratch);
+
 int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
                              size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
                              void* stream) {
+  return backward_weight_impl(x, dy, dw, dbias, workspace, workspace_bytes, N, T, Cin, Cout, dtype,
+                              stream, false);
+}
+
+int eqlinear_backward_weight_noalloc(const void* x, const void* dy, void* dw, void* dbias, int64_t N,
+                                     int T, int Cin, int Cout, int dtype, void* stream) {
+  return backward_weight_impl(x, dy, dw, dbias, nullptr, 0, N, T, Cin, Cout, dtype, stream, true);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Static scratch of the allocation-free entry point: one array per GPU (the
+// loader places a copy in every device's memory).  Host code never uses the
+// array's name as an address: the device address is resolved once per device,
+// with that device current, and kept.
+static __device__ __align__(256) char scratch[EQLINEAR_STATIC_SCRATCH_BYTES];
+
+namespace {
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's scratch array, or null if the runtime
+// cannot resolve it.  Valid after check_device() succeeded.
+void* device_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) {
+      (void)hipGetLastError();
+      ptr = nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  });
+  return g_scratch_ptr[dev];
+}
+}  // namespace
+
+static int backward_weight_impl(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
+                                size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
+                                void* stream, bool static_scratch) {
   int st = check_shape(N, T, Cin, Cout, dtype);
   if (st) return st;
   if (!dw) return EQL_ERR_INVALID_ARG;
@@ -397,7 +447,8 @@ int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbia
       (dbias && !aligned(dbias, e)) || (workspace && !aligned(workspace, 16)))
     return EQL_ERR_ALIGNMENT;
   const size_t need = eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dtype);
-  if (need > 0 && (!workspace || workspace_bytes < need)) return EQL_ERR_WORKSPACE;
+  if (static_scratch && need > EQLINEAR_STATIC_SCRATCH_BYTES) return EQL_ERR_SCRATCH;
+  if (!static_scratch && need > 0 && (!workspace || workspace_bytes < need)) return EQL_ERR_WORKSPACE;
   const Range r[5] = {{x, (size_t)N * Cin * T * e},
                       {dy, (size_t)N * Cout * T * e},
                       {dw, (size_t)T * Cin * Cout * e},
@@ -405,6 +456,10 @@ int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbia
                       {workspace, need}};
   if (any_overlap(r, 5)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
+  if (static_scratch && need > 0) {
+    workspace = device_scratch();
+    if (!workspace) return EQL_ERR_LAUNCH;
+  }
   const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype == EQL_F16);
   eqk::WgradArgs a{};
   a.x = x;
@@ -420,4 +475,4 @@ int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbia
   return launched(eqk::launch_wgrad(dtype == EQL_F16, T, a, p));
 }
 
-}  // extern "C"
+

@@ -190,6 +190,31 @@ def backward_weight(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int, Cout: i
     return dw, db
 
 
+def backward_weight_noalloc(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int, Cout: int,
+                            dw: torch.Tensor, db: torch.Tensor | None = None, stream=None):
+    """dw [T, Cout, Cin] (and db [Cout] when given) through the allocation-free
+    entry point: outputs are caller-provided and nothing is allocated, on the
+    host or the device (the split partials use the library's static device
+    scratch; calls that overlap on one GPU must not be issued)."""
+    dt = _dtype_code(x)
+    _check_same_dtype(x, dy=dy)
+    if tuple(x.shape[-2:]) != (Cin, T) or tuple(dy.shape[-2:]) != (Cout, T):
+        raise ValueError("x must be [..., %d, %d] and dy [..., %d, %d], got %s and %s"
+                         % (Cin, T, Cout, T, tuple(x.shape), tuple(dy.shape)))
+    if not (x.is_contiguous() and dy.is_contiguous()):
+        raise ValueError("x and dy must be contiguous (no copies are made)")
+    N = x.numel() // (Cin * T)
+    if dy.numel() != N * Cout * T:
+        raise ValueError("x and dy must have the same number of rows")
+    _check_out("dw", dw, (T, Cout, Cin), x.dtype)
+    _check_out("db", db, (Cout,), x.dtype)
+    _check_dev(x, dy, dw, db)
+    _lib.check(_lib.eqlinear_backward_weight_noalloc(_ptr(x), _ptr(dy), _ptr(dw), _ptr(db), N, T, Cin,
+                                                     Cout, dt, _stream(stream)),
+               "eqlinear_backward_weight_noalloc")
+    return dw, db
+
+
 # Weight spectra of the autograd path, per weight tensor: reused while the
 # weight's storage, version counter (bumped by every in-place update, e.g. an
 # optimizer step) and the current stream are unchanged.

@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 8, names
+    assert len(names) == 9, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -47,11 +47,11 @@ def test_abi_version_matches_header(lib):
 
 def test_status_strings(lib):
     seen = set()
-    for s in range(7):
+    for s in range(8):
         t = L.eqlinear_status_string(s)
         assert t and t != "unknown status"
         seen.add(t)
-    assert len(seen) == 7
+    assert len(seen) == 8
     assert L.eqlinear_status_string(99) == "unknown status"
     assert L.eqlinear_status_string(-1) == "unknown status"
 
@@ -137,3 +137,29 @@ def test_valid_arguments_without_device_report_no_device(lib):
     assert L.eqlinear_forward(A, A + 8 * MB, None, A + 16 * MB, 100, 4, 8, 8, 0, None) == \
         L.EQL_ERR_NO_DEVICE
     assert L.eqlinear_weight_spectrum(A, A + MB, 4, 8, 8, 1, None) == L.EQL_ERR_NO_DEVICE
+
+
+def test_noalloc_argument_checks(lib):
+    """The allocation-free weight gradient checks its arguments like the
+    workspace entry point, and refuses a problem whose split partials exceed
+    its static device scratch, all before any HIP call."""
+    g = L.eqlinear_backward_weight_noalloc
+    base = [A, A + 8 * MB, A + 16 * MB, A + 17 * MB, 1000, 8, 16, 16, L.EQL_F32, None]
+
+    def call(i, v):
+        args = list(base)
+        args[i] = v
+        return g(*args)
+    assert call(2, None) == L.EQL_ERR_INVALID_ARG
+    assert call(0, None) == L.EQL_ERR_INVALID_ARG
+    assert call(2, A + 8 * MB + 4) == L.EQL_ERR_INVALID_ARG   # dw overlaps dy
+    assert call(3, A + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(5, 17) == L.EQL_ERR_UNSUPPORTED
+    assert call(8, 5) == L.EQL_ERR_INVALID_ARG
+    GB = 1 << 30
+    T, C, N = 16, 2048, 1000
+    need = L.eqlinear_backward_weight_workspace_bytes(N, T, C, C, L.EQL_F32)
+    assert need > L.STATIC_SCRATCH_BYTES
+    assert g(A, A + GB, A + 2 * GB, None, N, T, C, C, L.EQL_F32, None) == L.EQL_ERR_SCRATCH
+    m = re.search(r"#define EQLINEAR_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert int(m.group(1)) << int(m.group(2)) == L.STATIC_SCRATCH_BYTES
