@@ -46,6 +46,12 @@ def parse():
                     help="rows of the oracle sample (0: sized to about 20 s of host work)")
     ap.add_argument("--all", action="store_true",
                     help="also time every other workload and dtype (one JSON line each on stderr)")
+    ap.add_argument("--tables", action="store_true",
+                    help="only rerun the paper's operator benchmark (Sec. 4.1, Tables 1-2): T=4, "
+                         "32768 rows, c = 16..2048, fp32 and fp16; one JSON line per (dtype, c)")
+    ap.add_argument("--tables-c", default="16,32,64,128,256,512,1024,2048",
+                    help="per-group widths of --tables")
+    ap.add_argument("--tables-runs", type=int, default=200, help="timed runs per measurement")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB, 5 times (reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -341,6 +347,122 @@ def measure(layer, dt, args, digest, with_cpu):
     return rec
 
 
+def _time_fn(fn, runs, warmup=10):
+    """Mean and median of ``runs`` calls of fn, each bracketed by HIP events on
+    the current stream (host launch time between calls is not counted)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * runs)]
+    for i in range(runs):
+        ev[2 * i].record(st)
+        fn()
+        ev[2 * i + 1].record(st)
+    torch.cuda.synchronize()
+    t = sorted(ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(runs))
+    return {"mean_ms": round(sum(t) / runs, 4), "median_ms": round(t[runs // 2], 4)}
+
+
+def run_tables(args):
+    """The paper's operator benchmark (Sec. 4.1, Tables 1-2) on this GPU: input
+    [B*N = 32768 rows, c, T = 4], output width D = C = 4c.  Three layers:
+    Standard Linear (torch F.linear, a dense C -> C weight), Naive EQ-Linear
+    (the equivariant weight unrolled into the dense T*c x T*c matrix
+    W[o*T+t, c*T+s] = w[(t-s) mod T, o, c], then F.linear; autograd folds the
+    dense gradient back onto w) and this library.  Forward = one layer call
+    (for this library with the weight spectrum precomputed, which a frozen
+    weight allows; its time is reported apart); backward = input, weight and
+    bias gradients.  Mean and median of ``--tables-runs`` event-timed runs.
+    For c >= 512 sampled rows of y and dx and sampled dw entries are checked
+    against the fp64 oracle."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+
+    import synth
+    from paper_2607_21271_amd import ops
+    from paper_2607_21271_amd import roofline as rf
+    T, N = 4, 32768
+    runs = args.tables_runs
+    for dt in ("f32", "f16"):
+        tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+        for c in [int(v) for v in args.tables_c.split(",")]:
+            torch.cuda.empty_cache()
+            inp = synth.draw(T, c, c, N, True, 6000 + c).rounded(dt)
+            dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+            x, w, b, dy = dev(inp.x), dev(inp.w), dev(inp.b), dev(inp.dy)
+            rec = {"table": "operator", "dtype": dt, "c": c, "T": T, "rows": N, "runs": runs}
+            print("tables: %s c=%d" % (dt, c), file=sys.stderr, flush=True)
+            # this library
+            wspec = ops.weight_spectrum(w)
+            y = torch.empty(N, c, T, dtype=tdt, device="cuda")
+            dx = torch.empty_like(x)
+            dw = torch.empty_like(w)
+            db = torch.empty_like(b)
+            ws = torch.empty(max(1, ops.workspace_bytes(N, T, c, c, tdt)), dtype=torch.uint8,
+                             device="cuda")
+            rec["flash_wspec"] = _time_fn(lambda: ops.weight_spectrum(w, out=wspec), runs)
+            rec["flash_fwd"] = _time_fn(lambda: ops.forward(x, wspec, b, T, c, c, out=y), runs)
+            rec["flash_bwd"] = _time_fn(lambda: (ops.backward_input(dy, wspec, T, c, c, out=dx),
+                                                 ops.backward_weight(x, dy, T, c, c, True, dw=dw, db=db,
+                                                                     workspace=ws)), runs)
+            if c >= 512:
+                import oracle
+                orc = oracle.oracle()
+                rs = np.random.RandomState(c)
+                rows = np.unique(np.concatenate([rs.randint(0, N, 14), [0, N - 1]]))
+                torch.cuda.synchronize()
+                ry = orc.forward(inp.x[rows], inp.w, inp.b)
+                rdx = orc.backward_input(inp.dy[rows], inp.w)
+                jj, oo, cc = rs.randint(0, T, 24), rs.randint(0, c, 24), rs.randint(0, c, 24)
+                rdw = orc.backward_weight_entries(inp.x, inp.dy, jj, oo, cc)
+                err = lambda g, r: float(np.max(np.abs(g - r)) / np.max(np.abs(r)))
+                rec["parity_sampled"] = {
+                    "y": err(y.double().cpu().numpy()[rows], ry),
+                    "dx": err(dx.double().cpu().numpy()[rows], rdx),
+                    "dw": err(dw.double().cpu().numpy()[jj, oo, cc], rdw)}
+            del wspec, y, dx, ws
+            # Standard Linear: dense C -> C
+            C = c * T
+            xs = x.view(N, C).detach().requires_grad_(True)
+            W = (torch.randn(C, C, device="cuda") / C ** 0.5).to(tdt).requires_grad_(True)
+            bs = torch.zeros(C, dtype=tdt, device="cuda", requires_grad=True)
+            dys = dy.view(N, C)
+            with torch.no_grad():
+                rec["standard_fwd"] = _time_fn(lambda: F.linear(xs, W, bs), runs)
+            ys = F.linear(xs, W, bs)
+            rec["standard_bwd"] = _time_fn(
+                lambda: torch.autograd.grad(ys, (xs, W, bs), dys, retain_graph=True), runs)
+            del ys, W
+            # Naive EQ-Linear: unrolled weight, autograd through the unrolling
+            t_idx = torch.arange(T, device="cuda")
+            lag = (t_idx[:, None] - t_idx[None, :]) % T            # [t, s]
+            wn = w.detach().clone().requires_grad_(True)
+            bn = b.detach().clone().requires_grad_(True)
+
+            def naive():
+                Wd = wn[lag].permute(2, 0, 3, 1).reshape(c * T, c * T)   # [o*T+t, c*T+s]
+                return F.linear(xs, Wd, bn.repeat_interleave(T))
+            with torch.no_grad():
+                rec["naive_fwd"] = _time_fn(naive, runs)
+            yn = naive()
+            rec["naive_bwd"] = _time_fn(
+                lambda: torch.autograd.grad(yn, (xs, wn, bn), dys, retain_graph=True), runs)
+            del yn
+            fl = rf.pass_flops(N, T, c, c)
+            rec["flash_fwd_tflops"] = round(fl / (rec["flash_fwd"]["mean_ms"] * 1e-3) / 1e12, 2)
+            rec["flash_bwd_tflops"] = round(2 * fl / (rec["flash_bwd"]["mean_ms"] * 1e-3) / 1e12, 2)
+            rec["flash_fwd_hbm_gbs"] = round(rf.pass_bytes("fwd", N, T, c, c, dt, True) /
+                                             (rec["flash_fwd"]["mean_ms"] * 1e-3) / 1e9, 1)
+            rec["speedup_fwd_vs_standard"] = round(rec["standard_fwd"]["mean_ms"] /
+                                                   rec["flash_fwd"]["mean_ms"], 2)
+            rec["speedup_bwd_vs_standard"] = round(rec["standard_bwd"]["mean_ms"] /
+                                                   rec["flash_bwd"]["mean_ms"], 2)
+            print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -355,6 +477,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.calibrate_copy > 0:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.tables:
+        run_tables(args)
         return
     digest = source_digest()
     name = args.workload or synth.HEADLINE

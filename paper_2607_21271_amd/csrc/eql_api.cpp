@@ -126,15 +126,18 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
 // Kernel choice.  The register-direct kernel writes few partials but reads
 // every row once per channel tile and transforms it there; the staged kernel
 // transforms each row once per workgroup tile but needs many row splits to
-// fill the device.  Measured on MI355X (bench.py, all workloads): the
+// fill the device, and with channel tiles enough to fill it alone it leaves a
+// whole row range to each workgroup.  Measured on MI355X (bench.py): the
 // register-direct kernel is faster for layers of at most 48 x 48 channels per
 // group element (EQ-ViT-S projection 12.9 vs 22.0 us fp16, 20.3 vs 30.8 us
-// fp32; the 16 x 16 layer 7.5 vs 15.0 us), level at 96 x 384, and slower on
-// the larger-row-count layers (Swin stage 1, the 64 x 64 sweep), so it is
-// used up to 48 x 48.
+// fp32; the 16 x 16 layer 7.5 vs 15.0 us) and from 512 x 512 up (T = 4,
+// 32768 rows, whole backward: 1.8 vs 2.7 ms at 512 fp32, 28 vs 121 ms at
+// 2048 fp32, 7.6 vs 26.8 ms at 2048 fp16), level at 96 x 384 and 256 x 256,
+// and slower on Swin stage 1 and the 64 x 64 sweep.
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   const int forced = wgrad_forced_kind();
-  if (forced == 1 || (forced < 0 && (int64_t)Cin * Cout <= 48 * 48))
+  const int64_t cc = (int64_t)Cin * Cout;
+  if (forced == 1 || (forced < 0 && (cc <= 48 * 48 || cc >= 512 * 512)))
     return wgrad_plan_rd(N, T, Cin, Cout, f16);
   return wgrad_plan_staged(N, T, Cin, Cout, f16);
 }
