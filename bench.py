@@ -52,6 +52,10 @@ def parse():
     ap.add_argument("--tables-c", default="16,32,64,128,256,512,1024,2048",
                     help="per-group widths of --tables")
     ap.add_argument("--tables-runs", type=int, default=200, help="timed runs per measurement")
+    ap.add_argument("--blocks", action="store_true",
+                    help="only time drop-in equivariant ViT encoder blocks (Sec. 4.2; random "
+                         "weights): this library's layer vs the naive unrolled layer vs a dense "
+                         "ViT block; one JSON line per (model, dtype, linear)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB, 5 times (reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -463,6 +467,68 @@ def run_tables(args):
             print(json.dumps(rec), flush=True)
 
 
+# ViT scales of the paper's Table 6 (embedding width, heads), run at T = 4 with
+# the paper's inference batch of 128 images of 197 tokens (224 / 16 patches and
+# a class token).
+BLOCK_MODELS = {"vit_s": (480, 6), "vit_b": (768, 12), "vit_l": (1024, 16)}
+
+
+def run_blocks(args):
+    """Per-block latency of EQ-ViT encoder blocks whose four linear layers are
+    this library's layer ("flash"), the naive unrolled layer ("naive"), or a
+    dense non-equivariant layer of the same widths ("standard"): forward
+    (inference, no autograd), the four linear layers' share of it, and forward
+    + backward.  Mean of ``--tables-runs`` event-timed runs."""
+    import torch
+
+    from paper_2607_21271_amd.blocks import EQViTBlock
+    T, B, L = 4, 128, 197
+    runs = max(10, args.tables_runs // 4)
+    for name, (width, heads) in BLOCK_MODELS.items():
+        C = width // T
+        for dt in ("f32", "f16"):
+            tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+            torch.manual_seed(0)
+            x0 = torch.randn(B, L, C, T, device="cuda", dtype=tdt)
+            gy = torch.randn_like(x0)
+            res = {}
+            for lin in ("standard", "naive", "flash"):
+                print("blocks: %s %s %s" % (name, dt, lin), file=sys.stderr, flush=True)
+                torch.manual_seed(1)
+                blk = EQViTBlock(T, C, heads, linear=lin, device="cuda", dtype=tdt)
+                with torch.no_grad():
+                    fwd = _time_fn(lambda: blk(x0), runs)
+                    h = blk.norm1(x0)
+                    a = blk.attention(blk.qkv(h))
+                    m = torch.nn.functional.gelu(blk.fc1(blk.norm2(x0)))
+                    lin_t = _time_fn(lambda: (blk.qkv(h), blk.proj(a), blk.fc1(h), blk.fc2(m)), runs)
+                res[lin] = {"fwd": fwd, "linear_fwd": lin_t}
+                if dt == "f32":   # training step in fp32 only (torch's fp16 attention backward is not used)
+                    x = x0.clone().requires_grad_(True)
+
+                    def train():
+                        y = blk(x)
+                        y.backward(gy)
+                    res[lin]["fwd_bwd"] = _time_fn(train, runs)
+                    del x
+                del blk
+                torch.cuda.empty_cache()
+            rec = {"table": "block", "model": name, "dtype": dt, "T": T, "C_per_group": C,
+                   "heads": heads, "tokens": B * L, "runs": runs, "results": res,
+                   "fwd_speedup_vs_naive": round(res["naive"]["fwd"]["mean_ms"] /
+                                                 res["flash"]["fwd"]["mean_ms"], 2),
+                   "fwd_speedup_vs_standard": round(res["standard"]["fwd"]["mean_ms"] /
+                                                    res["flash"]["fwd"]["mean_ms"], 2),
+                   "fwd_bwd_speedup_vs_naive": (round(res["naive"]["fwd_bwd"]["mean_ms"] /
+                                                      res["flash"]["fwd_bwd"]["mean_ms"], 2)
+                                                if dt == "f32" else None),
+                   "linear_share_flash": round(res["flash"]["linear_fwd"]["mean_ms"] /
+                                               res["flash"]["fwd"]["mean_ms"], 3),
+                   "linear_share_naive": round(res["naive"]["linear_fwd"]["mean_ms"] /
+                                               res["naive"]["fwd"]["mean_ms"], 3)}
+            print(json.dumps(rec), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -480,6 +546,9 @@ def main():
         return
     if args.tables:
         run_tables(args)
+        return
+    if args.blocks:
+        run_blocks(args)
         return
     digest = source_digest()
     name = args.workload or synth.HEADLINE

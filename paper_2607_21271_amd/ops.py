@@ -217,18 +217,22 @@ def backward_weight_noalloc(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int,
 
 # Weight spectra of the autograd path, per weight tensor: reused while the
 # weight's storage, version counter (bumped by every in-place update, e.g. an
-# optimizer step) and the current stream are unchanged.
-_SPEC_CACHE: "weakref.WeakKeyDictionary[torch.Tensor, tuple]" = weakref.WeakKeyDictionary()
+# optimizer step) and the current stream are unchanged.  Keyed by id() with a
+# weak reference to the tensor (tensors do not compare as dictionary keys); an
+# entry leaves the cache when its tensor is freed.
+_SPEC_CACHE: dict = {}
 
 
 def cached_weight_spectrum(w: torch.Tensor) -> torch.Tensor:
     stream = torch.cuda.current_stream(w.device).cuda_stream
     key = (w.data_ptr(), w._version, tuple(w.shape), w.dtype, stream)
-    ent = _SPEC_CACHE.get(w)
-    if ent is not None and ent[0] == key:
-        return ent[1]
+    ent = _SPEC_CACHE.get(id(w))
+    if ent is not None and ent[0]() is w and ent[1] == key:
+        return ent[2]
     spec = weight_spectrum(w)
-    _SPEC_CACHE[w] = (key, spec)
+    wid = id(w)
+    ref = weakref.ref(w, lambda _r, wid=wid: _SPEC_CACHE.pop(wid, None))
+    _SPEC_CACHE[wid] = (ref, key, spec)
     return spec
 
 

@@ -105,3 +105,23 @@ def test_autograd_function_refuses_mixed_dtypes():
     w = torch.zeros(T, COUT, CIN, dtype=torch.float32)
     with pytest.raises(TypeError, match="w has dtype"):
         ops.EQLinearFunction.apply(x, w, None)
+
+
+def test_spectrum_cache_is_keyed_on_the_weight_version(monkeypatch):
+    """The autograd path recomputes the weight spectrum after an in-place update
+    of the weight and reuses it otherwise (CPU: the spectrum call is stubbed)."""
+    calls = []
+    monkeypatch.setattr(ops, "weight_spectrum", lambda w: calls.append(w._version) or object())
+    monkeypatch.setattr(ops.torch.cuda, "current_stream", lambda dev=None: type("S", (), {"cuda_stream": 0})())
+    w = torch.zeros(T, COUT, CIN)
+    a = ops.cached_weight_spectrum(w)
+    assert ops.cached_weight_spectrum(w) is a and len(calls) == 1
+    w.add_(1.0)
+    b = ops.cached_weight_spectrum(w)
+    assert b is not a and len(calls) == 2
+    w2 = torch.zeros(T, COUT, CIN)
+    ops.cached_weight_spectrum(w2)
+    assert len(calls) == 3
+    n = len(ops._SPEC_CACHE)
+    del w2
+    assert len(ops._SPEC_CACHE) == n - 1
