@@ -133,11 +133,11 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
 // fp32; the 16 x 16 layer 7.5 vs 15.0 us) and from 512 x 512 up (T = 4,
 // 32768 rows, whole backward: 1.8 vs 2.7 ms at 512 fp32, 28 vs 121 ms at
 // 2048 fp32, 7.6 vs 26.8 ms at 2048 fp16), level at 96 x 384 and 256 x 256,
-// and slower on Swin stage 1 and the 64 x 64 sweep.
+// and slower on Swin stage 1 (24 x 96: 120 vs 79 us) and the 64 x 64 sweep.
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   const int forced = wgrad_forced_kind();
-  const int64_t cc = (int64_t)Cin * Cout;
-  if (forced == 1 || (forced < 0 && (cc <= 48 * 48 || cc >= 512 * 512)))
+  const int lo = Cin < Cout ? Cin : Cout, hi = Cin < Cout ? Cout : Cin;
+  if (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512)))
     return wgrad_plan_rd(N, T, Cin, Cout, f16);
   return wgrad_plan_staged(N, T, Cin, Cout, f16);
 }
