@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 2
+#define EQLINEAR_ABI_VERSION 3
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
@@ -114,8 +114,8 @@ int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cou
 int eqlinear_forward(const void* x, const void* wspec, const void* bias, void* y, int64_t N,
                      int T, int Cin, int Cout, int dtype, void* stream);
 
-/* Input gradient (the backward pass "in the same Fourier basis" of Appendix
- * A.2 "Forward and backward passes"): dYhat = rDFT(dy),
+/* Input gradient (the backward pass computed in the Fourier basis of the
+ * forward, Appendix A.2 "Forward and backward passes"): dYhat = rDFT(dy),
  *     dXhat_k[n,c] = sum_o dYhat_k[n,o] conj(What_k[o,c]),
  * dx = irDFT(dXhat), i.e. dx[n,c,s] = sum_j sum_o w[j,o,c] dy[n,o,(s+j) mod T].
  * dy [N,Cout,T] in, dx [N,Cin,T] out; wspec as produced by
@@ -143,6 +143,40 @@ size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int C
 int eqlinear_backward_weight(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
                              size_t workspace_bytes, int64_t N, int T, int Cin, int Cout, int dtype,
                              void* stream);
+
+/* Bytes of device workspace that eqlinear_backward needs for this problem
+ * (fp32 partial sums of the weight gradient's row splits, for whichever path
+ * eqlinear_backward_is_fused reports); 0 if the arguments are invalid or
+ * N = 0. */
+size_t eqlinear_backward_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype);
+
+/* 1 if eqlinear_backward runs this problem as one fused pass, 0 if it runs
+ * the input- and weight-gradient kernels one after the other (or the
+ * arguments are invalid).  Depends only on the arguments (and on the
+ * EQL_BWD_FUSED environment variable: 0 never fuses, 1 fuses whenever the
+ * layer fits). */
+int eqlinear_backward_is_fused(int64_t N, int T, int Cin, int Cout, int dtype);
+
+/* The whole backward pass of the layer in one call: dx as
+ * eqlinear_backward_input computes it, dw and dbias as
+ * eqlinear_backward_weight computes them (same operations, same layouts,
+ * same precision rules).  Where every (input, output) channel pair of the
+ * layer fits one workgroup's accumulators and the rows are many against them
+ * (eqlinear_backward_is_fused), this runs as one pass that reads each row of
+ * x and dy once and feeds all three gradients from the same spectra, the
+ * single fused dataflow of Sec. 3.5 applied to the backward pass of Appendix
+ * A.2 ("Forward and backward passes"); then a fixed-order reduction of the
+ * weight gradient's row splits.  Otherwise the two gradient passes run one
+ * after the other on `stream`.  x [N,Cin,T], dy [N,Cout,T] and wspec (of w,
+ * from eqlinear_weight_spectrum) in; dx [N,Cin,T], dw [T,Cout,Cin] and dbias
+ * [Cout] (or NULL to skip it) out.  workspace is caller-owned device memory of
+ * at least eqlinear_backward_workspace_bytes() bytes (may be NULL when that
+ * is 0).  The fused and two-pass paths sum in different orders, so their
+ * results agree to rounding, not bitwise; each is bitwise reproducible.
+ * N = 0 writes zeros to dw and dbias and leaves dx (empty) alone. */
+int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx, void* dw, void* dbias,
+                      void* workspace, size_t workspace_bytes, int64_t N, int T, int Cin, int Cout,
+                      int dtype, void* stream);
 
 /* eqlinear_backward_weight without a workspace argument, for callers that
  * cannot allocate device memory (code under HIP graph capture, serving loops,

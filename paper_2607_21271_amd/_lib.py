@@ -41,6 +41,9 @@ SIGNATURES = {
     "eqlinear_backward_weight_workspace_bytes": (_sz, [_i64, _i, _i, _i, _i]),
     "eqlinear_backward_weight": (_i, [_vp, _vp, _vp, _vp, _vp, _sz, _i64, _i, _i, _i, _i, _vp]),
     "eqlinear_backward_weight_noalloc": (_i, [_vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _vp]),
+    "eqlinear_backward_workspace_bytes": (_sz, [_i64, _i, _i, _i, _i]),
+    "eqlinear_backward_is_fused": (_i, [_i64, _i, _i, _i, _i]),
+    "eqlinear_backward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i64, _i, _i, _i, _i, _vp]),
 }
 
 
@@ -117,3 +120,17 @@ def eqlinear_backward_weight(x, dy, dw, dbias, workspace, workspace_bytes, N, T,
 
 def eqlinear_backward_weight_noalloc(x, dy, dw, dbias, N, T, Cin, Cout, dtype, stream) -> int:
     return lib().eqlinear_backward_weight_noalloc(x, dy, dw, dbias, N, T, Cin, Cout, dtype, stream)
+
+
+def eqlinear_backward_workspace_bytes(N, T, Cin, Cout, dtype) -> int:
+    return lib().eqlinear_backward_workspace_bytes(N, T, Cin, Cout, dtype)
+
+
+def eqlinear_backward_is_fused(N, T, Cin, Cout, dtype) -> int:
+    return lib().eqlinear_backward_is_fused(N, T, Cin, Cout, dtype)
+
+
+def eqlinear_backward(x, dy, wspec, dx, dw, dbias, workspace, workspace_bytes, N, T, Cin, Cout, dtype,
+                      stream) -> int:
+    return lib().eqlinear_backward(x, dy, wspec, dx, dw, dbias, workspace, workspace_bytes, N, T, Cin,
+                                   Cout, dtype, stream)

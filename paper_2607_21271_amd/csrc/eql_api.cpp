@@ -198,6 +198,69 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
   return p;
 }
 
+// Single-pass backward: EQL_BWD_FUSED=0 never takes it, =1 takes it wherever
+// a variant fits (tests, A/B timing); unset, the rule of fused_plan decides.
+static int bwd_forced_fused() {
+  const char* v = getenv("EQL_BWD_FUSED");
+  return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
+}
+
+// The smallest variant tile that holds every channel pair (a variant built
+// for this T, LDS within the CU with one staging buffer; two when they fit), about one split per CU of a 256-CU device with at least
+// four chunks each, and each split's rows addressable with 31 bits.  Taken
+// when at least 128 splits result and the fp32 partials, written and read
+// back, cost at most half of the second read of x and dy that the two-kernel
+// path makes (large row counts against a small tile: Swin stage 1, 401,408
+// rows of 24 -> 96 channels at T = 4, writes 17 MB of partials against 385 MB
+// of x and dy; the EQ-ViT-B MLP's 96 x 384 x 8 tile does not fit one
+// workgroup at all).
+FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+  static const int kVariants[][3] = {{2, 1, 1}, {4, 1, 1}, {2, 1, 2}, {2, 2, 1}, {2, 1, 3}};
+  FusedPlan p{};
+  const int forced = bwd_forced_fused();
+  if (forced == 0 || N <= 0) return p;
+  const int KR = f16 ? 32 : 16;
+  const int C16 = round_up(Cin, 16);
+  const int nks = (Cout + KR - 1) / KR;
+  long best = -1;
+  for (const auto& v : kVariants) {
+    const int wgc = v[0], ct = v[1], otw = v[2];
+    const int BC = wgc * 16 * ct, BO = (8 / wgc) * 16 * otw;
+    if (!fused_variant_ok(T, ct, otw) || BC < Cin || BO < Cout || nks * KR > BO) continue;
+    if (fused_lds_bytes(T, BC, BO, KR, nks, C16, false) > kLdsBytes) continue;
+    const long area = (long)BC * BO;
+    if (best < 0 || area < best) {
+      best = area;
+      p.wgc = wgc; p.ct = ct; p.otw = otw; p.BC = BC; p.BO = BO;
+    }
+  }
+  if (best < 0) return p;
+  p.KR = KR;
+  p.nks = nks;
+  p.C16 = C16;
+  p.dbuf = fused_lds_bytes(T, p.BC, p.BO, KR, nks, C16, true) <= kLdsBytes ? 1 : 0;
+  p.lds = fused_lds_bytes(T, p.BC, p.BO, KR, nks, C16, p.dbuf != 0);
+  int64_t s = 256;
+  const int64_t max_s = (N + 4 * KR - 1) / (4 * KR);
+  if (s > max_s) s = max_s;
+  if (s < 1) s = 1;
+  const double eb = f16 ? 2.0 : 4.0;
+  const double row_bytes = (double)(Cin > Cout ? Cin : Cout) * T * eb;
+  while ((double)((N + s - 1) / s + KR) * row_bytes >= 2147483648.0) ++s;
+  int64_t rows = (N + s - 1) / s;
+  rows = (rows + KR - 1) / KR * KR;
+  p.S = (int)((N + rows - 1) / rows);
+  p.rows_per_split = rows;
+  p.part_bytes = (size_t)p.S * T * p.BC * p.BO * sizeof(float);
+  p.dbpart_bytes = (size_t)p.S * p.BO * sizeof(float);
+  if (forced < 0) {
+    const double xdy = (double)N * (Cin + Cout) * T * eb;
+    if (p.S < 128 || 2.0 * (double)p.part_bytes > 0.5 * xdy) return FusedPlan{};
+  }
+  p.ok = 1;
+  return p;
+}
+
 }  // namespace eqk
 
 namespace {
@@ -479,3 +542,74 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
 }
 
 
+
+// ---------------------------------------------------------------------------
+// Whole backward in one call.  With a fused plan, one pass of
+// eql_bwd_fused_kernel writes dx and the weight-gradient partials, then the
+// partial reduction writes dw and db; otherwise the input-gradient kernel and
+// the weight-gradient kernels run one after the other, exactly as the two
+// separate entry points do.
+extern "C" {
+
+int eqlinear_backward_is_fused(int64_t N, int T, int Cin, int Cout, int dtype) {
+  if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK) return 0;
+  return eqk::fused_plan(N, T, Cin, Cout, dtype == EQL_F16).ok ? 1 : 0;
+}
+
+size_t eqlinear_backward_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype) {
+  if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK || N == 0) return 0;
+  const eqk::FusedPlan f = eqk::fused_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  if (f.ok) return align256(f.part_bytes) + align256(f.dbpart_bytes);
+  return eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dtype);
+}
+
+int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx, void* dw, void* dbias,
+                      void* workspace, size_t workspace_bytes, int64_t N, int T, int Cin, int Cout,
+                      int dtype, void* stream) {
+  int st = check_shape(N, T, Cin, Cout, dtype);
+  if (st) return st;
+  if (!wspec || !dw) return EQL_ERR_INVALID_ARG;
+  if (N > 0 && (!x || !dy || !dx)) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if (!aligned(wspec, 16) || (x && !aligned(x, 16)) || (dy && !aligned(dy, 16)) || (dx && !aligned(dx, 16)) ||
+      !aligned(dw, e) || (dbias && !aligned(dbias, e)) || (workspace && !aligned(workspace, 16)))
+    return EQL_ERR_ALIGNMENT;
+  const size_t need = eqlinear_backward_workspace_bytes(N, T, Cin, Cout, dtype);
+  if (need > 0 && (!workspace || workspace_bytes < need)) return EQL_ERR_WORKSPACE;
+  const Range r[7] = {{x, (size_t)N * Cin * T * e},
+                      {dy, (size_t)N * Cout * T * e},
+                      {wspec, eqlinear_weight_spectrum_bytes(T, Cin, Cout, dtype)},
+                      {dx, (size_t)N * Cin * T * e},
+                      {dw, (size_t)T * Cin * Cout * e},
+                      {dbias, dbias ? (size_t)Cout * e : 0},
+                      {workspace, need}};
+  if (any_overlap(r, 7)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  const bool f16 = dtype == EQL_F16;
+  const eqk::FusedPlan p = eqk::fused_plan(N, T, Cin, Cout, f16);
+  if (!p.ok) {
+    st = eqlinear_backward_input(dy, wspec, dx, N, T, Cin, Cout, dtype, stream);
+    if (st) return st;
+    return eqlinear_backward_weight(x, dy, dw, dbias, workspace, workspace_bytes, N, T, Cin, Cout, dtype,
+                                    stream);
+  }
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, f16);
+  eqk::FusedArgs a{};
+  a.x = x;
+  a.dy = dy;
+  a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
+  a.dx = dx;
+  a.dw = dw;
+  a.db = dbias;
+  a.part = (float*)workspace;
+  a.dbpart = (float*)((char*)workspace + align256(p.part_bytes));
+  a.N = N;
+  a.Cin = Cin;
+  a.Cout = Cout;
+  a.CinB = d.CinB;
+  a.CoutB = d.CoutB;
+  a.stream = (hipStream_t)stream;
+  return launched(eqk::launch_bwd_fused(f16, T, a, p));
+}
+
+}  // extern "C"

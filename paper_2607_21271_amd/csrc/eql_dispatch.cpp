@@ -37,4 +37,8 @@ hipError_t launch_wgrad(bool f16, int T, const WgradArgs& a, const WgradPlan& p)
   return by_type(f16, T, [&](auto inst) { return decltype(inst)::wgrad(a, p); });
 }
 
+hipError_t launch_bwd_fused(bool f16, int T, const FusedArgs& a, const FusedPlan& p) {
+  return by_type(f16, T, [&](auto inst) { return decltype(inst)::bwd_fused(a, p); });
+}
+
 }  // namespace eqk

@@ -24,6 +24,11 @@ hipError_t Inst<T, F16>::wgrad(const WgradArgs& a, const WgradPlan& p) {
   return wgrad_t<T, F16>(a, p);
 }
 
+template <int T, bool F16>
+hipError_t Inst<T, F16>::bwd_fused(const FusedArgs& a, const FusedPlan& p) {
+  return fused_t<T, F16>(a, p);
+}
+
 template struct Inst<EQK_T, (EQK_F16 != 0)>;
 
 }  // namespace eqk

@@ -185,6 +185,45 @@ inline void wgrad_reduce_shape(int T, int S, int64_t items, int& nthr, int& ipw,
   if (G > 32) G = 32;
 }
 
+// Plan of the single-pass backward (eql_bwd_fused_kernel): the variant (wave
+// grid rows, c-tiles, o-tiles per wave of the eql_wgrad_kernel grid) whose
+// workgroup tile BC x BO holds every channel pair of the layer, the row
+// splits, the input-gradient steps of KR output channels, and the LDS.  ok = 0
+// when the layer does not take this path (then eqlinear_backward runs the
+// input- and weight-gradient kernels one after the other).  Depends only on
+// the problem, not on the device.
+struct FusedPlan {
+  int ok;
+  int wgc, ct, otw, BC, BO;
+  int KR, nks, C16;  // rows per chunk (= output channels per step), steps, Cin rounded to 16
+  int dbuf, lds;     // two staging buffers; dynamic LDS bytes
+  int S;
+  int64_t rows_per_split;
+  size_t part_bytes, dbpart_bytes;
+};
+FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16);
+// Variants of eql_bwd_fused_kernel built for group order T: those that fit
+// the 256 registers of a lane at two waves per SIMD without spilling (the
+// weight-gradient accumulators, the input-gradient tile, the prefetched raw
+// rows and the transforms; the post-build check refuses a spilling one).
+constexpr bool fused_variant_ok(int T, int ct, int otw) {
+  return ct * otw == 1 ? T <= 11
+         : (ct == 1 && otw == 2) ? T <= 6
+         : (ct == 2 && otw == 1) ? T <= 7
+         : (ct == 1 && otw == 3) ? T <= 4
+                                 : false;
+}
+// LDS bytes of one workgroup of eql_bwd_fused_kernel: one or two staging
+// buffers (x planes, dy planes by row, dy planes by output channel), then the
+// weight spectrum.  Every staged row is 64 bytes: KR rows (weight-gradient
+// staging) or KR output channels (input-gradient staging and weights) of one
+// element each.
+constexpr int kFusedRowBytes = 64;
+inline int fused_lds_bytes(int T, int BC, int BO, int KR, int nks, int C16, bool dbuf) {
+  const int stg = T * (BC + BO) * kFusedRowBytes + nks * T * KR * kFusedRowBytes;
+  return (dbuf ? 2 : 1) * stg + nks * T * C16 * kFusedRowBytes;
+}
+
 struct GemmArgs {
   const void* in;
   const void* wsp;   // plane block of the layout this pass reads
@@ -208,6 +247,20 @@ struct WgradArgs {
   hipStream_t stream;
 };
 
+struct FusedArgs {
+  const void* x;
+  const void* dy;
+  const void* wsp;   // backward-layout plane block of the weight spectrum
+  void* dx;
+  void* dw;
+  void* db;          // may be null
+  float* part;
+  float* dbpart;
+  int64_t N;
+  int Cin, Cout, CinB, CoutB;
+  hipStream_t stream;
+};
+
 // Launches of one group order and element type (eql_inst.hip, one object per
 // (T, dtype) so the instantiations build in parallel).
 template <int T, bool F16>
@@ -215,11 +268,13 @@ struct Inst {
   static hipError_t wspec(const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
   static hipError_t gemm(bool bwd, const GemmArgs& a);
   static hipError_t wgrad(const WgradArgs& a, const WgradPlan& p);
+  static hipError_t bwd_fused(const FusedArgs& a, const FusedPlan& p);
 };
 
 // Dispatch over T (eql_dispatch.cpp).
 hipError_t launch_wspec(bool f16, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
 hipError_t launch_gemm(bool f16, int T, bool bwd, const GemmArgs& a);
 hipError_t launch_wgrad(bool f16, int T, const WgradArgs& a, const WgradPlan& p);
+hipError_t launch_bwd_fused(bool f16, int T, const FusedArgs& a, const FusedPlan& p);
 
 }  // namespace eqk

@@ -7,6 +7,7 @@
 #include "eql_kernels.h"
 #include "eql_wgrad.h"
 #include "eql_wgrad_rd.h"
+#include "eql_bwd_fused.h"
 #include "eql_launch.h"
 
 namespace eqk {
@@ -174,6 +175,62 @@ hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p) {
     hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16, 1024>), dim3(blocks), dim3(1024), 0, a.stream,
                        a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
   return hipGetLastError();
+}
+
+// Single-pass backward: the fused kernel (one workgroup per row split), then
+// the split-partial reduction of the weight gradient.
+template <int T, bool F16, int WGC, int CT, int OTW>
+hipError_t fused_variant(const FusedArgs& f, const FusedPlan& p) {
+  constexpr int BC = WGC * 16 * CT, BO = (8 / WGC) * 16 * OTW;
+  constexpr int KR = F16 ? 32 : 16;
+  if (p.BC != BC || p.BO != BO || p.KR != KR || p.nks * KR > BO || p.C16 > BC ||
+      p.lds != fused_lds_bytes(T, BC, BO, KR, p.nks, p.C16, p.dbuf != 0) || p.lds > kLdsBytes)
+    return hipErrorInvalidValue;
+  WgradArgs a{};
+  a.x = f.x;
+  a.dy = f.dy;
+  a.dw = f.dw;
+  a.db = f.db;
+  a.part = f.part;
+  a.dbpart = f.dbpart;
+  a.N = f.N;
+  a.Cin = f.Cin;
+  a.Cout = f.Cout;
+  a.stream = f.stream;
+  WgradPlan wp{};
+  wp.S = p.S;
+  wp.Cin_pad = BC;
+  wp.Cout_pad = BO;
+  if (p.S > 0) {
+    auto k = eql_bwd_fused_kernel<T, F16, WGC, CT, OTW>;
+    if (p.lds > 64 * 1024) {
+      hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds);
+      if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k, dim3((unsigned)p.S), dim3(512), p.lds, f.stream, f.x, f.dy, f.wsp, f.dx, f.part,
+                       f.db ? f.dbpart : nullptr, f.N, f.Cin, f.Cout, p.rows_per_split, p.S, f.CinB,
+                       f.CoutB, p.nks, p.dbuf);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return wgrad_reduce<T, F16>(a, wp);
+}
+
+template <int T, bool F16>
+hipError_t fused_t(const FusedArgs& f, const FusedPlan& p) {
+  // the variants of fused_plan that fit the registers (fused_variant_ok)
+#define EQK_FU(W_, C_, O_)                                                  \
+  if constexpr (fused_variant_ok(T, C_, O_)) {                             \
+    if (p.wgc == (W_) && p.ct == (C_) && p.otw == (O_))                    \
+      return fused_variant<T, F16, W_, C_, O_>(f, p);                       \
+  }
+  EQK_FU(2, 1, 1)
+  EQK_FU(4, 1, 1)
+  EQK_FU(2, 1, 2)
+  EQK_FU(2, 2, 1)
+  EQK_FU(2, 1, 3)
+#undef EQK_FU
+  return hipErrorInvalidValue;
 }
 
 template <int T, bool F16>

@@ -23,6 +23,10 @@ Checks, per kernel:
                      of these kernels; the check keeps a build from carrying
                      the refused form in code that bypassed the assembler's
                      operand validation.
+  fused_scratch      a single-pass backward kernel (eql_bwd_fused_kernel) uses
+                     scratch memory: only variants that fit the registers are
+                     built, and a spilling one would run far slower than the
+                     two-kernel path the host would otherwise have chosen.
 """
 from __future__ import annotations
 
@@ -39,6 +43,7 @@ _F32_DEF = re.compile(r"^\s*(v_cvt_f32_f16\S*|v_add_f32\S*|v_sub_f32\S*|v_subrev
 _DEF_RANGE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v\[(\d+):(\d+)\]")
 _DEF_ONE = re.compile(r"^\s*(v_\S+|buffer_load\S*|global_load\S*|ds_read\S*)\s+v(\d+)\b")
 _UNPACK_FIRST = re.compile(r"^\s*v_cvt_f32_f16_e32 v(\d+), v(\d+)\s*$")
+_SCRATCH = re.compile(r"^; ScratchSize: (\d+)")
 _MFMA = re.compile(r"^\s*v_mfma\S*\s+([va])\[(\d+):(\d+)\],\s*[^,]+,\s*[^,]+,\s*([va])\[(\d+):(\d+)\]")
 
 
@@ -59,6 +64,10 @@ def scan_lines(lines):
             continue
         if "ASMEND" in line:
             in_asm = False
+            continue
+        sc = _SCRATCH.match(line)
+        if sc and kernel and "eql_bwd_fused_kernel" in kernel and int(sc.group(1)) > 0:
+            problems.append((kernel, "fused_scratch", line.strip()))
             continue
         if _BLOCK_END.match(line):
             last = {}

@@ -215,6 +215,60 @@ def backward_weight_noalloc(x: torch.Tensor, dy: torch.Tensor, T: int, Cin: int,
     return dw, db
 
 
+def backward_workspace_bytes(N: int, T: int, Cin: int, Cout: int, dtype: torch.dtype) -> int:
+    return _lib.eqlinear_backward_workspace_bytes(N, T, Cin, Cout, _DT[dtype])
+
+
+def backward_is_fused(N: int, T: int, Cin: int, Cout: int, dtype: torch.dtype) -> bool:
+    """True if ``backward`` runs this problem as one fused pass over x and dy."""
+    return bool(_lib.eqlinear_backward_is_fused(N, T, Cin, Cout, _DT[dtype]))
+
+
+def backward(x: torch.Tensor, dy: torch.Tensor, wspec: torch.Tensor, T: int, Cin: int, Cout: int,
+             with_bias: bool = True, dx: torch.Tensor | None = None, dw: torch.Tensor | None = None,
+             db: torch.Tensor | None = None, workspace: torch.Tensor | None = None, stream=None):
+    """(dx [..., Cin, T], dw [T, Cout, Cin], db [Cout] or None) in one call of
+    eqlinear_backward (one fused pass where the library plans one)."""
+    dt = _dtype_code(x)
+    _check_same_dtype(x, dy=dy)
+    if tuple(x.shape[-2:]) != (Cin, T) or tuple(dy.shape[-2:]) != (Cout, T):
+        raise ValueError("x must be [..., %d, %d] and dy [..., %d, %d], got %s and %s"
+                         % (Cin, T, Cout, T, tuple(x.shape), tuple(dy.shape)))
+    N = x.numel() // (Cin * T)
+    if dy.numel() != N * Cout * T:
+        raise ValueError("x and dy must have the same number of rows")
+    _check_wspec(wspec, T, Cin, Cout, x.dtype)
+    if not with_bias:
+        db = None
+    lead = x.shape[:-2]
+    _check_out("dx", dx, tuple(lead) + (Cin, T), x.dtype)
+    _check_out("dw", dw, (T, Cout, Cin), x.dtype)
+    _check_out("db", db, (Cout,), x.dtype)
+    need = _lib.eqlinear_backward_workspace_bytes(N, T, Cin, Cout, dt)
+    if workspace is not None:
+        if workspace.dim() != 1 or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous 1-d buffer")
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError("workspace has %d bytes, needs %d"
+                             % (workspace.numel() * workspace.element_size(), need))
+    _check_dev(x, dy, wspec, dx, dw, db, workspace)
+    x = x.contiguous()
+    dy = dy.contiguous()
+    if dx is None:
+        dx = torch.empty(*lead, Cin, T, dtype=x.dtype, device=x.device)
+    if dw is None:
+        dw = torch.empty(T, Cout, Cin, dtype=x.dtype, device=x.device)
+    if with_bias and db is None:
+        db = torch.empty(Cout, dtype=x.dtype, device=x.device)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    wsb = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _lib.check(_lib.eqlinear_backward(_ptr(x), _ptr(dy), _ptr(wspec), _ptr(dx), _ptr(dw), _ptr(db),
+                                      _ptr(workspace), wsb, N, T, Cin, Cout, dt, _stream(stream)),
+               "eqlinear_backward")
+    return dx, dw, db
+
+
 # Weight spectra of the autograd path, per weight tensor: reused while the
 # weight's storage, version counter (bumped by every in-place update, e.g. an
 # optimizer step) and the current stream are unchanged.  Keyed by id() with a
@@ -255,9 +309,12 @@ class EQLinearFunction(torch.autograd.Function):
         T, Cout, Cin = w.shape
         gy = gy.contiguous()
         gx = gw = gb = None
-        if ctx.needs_input_grad[0]:
+        want_w = ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2])
+        if ctx.needs_input_grad[0] and want_w:
+            gx, gw, gb = backward(x, gy, ctx.wspec, T, Cin, Cout, with_bias=ctx.has_bias)
+        elif ctx.needs_input_grad[0]:
             gx = backward_input(gy, ctx.wspec, T, Cin, Cout)
-        if ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2]):
+        elif want_w:
             gw, gb = backward_weight(x, gy, T, Cin, Cout, with_bias=ctx.has_bias)
         return gx, gw, gb
 

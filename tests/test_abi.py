@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 9, names
+    assert len(names) == 12, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -163,3 +163,65 @@ def test_noalloc_argument_checks(lib):
     assert g(A, A + GB, A + 2 * GB, None, N, T, C, C, L.EQL_F32, None) == L.EQL_ERR_SCRATCH
     m = re.search(r"#define EQLINEAR_STATIC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
     assert int(m.group(1)) << int(m.group(2)) == L.STATIC_SCRATCH_BYTES
+
+
+def test_whole_backward_plan_and_workspace(lib):
+    """eqlinear_backward fuses large row counts against a small tile (Swin
+    stage 1) and not the EQ-ViT-B MLP (96 x 384 x 8 does not fit one
+    workgroup); its workspace query follows the chosen path."""
+    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 1
+    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F32) == 1
+    assert L.eqlinear_backward_is_fused(12608, 8, 96, 384, L.EQL_F16) == 0
+    assert L.eqlinear_backward_is_fused(12608, 8, 48, 48, L.EQL_F16) == 0   # partials would dominate
+    assert L.eqlinear_backward_is_fused(10 ** 7, 16, 16, 16, L.EQL_F32) == 0  # no variant built for T = 16
+    assert L.eqlinear_backward_is_fused(0, 4, 24, 96, L.EQL_F16) == 0
+    assert L.eqlinear_backward_is_fused(100, 17, 4, 4, L.EQL_F16) == 0
+    assert L.eqlinear_backward_workspace_bytes(12608, 8, 96, 384, L.EQL_F16) == \
+        L.eqlinear_backward_weight_workspace_bytes(12608, 8, 96, 384, L.EQL_F16)
+    # fused: 256 splits of a 32 x 128 tile, 4 planes of fp32, plus the bias partials
+    assert L.eqlinear_backward_workspace_bytes(401408, 4, 24, 96, L.EQL_F16) == \
+        256 * 4 * 32 * 128 * 4 + 256 * 128 * 4
+    assert L.eqlinear_backward_workspace_bytes(0, 4, 24, 96, L.EQL_F16) == 0
+
+
+def test_whole_backward_forced_plan(lib, monkeypatch):
+    monkeypatch.setenv("EQL_BWD_FUSED", "1")
+    assert L.eqlinear_backward_is_fused(100, 4, 24, 96, L.EQL_F16) == 1
+    assert L.eqlinear_backward_is_fused(100, 8, 96, 384, L.EQL_F16) == 0     # no variant holds it
+    monkeypatch.setenv("EQL_BWD_FUSED", "0")
+    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 0
+
+
+def test_whole_backward_argument_checks(lib):
+    f = L.eqlinear_backward
+    N, T, Cin, Cout = 1000, 4, 24, 96
+    need = L.eqlinear_backward_workspace_bytes(N, T, Cin, Cout, L.EQL_F32)
+    base = [A, A + 8 * MB, A + 16 * MB, A + 24 * MB, A + 32 * MB, A + 33 * MB, A + 40 * MB, need,
+            N, T, Cin, Cout, L.EQL_F32, None]
+    names = ["x", "dy", "wspec", "dx", "dw", "db", "ws", "wsb", "N", "T", "Cin", "Cout", "dtype",
+             "stream"]
+
+    def call(**kw):
+        args = list(base)
+        for k, v in kw.items():
+            args[names.index(k)] = v
+        return f(*args)
+    assert call(T=0) == L.EQL_ERR_INVALID_ARG
+    assert call(T=17) == L.EQL_ERR_UNSUPPORTED
+    assert call(dtype=3) == L.EQL_ERR_INVALID_ARG
+    for k in ("x", "dy", "wspec", "dx", "dw"):
+        assert call(**{k: None}) == L.EQL_ERR_INVALID_ARG, k
+    assert call(db=None) != L.EQL_ERR_INVALID_ARG
+    assert call(x=A + 4) == L.EQL_ERR_ALIGNMENT
+    assert call(dx=A + 24 * MB + 8) == L.EQL_ERR_ALIGNMENT
+    assert call(wspec=A + 16 * MB + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(dw=A + 32 * MB + 2) == L.EQL_ERR_ALIGNMENT
+    assert call(ws=A + 40 * MB + 4) == L.EQL_ERR_ALIGNMENT
+    assert call(wsb=need - 1) == L.EQL_ERR_WORKSPACE
+    assert call(ws=None) == L.EQL_ERR_WORKSPACE
+    assert call(dx=A + 16) == L.EQL_ERR_INVALID_ARG           # dx overlaps x
+    assert call(dw=A + 8 * MB) == L.EQL_ERR_INVALID_ARG       # dw overlaps dy
+    assert call(ws=A + 24 * MB) == L.EQL_ERR_INVALID_ARG      # workspace overlaps dx
+    # N = 0: row tensors may be NULL, no workspace needed
+    r = call(N=0, x=None, dy=None, dx=None, ws=None, wsb=0)
+    assert r in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)

@@ -1,0 +1,180 @@
+"""GPU parity of the whole-backward entry point eqlinear_backward (dx, dw and db
+in one call) against the fp64 oracle, through the C ABI.
+
+The single-pass kernel is forced (EQL_BWD_FUSED=1) on small shapes that span
+several row chunks, several row splits and a ragged tail, every variant tile
+and every group order it is built for; at the full Swin stage-1 size the
+library's own plan picks it.  Same bar as the other parity tests: per output
+tensor max|gpu - oracle| / max|oracle| <= 1e-5 (fp32), <= 5e-3 (fp16).
+"""
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import TOL, rel_err, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _run_backward(inp, dt, fused_env, monkeypatch):
+    from paper_2607_21271_amd import ops
+    if fused_env is None:
+        monkeypatch.delenv("EQL_BWD_FUSED", raising=False)
+    else:
+        monkeypatch.setenv("EQL_BWD_FUSED", fused_env)
+    T, Cout, Cin = inp.w.shape
+    x, w, dy = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.dy, dt)
+    N = inp.x.shape[0]
+    fused = ops.backward_is_fused(N, T, Cin, Cout, x.dtype)
+    wspec = ops.weight_spectrum(w)
+    dx, dw, db = ops.backward(x, dy, wspec, T, Cin, Cout, with_bias=inp.b is not None)
+    torch.cuda.synchronize()
+    out = {"dx": dx.float().cpu().numpy(), "dw": dw.float().cpu().numpy(),
+           "db": None if db is None else db.float().cpu().numpy()}
+    return out, fused
+
+
+def _compare(orc, inp, dt, g, tag):
+    dx = orc.backward_input(inp.dy, inp.w)
+    dw, db = orc.backward_weight(inp.x, inp.dy, with_bias=inp.b is not None)
+    errs = {"dx": rel_err(g["dx"], dx), "dw": rel_err(g["dw"], dw)}
+    if db is not None:
+        errs["db"] = rel_err(g["db"], db)
+    say(tag, dt, {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (tag, dt, k, v)
+
+
+# (T, Cin, Cout, N, bias): every group order with a built variant, every tile
+# (32x64, 64x32, 32x128, 64x64, 32x192), ragged channel counts, a split of a
+# single partial chunk, row counts spanning many splits and a ragged tail.
+FUSED_CASES = [
+    (1, 5, 7, 37, True), (2, 16, 16, 300, True), (3, 33, 19, 1029, False), (4, 24, 96, 2085, True),
+    (4, 24, 96, 5000, False), (4, 16, 150, 777, True), (4, 40, 64, 1500, True), (4, 48, 30, 999, True),
+    (5, 20, 60, 513, True), (6, 16, 100, 611, False), (7, 33, 40, 401, True), (8, 24, 48, 1037, True),
+    (8, 32, 64, 700, True), (9, 30, 40, 300, True), (10, 64, 32, 257, False), (11, 13, 21, 129, True),
+    (4, 1, 1, 1, True), (4, 24, 96, 31, True),
+]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", FUSED_CASES,
+                         ids=["T%d-%dx%d-N%d" % c[:4] for c in FUSED_CASES])
+def test_fused_backward_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+    say("fused", T, Cin, Cout, N, bias, dt)
+    inp = synth.draw(T, Cin, Cout, N, bias, 4100 + 31 * T + Cin + 5 * Cout + N).rounded(dt)
+    g, fused = _run_backward(inp, dt, "1", monkeypatch)
+    assert fused, "a variant should hold this layer"
+    _compare(orc, inp, dt, g, "fused T%d %dx%d N%d" % (T, Cin, Cout, N))
+
+
+TWO_PASS_CASES = [(8, 96, 384, 517, False), (4, 24, 96, 2085, True), (16, 64, 64, 129, True)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", TWO_PASS_CASES,
+                         ids=["T%d-%dx%d-N%d" % c[:4] for c in TWO_PASS_CASES])
+def test_two_pass_backward_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+    say("two-pass", T, Cin, Cout, N, bias, dt)
+    inp = synth.draw(T, Cin, Cout, N, bias, 4300 + T + Cin + Cout + N).rounded(dt)
+    g, fused = _run_backward(inp, dt, "0", monkeypatch)
+    assert not fused
+    _compare(orc, inp, dt, g, "two-pass T%d %dx%d N%d" % (T, Cin, Cout, N))
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_swin_stage1_full_size_plans_fused(orc, monkeypatch, dt):
+    """Swin stage 1 at its full 401,408 rows: the library's own plan takes the
+    single pass; every element of dx, dw and db against the oracle."""
+    l = synth.LAYERS["swin_s1"]
+    say("fused full", l.name, dt, "N =", l.N)
+    inp = synth.draw_layer(l).rounded(dt)
+    g, fused = _run_backward(inp, dt, None, monkeypatch)
+    assert fused
+    _compare(orc, inp, dt, g, "swin_s1 full fused")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_fused_backward_bitwise_reproducible(monkeypatch, dt):
+    inp = synth.draw(4, 24, 96, 3001, True, 4242).rounded(dt)
+    a, fa = _run_backward(inp, dt, "1", monkeypatch)
+    b, fb = _run_backward(inp, dt, "1", monkeypatch)
+    assert fa and fb
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_whole_backward_zero_rows(monkeypatch, dt):
+    from paper_2607_21271_amd import ops
+    monkeypatch.setenv("EQL_BWD_FUSED", "1")
+    T, Cin, Cout = 4, 24, 96
+    w = to_dev(np.random.RandomState(3).standard_normal((T, Cout, Cin)), dt)
+    wspec = ops.weight_spectrum(w)
+    x = torch.empty(0, Cin, T, dtype=w.dtype, device="cuda")
+    dy = torch.empty(0, Cout, T, dtype=w.dtype, device="cuda")
+    dw = torch.full((T, Cout, Cin), 7.0, dtype=w.dtype, device="cuda")
+    db = torch.full((Cout,), 7.0, dtype=w.dtype, device="cuda")
+    dx, dw, db = ops.backward(x, dy, wspec, T, Cin, Cout, True, dw=dw, db=db)
+    torch.cuda.synchronize()
+    assert dx.shape == (0, Cin, T)
+    assert torch.all(dw == 0) and torch.all(db == 0)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_fused_backward_guard_bands(monkeypatch, dt):
+    """dx, dw and db written into views of sentinel-filled buffers leave the
+    slack alone."""
+    from paper_2607_21271_amd import ops
+    monkeypatch.setenv("EQL_BWD_FUSED", "1")
+    T, Cin, Cout, N = 4, 24, 40, 333
+    inp = synth.draw(T, Cin, Cout, N, True, 78).rounded(dt)
+    x, w, dy = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.dy, dt)
+    wspec = ops.weight_spectrum(w)
+    SENT, PAD = 12345.0, 64
+    tdt = x.dtype
+
+    def padded(n):
+        buf = torch.full((n + 2 * PAD,), SENT, dtype=tdt, device="cuda")
+        return buf, buf[PAD:PAD + n]
+    bx, vx = padded(N * Cin * T)
+    bw, vw = padded(T * Cout * Cin)
+    bb, vb = padded(Cout)
+    ops.backward(x, dy, wspec, T, Cin, Cout, True, dx=vx.view(N, Cin, T), dw=vw.view(T, Cout, Cin),
+                 db=vb)
+    torch.cuda.synchronize()
+    for buf in (bx, bw, bb):
+        assert torch.all(buf[:PAD] == SENT) and torch.all(buf[-PAD:] == SENT)
+    ref_dx, ref_dw, ref_db = ops.backward(x, dy, wspec, T, Cin, Cout, True)
+    torch.cuda.synchronize()
+    assert torch.equal(vx.view(N, Cin, T), ref_dx)
+    assert torch.equal(vw.view(T, Cout, Cin), ref_dw)
+    assert torch.equal(vb, ref_db)
+
+
+def test_autograd_uses_whole_backward(orc, monkeypatch):
+    """EQLinear under autograd: x, w and b gradients through eqlinear_backward
+    (forced single pass) against the oracle."""
+    from paper_2607_21271_amd import ops
+    monkeypatch.setenv("EQL_BWD_FUSED", "1")
+    T, Cin, Cout, N = 4, 24, 96, 700
+    inp = synth.draw(T, Cin, Cout, N, True, 91).rounded("f32")
+    x = to_dev(inp.x, "f32").requires_grad_(True)
+    w = to_dev(inp.w, "f32").requires_grad_(True)
+    b = to_dev(inp.b, "f32").requires_grad_(True)
+    y = ops.EQLinearFunction.apply(x, w, b)
+    y.backward(to_dev(inp.dy, "f32"))
+    torch.cuda.synchronize()
+    dx = orc.backward_input(inp.dy, inp.w)
+    dw, db = orc.backward_weight(inp.x, inp.dy, with_bias=True)
+    assert rel_err(x.grad.cpu().numpy(), dx) <= TOL["f32"]
+    assert rel_err(w.grad.cpu().numpy(), dw) <= TOL["f32"]
+    assert rel_err(b.grad.cpu().numpy(), db) <= TOL["f32"]

@@ -100,6 +100,29 @@ def test_backward_weight_checks():
         ops.backward_weight(x, dy, T, CIN, COUT, workspace=torch.empty(need, dtype=torch.uint8))
 
 
+def test_whole_backward_checks():
+    x = torch.zeros(N, CIN, T, dtype=torch.float16)
+    dy = torch.zeros(N, COUT, T, dtype=torch.float16)
+    with pytest.raises(TypeError, match="dy"):
+        ops.backward(x, dy.float(), spec(), T, CIN, COUT)
+    with pytest.raises(ValueError, match="rows"):
+        ops.backward(x, dy[:-1], spec(), T, CIN, COUT)
+    with pytest.raises(ValueError, match="weight spectrum"):
+        ops.backward(x, dy, spec(torch.float32), T, CIN, COUT)
+    with pytest.raises(ValueError, match="dx"):
+        ops.backward(x, dy, spec(), T, CIN, COUT, dx=torch.empty(N, COUT, T, dtype=torch.float16))
+    with pytest.raises(ValueError, match="dw"):
+        ops.backward(x, dy, spec(), T, CIN, COUT, dw=torch.empty(T, CIN, COUT, dtype=torch.float16))
+    with pytest.raises(TypeError, match="db"):
+        ops.backward(x, dy, spec(), T, CIN, COUT, db=torch.empty(COUT, dtype=torch.float32))
+    need = ops.backward_workspace_bytes(N, T, CIN, COUT, torch.float16)
+    assert need > 0
+    with pytest.raises(ValueError, match="workspace"):
+        ops.backward(x, dy, spec(), T, CIN, COUT, workspace=torch.empty(need - 1, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="GPU"):
+        ops.backward(x, dy, spec(), T, CIN, COUT)
+
+
 def test_autograd_function_refuses_mixed_dtypes():
     x = torch.zeros(N, CIN, T, dtype=torch.float16)
     w = torch.zeros(T, COUT, CIN, dtype=torch.float32)
