@@ -127,21 +127,24 @@ class Workload:
                                  dtype=torch.uint8, device="cuda")
         self.dw = torch.empty(l.T, l.Cout, l.Cin, dtype=tdt, device="cuda")
         self.db = torch.empty(l.Cout, dtype=tdt, device="cuda") if l.bias else None
-        nws = ops.workspace_bytes(l.N, l.T, l.Cin, l.Cout, tdt)
+        nws = max(ops.workspace_bytes(l.N, l.T, l.Cin, l.Cout, tdt),
+                  ops.backward_workspace_bytes(l.N, l.T, l.Cin, l.Cout, tdt))
+        self.fused = ops.backward_is_fused(l.N, l.T, l.Cin, l.Cout, tdt)
         self.ws = torch.empty(max(nws, 1), dtype=torch.uint8, device="cuda")
         self.stream = torch.cuda.current_stream()
 
     def step(self, i, stream=None):
         """One training step of the layer on input set i: weight spectrum,
-        forward, input gradient, weight and bias gradients."""
+        forward, then input, weight and bias gradients in one call of the
+        whole-backward entry point (one fused pass where the library plans
+        one, else the input- and weight-gradient kernels in turn)."""
         l, ops = self.layer, self.ops
         st = stream if stream is not None else self.stream
         x, dy, y, dx = self.sets[i % len(self.sets)]
         ops.weight_spectrum(self.w, out=self.wspec, stream=st)
         ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=st)
-        ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=st)
-        ops.backward_weight(x, dy, l.T, l.Cin, l.Cout, with_bias=l.bias, dw=self.dw, db=self.db,
-                            workspace=self.ws, stream=st)
+        ops.backward(x, dy, self.wspec, l.T, l.Cin, l.Cout, with_bias=l.bias, dx=dx, dw=self.dw,
+                     db=self.db, workspace=self.ws, stream=st)
 
     def _graph(self, fn):
         import torch
@@ -190,6 +193,9 @@ class Workload:
                 ops.weight_spectrum(self.w, out=self.wspec, stream=st)
             elif kind == "fwd":
                 ops.forward(x, self.wspec, self.b, l.T, l.Cin, l.Cout, out=y, stream=st)
+            elif kind == "bwd":
+                ops.backward(x, dy, self.wspec, l.T, l.Cin, l.Cout, with_bias=l.bias, dx=dx,
+                             dw=self.dw, db=self.db, workspace=self.ws, stream=st)
             elif kind == "dx":
                 ops.backward_input(dy, self.wspec, l.T, l.Cin, l.Cout, out=dx, stream=st)
             else:
@@ -198,7 +204,7 @@ class Workload:
 
         ops.weight_spectrum(self.w, out=self.wspec)
         out = {}
-        for kind in ("wspec", "fwd", "dx", "dw"):
+        for kind in ("wspec", "fwd", "bwd", "dx", "dw"):
             g = self._graph(lambda st: [launch(kind, r, st) for r in range(R)])
             n = max(1, reps // R)
             g.replay()
@@ -280,7 +286,8 @@ def cpu_baseline(layer, dt, inp, rows_req):
 KERNELS = {"wspec": "eqlinear_weight_spectrum (eql_wspec_kernel)",
            "fwd": "eqlinear_forward (eql_gemm_kernel, forward)",
            "dx": "eqlinear_backward_input (eql_gemm_kernel, input gradient)",
-           "dw": "eqlinear_backward_weight (eql_wgrad_kernel + eql_wgrad_reduce_kernel)"}
+           "dw": "eqlinear_backward_weight (eql_wgrad_kernel + eql_wgrad_reduce_kernel)",
+           "bwd": "eqlinear_backward, single pass (eql_bwd_fused_kernel + eql_wgrad_reduce_kernel)"}
 
 
 def measure(layer, dt, args, digest, with_cpu):
@@ -297,24 +304,26 @@ def measure(layer, dt, args, digest, with_cpu):
     flops = 3 * rf.pass_flops(N, l.T, l.Cin, l.Cout)
     dense = 3 * rf.dense_equiv_flops(N, l.T, l.Cin, l.Cout)
     nbytes = {k: rf.pass_bytes(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
-              for k in ("wspec", "fwd", "dx", "dw")}
-    dom = max(("fwd", "dx", "dw"), key=lambda k: per[k])
-    bound = "hbm" if rf.pass_bytes(dom, N, l.T, l.Cin, l.Cout, dt) / (
-        rf.PEAK_HBM_GBS * 1e9) >= rf.pass_flops(N, l.T, l.Cin, l.Cout) / (
+              for k in ("wspec", "fwd", "bwd", "dx", "dw")}
+    # the entry points the step runs: with a fused plan the whole backward is
+    # one pass (plus its reduction), else its input- and weight-gradient passes
+    step_passes = ("wspec", "fwd", "bwd") if wl.fused else ("wspec", "fwd", "dx", "dw")
+    dom = max(step_passes[1:], key=lambda k: per[k])
+    dom_flops = rf.pass_flops(N, l.T, l.Cin, l.Cout) * (2 if dom == "bwd" else 1)
+    bound = "hbm" if nbytes[dom] / (rf.PEAK_HBM_GBS * 1e9) >= dom_flops / (
         rf.PEAK_MFMA_TFLOPS[dt] * 1e12) else "mfma"
     t_dom = per[dom] * 1e-6
     if bound == "hbm":
         achieved = nbytes[dom] / t_dom / 1e9
         peak, unit = rf.PEAK_HBM_GBS, "GB/s"
     else:
-        achieved = rf.pass_flops(N, l.T, l.Cin, l.Cout) / t_dom / 1e12
+        achieved = dom_flops / t_dom / 1e12
         peak, unit = rf.PEAK_MFMA_TFLOPS[dt], "TFLOP/s"
     traffic = stored_traffic(l.name, dt, dom, digest)
     roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
             "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": KERNELS[dom],
             "algorithmic_bytes_per_launch": nbytes[dom], "avg_launch_us": round(per[dom], 2)}
-    roof_all = sum(rf.roofline_time_s(k, N, l.T, l.Cin, l.Cout, dt, l.bias)
-                   for k in ("wspec", "fwd", "dx", "dw"))
+    roof_all = sum(rf.roofline_time_s(k, N, l.T, l.Cin, l.Cout, dt, l.bias) for k in step_passes)
     rec = {
         "metric": METRIC, "value": round(N / sec, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(sec * 1e3, 4),
@@ -330,8 +339,11 @@ def measure(layer, dt, args, digest, with_cpu):
         "tflops_dense_equiv": round(dense / sec / 1e12, 2),
         "step_us": {"mean": round(sec * 1e6, 2), "median": round(_pct(per_step, 50), 2),
                     "p10": round(_pct(per_step, 10), 2), "p90": round(_pct(per_step, 90), 2)},
+        "backward": "single pass (eqlinear_backward: eql_bwd_fused_kernel + reduction)" if wl.fused
+                    else "two passes (eqlinear_backward: input-gradient kernel, then weight-gradient "
+                         "kernel + reduction)",
         "timing": "step = one replay of a HIP graph holding one input set's launches (weight "
-                  "spectrum, forward, input gradient, weight gradient); ms_per_step is the mean "
+                  "spectrum, forward, whole backward); ms_per_step is the mean "
                   "over the timed replays (host clock around all of them), step_us its "
                   "distribution from HIP events around each replay; pass_us = average launch "
                   "of each entry point, timed with HIP events around graph replays of "

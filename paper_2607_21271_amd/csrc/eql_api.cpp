@@ -213,7 +213,10 @@ static int bwd_forced_fused() {
 // path makes (large row counts against a small tile: Swin stage 1, 401,408
 // rows of 24 -> 96 channels at T = 4, writes 17 MB of partials against 385 MB
 // of x and dy; the EQ-ViT-B MLP's 96 x 384 x 8 tile does not fit one
-// workgroup at all).
+// workgroup at all).  fp16 only: in fp32 the staging does not fit two
+// buffers, and the single-buffered pass measured slower than the two kernels
+// (Swin stage 1 shape in fp32: 494 against 383 us on MI355X); fp16 Swin
+// stage 1 runs in 121 us against 162 us.
 FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   static const int kVariants[][3] = {{2, 1, 1}, {4, 1, 1}, {2, 1, 2}, {2, 2, 1}, {2, 1, 3}};
   FusedPlan p{};
@@ -226,7 +229,7 @@ FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   for (const auto& v : kVariants) {
     const int wgc = v[0], ct = v[1], otw = v[2];
     const int BC = wgc * 16 * ct, BO = (8 / wgc) * 16 * otw;
-    if (!fused_variant_ok(T, ct, otw) || BC < Cin || BO < Cout || nks * KR > BO) continue;
+    if (!fused_variant_ok(T, f16, wgc, ct, otw) || BC < Cin || BO < Cout || nks * KR > BO) continue;
     if (fused_lds_bytes(T, BC, BO, KR, nks, C16, false) > kLdsBytes) continue;
     const long area = (long)BC * BO;
     if (best < 0 || area < best) {
@@ -255,7 +258,7 @@ FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   p.dbpart_bytes = (size_t)p.S * p.BO * sizeof(float);
   if (forced < 0) {
     const double xdy = (double)N * (Cin + Cout) * T * eb;
-    if (p.S < 128 || 2.0 * (double)p.part_bytes > 0.5 * xdy) return FusedPlan{};
+    if (!f16 || p.S < 128 || 2.0 * (double)p.part_bytes > 0.5 * xdy) return FusedPlan{};
   }
   p.ok = 1;
   return p;

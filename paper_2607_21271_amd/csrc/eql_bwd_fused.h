@@ -131,25 +131,30 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
     }
   }
 
-  uint32_t rx[UX][RAW], rd[UD][RAW];
-  auto issue = [&](int chunk) __attribute__((always_inline)) {
+  // Raw rows of one chunk.  Every thread issues the same loads on every call
+  // (items past the tile or the layer's channels, and rows past the split,
+  // read from offsets beyond the buffer range and come back zero), so the
+  // compiler's memory-counter waits stay exact across the loop.
+  // NSET register sets: chunk c is loaded into set c % NSET, NSET chunks
+  // ahead of its transform, so NSET chunks of loads are in flight per thread.
+  constexpr int NSET = 2;
+  uint32_t rx[NSET][UX][RAW], rd[NSET][UD][RAW];
+  auto issue = [&](auto set, int chunk) __attribute__((always_inline)) {
+    constexpr int R = decltype(set)::value;
     const int n0 = chunk * KR;  // row offset within the split
 #pragma unroll
     for (int u = 0; u < UX; ++u) {
       const int item = tid + 512 * u;
       int c, rp;
       wgrad_item<BC>(item, c, rp);
-      if ((NIX % 512 == 0 || item < NIX) && c < Cin) {
+      const bool ok = (NIX % 512 == 0 || item < NIX) && c < Cin;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          uint32_t w[WPR];
-          load_row<T, EB>(xrs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cin + c) * ITB), w);
+      for (int h = 0; h < 2; ++h) {
+        uint32_t w[WPR];
+        const uint32_t off = ok ? (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cin + c) * ITB) : kDropOffset;
+        load_row<T, EB>(xrs, off, w);
 #pragma unroll
-          for (int q = 0; q < WPR; ++q) rx[u][h * WPR + q] = w[q];
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < RAW; ++q) rx[u][q] = 0u;
+        for (int q = 0; q < WPR; ++q) rx[R][u][h * WPR + q] = w[q];
       }
     }
 #pragma unroll
@@ -157,17 +162,14 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
       const int item = tid + 512 * u;
       int o, rp;
       wgrad_item<BO>(item, o, rp);
-      if ((NID % 512 == 0 || item < NID) && o < Cout) {
+      const bool ok = (NID % 512 == 0 || item < NID) && o < Cout;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          uint32_t w[WPR];
-          load_row<T, EB>(drs, (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cout + o) * ITB), w);
+      for (int h = 0; h < 2; ++h) {
+        uint32_t w[WPR];
+        const uint32_t off = ok ? (uint32_t)(((int64_t)(n0 + 2 * rp + h) * Cout + o) * ITB) : kDropOffset;
+        load_row<T, EB>(drs, off, w);
 #pragma unroll
-          for (int q = 0; q < WPR; ++q) rd[u][h * WPR + q] = w[q];
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < RAW; ++q) rd[u][q] = 0u;
+        for (int q = 0; q < WPR; ++q) rd[R][u][h * WPR + q] = w[q];
       }
     }
   };
@@ -177,7 +179,8 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
   for (int u = 0; u < UD; ++u) dbacc[u] = 0.0f;
 
   const int n_dr = nks * KR;  // output channels of the input-gradient staging
-  auto publish = [&](int buf) __attribute__((always_inline)) {
+  auto publish = [&](auto set, int buf) __attribute__((always_inline)) {
+    constexpr int R = decltype(set)::value;
     char* const xs = smem + buf * STG;
     char* const ds = xs + XSB;
     char* const dr = ds + DSB;
@@ -189,13 +192,13 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
       wgrad_item<BC>(item, c, rp);
       if constexpr (F16) {
         half2v P[T];
-        transform_pair<T>(rx[u], P);
+        transform_pair<T>(rx[R][u], P);
 #pragma unroll
         for (int p = 0; p < T; ++p)
           *reinterpret_cast<uint32_t*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) = __builtin_bit_cast(uint32_t, P[p]);
       } else {
         float P0[T], P1[T];
-        transform_rows<T>(rx[u], P0, P1);
+        transform_rows<T>(rx[R][u], P0, P1);
 #pragma unroll
         for (int p = 0; p < T; ++p)
           *reinterpret_cast<u32x2*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) =
@@ -214,7 +217,7 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
       char* const drs_base = dr + s * T * KR * RB;
       if constexpr (F16) {
         half2v P[T];
-        transform_pair<T>(rd[u], P);
+        transform_pair<T>(rd[R][u], P);
         dbacc[u] = __builtin_amdgcn_fdot2(P[0], half2v{(_Float16)1.0f, (_Float16)1.0f}, dbacc[u], false);
 #pragma unroll
         for (int p = 0; p < T; ++p) {
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
         }
       } else {
         float P0[T], P1[T];
-        transform_rows<T>(rd[u], P0, P1);
+        transform_rows<T>(rd[R][u], P0, P1);
         dbacc[u] += P0[0] + P1[0];
 #pragma unroll
         for (int p = 0; p < T; ++p) {
@@ -286,15 +289,26 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
 
   // input gradient of one staged chunk: D[n][c] = sum_o dYhat[n][o] conj(What[o][c])
   //   Re += Dr Wr + Di Wi,   Im += Di Wr + (-Dr) Wi
-  // Lane (g, i) of a tile ends with input channel i of rows 4g .. 4g+3 in every
-  // plane; the 16 lanes of a lane group store 16 consecutive channels of one
-  // row (16*T contiguous elements).
+  // on tiles of 16 rows x 16 input channels, one per wave (RT * C16 / 16 <= 8
+  // tiles per chunk).  Lane (g, i) of a tile ends with input channel i of rows
+  // 4g .. 4g+3 in every plane; the inverse transforms go to registers
+  // (dxv, dxoff) and dx_store writes them later, the 16 lanes of a lane group
+  // storing 16 consecutive channels of one row (16*T contiguous elements).
+  // Every wave issues the same stores on every chunk (a wave without a tile,
+  // rows past the split and channels past Cin store to an offset beyond the
+  // buffer range, which writes nothing), so the stores never make the
+  // counter waits of the next chunk's loads inexact.
+  static_assert(RT * BC / 16 <= 8, "one input-gradient tile per wave");
   const int n_tiles = RT * (C16 / 16);
-  auto dx_chunk = [&](int buf, int chunk) __attribute__((always_inline)) {
+  float dxv[4][T];
+  uint32_t dxoff[4];
+  auto dx_compute = [&](int buf, int chunk) __attribute__((always_inline)) {
     const char* const dr = smem + buf * STG + XSB + DSB;
-    for (int t = wave; t < n_tiles; t += 8) {  // uniform across the wave
-      const int rt = t % RT;
-      const int cti = t / RT;
+    const bool has_tile = wave < n_tiles;  // uniform across the wave
+    const int rt = wave % RT;
+    const int cti = wave / RT;
+    const int c = cti * 16 + li;
+    if (has_tile) {
       floatx4 ax[T];
 #pragma unroll
       for (int p = 0; p < T; ++p) ax[p] = floatx4{0.f, 0.f, 0.f, 0.f};
@@ -317,62 +331,89 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
           frag_mma<F16, KW>(ax[i], frag_neg<F16, FB>(ar), wi);
         });
       }
-      const int c = cti * 16 + li;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int64_t n = (int64_t)chunk * KR + rt * 16 + 4 * g + q;  // row within the split
-        float Pl[T], ul[T];
+        float Pl[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) Pl[p] = ax[p][q];
-        irdft<T>(Pl, ul);
-        const uint32_t off = (n < len && c < Cin) ? (uint32_t)((n * Cin + c) * ITB) : kDropOffset;
-        store_run_rsrc<F16, T>(dxrs, off, ul);
-        // one row's inverse transform at a time (four interleaved need
-        // registers that large T does not have)
-        if constexpr (T > 4) __builtin_amdgcn_sched_barrier(0);
+        irdft<T>(Pl, dxv[q]);
       }
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int64_t n = (int64_t)chunk * KR + rt * 16 + 4 * g + q;  // row within the split
+      dxoff[q] = (has_tile && n < len && c < Cin) ? (uint32_t)((n * Cin + c) * ITB) : kDropOffset;
     }
   };
+  auto dx_store = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) store_run_rsrc<F16, T>(dxrs, dxoff[q], dxv[q]);
+  };
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    dxoff[q] = kDropOffset;
+#pragma unroll
+    for (int t = 0; t < T; ++t) dxv[q][t] = 0.0f;
+  }
 
+  // Chunk loop, unrolled by NSET so that each chunk's register set is a
+  // compile-time index.  The loads of chunk ch+NSET are issued while chunk ch
+  // is computed; each wave's waits for a chunk's loads come before its dx
+  // stores of the current chunk are issued.
   if (dbuf) {
-    // chunk ch staged in buffer ch & 1; raw loads run two chunks ahead of the
-    // MFMAs; the two waves of a SIMD take the transform and the MFMAs in
-    // opposite order (as in eql_wgrad_kernel)
-    if (nchunks > 0) {
-      issue(0);
-      publish(0);
-    }
-    if (nchunks > 1) issue(1);
-    const bool transform_first = wave < 4;
-    for (int ch = 0; ch < nchunks; ++ch) {
+    // chunk ch staged in buffer ch & 1; one barrier per chunk:
+    //   barrier; MFMAs of ch (both gradients); transform chunk ch+1 into the
+    //   other buffer; dx stores of ch; loads of chunk ch+1+NSET.  (Splitting
+    //   the waves of a SIMD into transform-first and multiply-first, as the
+    //   weight-gradient kernel does, measured slower here: 138 against 121 us
+    //   on Swin stage 1.)
+    auto step = [&](auto set, int ch) __attribute__((always_inline)) {
+      using Q = std::integral_constant<int, (decltype(set)::value + 1) % NSET>;  // set of chunk ch+1
+      const int b = ch & 1;
       __syncthreads();  // chunk ch staged (and the weights at ch = 0); chunk ch-1 finished
-      const bool more = ch + 1 < nchunks;
-      if (transform_first) {
-        if (more) {
-          publish((ch + 1) & 1);
-          if (ch + 2 < nchunks) issue(ch + 2);
+      mma_chunk(b);
+      dx_compute(b, ch);
+      publish(Q{}, b ^ 1);  // chunk ch+1 (zeros past the end)
+      dx_store();
+      issue(Q{}, ch + 1 + NSET);
+    };
+    static_for<NSET>([&](auto si) { issue(si, decltype(si)::value); });
+    publish(std::integral_constant<int, 0>{}, 0);
+    issue(std::integral_constant<int, 0>{}, NSET);
+    for (int ch = 0; ch < nchunks; ch += NSET) {
+      bool done = false;
+      static_for<NSET>([&](auto si) {
+        if (!done) {
+          if (ch + decltype(si)::value >= nchunks) done = true;
+          else step(si, ch + decltype(si)::value);
         }
-        mma_chunk(ch & 1);
-        dx_chunk(ch & 1, ch);
-      } else {
-        mma_chunk(ch & 1);
-        dx_chunk(ch & 1, ch);
-        if (more) {
-          publish((ch + 1) & 1);
-          if (ch + 2 < nchunks) issue(ch + 2);
-        }
-      }
+      });
+      if (done) break;
     }
   } else {
-    if (nchunks > 0) issue(0);
-    for (int ch = 0; ch < nchunks; ++ch) {
-      publish(0);
-      __syncthreads();                       // spectra of chunk ch (and the weights) visible
-      if (ch + 1 < nchunks) issue(ch + 1);   // in flight during the MFMAs
+    //   transform chunk ch; barrier; dx stores of ch-1; loads of chunk
+    //   ch+NSET; MFMAs of ch; barrier
+    auto step = [&](auto set, int ch) __attribute__((always_inline)) {
+      publish(set, 0);
+      __syncthreads();   // spectra of chunk ch (and the weights) visible
+      dx_store();        // chunk ch-1 (nothing at ch = 0)
+      issue(set, ch + NSET);
       mma_chunk(0);
-      dx_chunk(0, ch);
-      __syncthreads();                       // staging free for the next chunk
+      dx_compute(0, ch);
+      __syncthreads();   // staging free for the next chunk
+    };
+    static_for<NSET>([&](auto si) { issue(si, decltype(si)::value); });
+    for (int ch = 0; ch < nchunks; ch += NSET) {
+      bool done = false;
+      static_for<NSET>([&](auto si) {
+        if (!done) {
+          if (ch + decltype(si)::value >= nchunks) done = true;
+          else step(si, ch + decltype(si)::value);
+        }
+      });
+      if (done) break;
     }
+    dx_store();
   }
 
   // ---- weight-gradient partial: part[split][p][c/4][o][c%4] (padded extents BC, BO)

@@ -202,16 +202,22 @@ struct FusedPlan {
   size_t part_bytes, dbpart_bytes;
 };
 FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16);
-// Variants of eql_bwd_fused_kernel built for group order T: those that fit
-// the 256 registers of a lane at two waves per SIMD without spilling (the
-// weight-gradient accumulators, the input-gradient tile, the prefetched raw
-// rows and the transforms; the post-build check refuses a spilling one).
-constexpr bool fused_variant_ok(int T, int ct, int otw) {
-  return ct * otw == 1 ? T <= 11
-         : (ct == 1 && otw == 2) ? T <= 6
-         : (ct == 2 && otw == 1) ? T <= 7
-         : (ct == 1 && otw == 3) ? T <= 4
-                                 : false;
+// Variants of eql_bwd_fused_kernel built for group order T and element
+// type: those that fit the 256 registers of a lane at two waves per SIMD
+// without spilling (the weight-gradient accumulators, the input-gradient
+// tile, two chunks of prefetched raw rows and the transforms; found by
+// compiling every variant, and the post-build check refuses a spilling one).
+constexpr bool fused_variant_ok(int T, bool f16, int ct, int otw) {
+  const int tmax = (ct == 1 && otw == 1) ? (f16 ? 6 : 11)
+                   : (ct == 2 && otw == 1) ? (f16 ? 5 : 7)
+                   : (ct == 1 && otw == 2) ? (f16 ? 4 : 5)
+                   : (ct == 1 && otw == 3) ? (f16 ? 2 : 3)
+                                           : 0;
+  return T <= tmax;
+}
+// 4 x 1 waves with one 16-channel block each: fewer registers than 2 x 4
+constexpr bool fused_variant_ok(int T, bool f16, int wgc, int ct, int otw) {
+  return wgc == 4 && ct == 1 && otw == 1 ? T <= (f16 ? 8 : 11) : fused_variant_ok(T, f16, ct, otw);
 }
 // LDS bytes of one workgroup of eql_bwd_fused_kernel: one or two staging
 // buffers (x planes, dy planes by row, dy planes by output channel), then the

@@ -220,7 +220,7 @@ template <int T, bool F16>
 hipError_t fused_t(const FusedArgs& f, const FusedPlan& p) {
   // the variants of fused_plan that fit the registers (fused_variant_ok)
 #define EQK_FU(W_, C_, O_)                                                  \
-  if constexpr (fused_variant_ok(T, C_, O_)) {                             \
+  if constexpr (fused_variant_ok(T, F16, W_, C_, O_)) {                    \
     if (p.wgc == (W_) && p.ct == (C_) && p.otw == (O_))                    \
       return fused_variant<T, F16, W_, C_, O_>(f, p);                       \
   }

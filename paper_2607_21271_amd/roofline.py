@@ -71,6 +71,8 @@ def pass_bytes(kind: str, N, T, Cin, Cout, dtype: str, bias: bool = False) -> fl
         return a + b + wb
     if kind == "dw":
         return a + b + wb + bb
+    if kind == "bwd":            # whole backward in one pass: x, dy, spectrum in; dx, dw, db out
+        return 2 * a + b + 2 * wb + bb
     if kind == "wspec":
         return 2 * wb
     raise ValueError(kind)
@@ -81,5 +83,5 @@ def roofline_time_s(kind, N, T, Cin, Cout, dtype, bias=False) -> float:
     t_mem = pass_bytes(kind, N, T, Cin, Cout, dtype, bias) / (PEAK_HBM_GBS * 1e9)
     if kind == "wspec":
         return t_mem
-    t_mma = pass_flops(N, T, Cin, Cout) / (PEAK_MFMA_TFLOPS[dtype] * 1e12)
+    t_mma = pass_flops(N, T, Cin, Cout) * (2 if kind == "bwd" else 1) / (PEAK_MFMA_TFLOPS[dtype] * 1e12)
     return max(t_mem, t_mma)

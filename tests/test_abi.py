@@ -170,7 +170,7 @@ def test_whole_backward_plan_and_workspace(lib):
     stage 1) and not the EQ-ViT-B MLP (96 x 384 x 8 does not fit one
     workgroup); its workspace query follows the chosen path."""
     assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 1
-    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F32) == 1
+    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F32) == 0   # fp16 only
     assert L.eqlinear_backward_is_fused(12608, 8, 96, 384, L.EQL_F16) == 0
     assert L.eqlinear_backward_is_fused(12608, 8, 48, 48, L.EQL_F16) == 0   # partials would dominate
     assert L.eqlinear_backward_is_fused(10 ** 7, 16, 16, 16, L.EQL_F32) == 0  # no variant built for T = 16
@@ -187,6 +187,9 @@ def test_whole_backward_plan_and_workspace(lib):
 def test_whole_backward_forced_plan(lib, monkeypatch):
     monkeypatch.setenv("EQL_BWD_FUSED", "1")
     assert L.eqlinear_backward_is_fused(100, 4, 24, 96, L.EQL_F16) == 1
+    assert L.eqlinear_backward_is_fused(100, 4, 24, 96, L.EQL_F32) == 1
+    assert L.eqlinear_backward_is_fused(100, 11, 13, 21, L.EQL_F32) == 1
+    assert L.eqlinear_backward_is_fused(100, 11, 13, 21, L.EQL_F16) == 0   # no fp16 variant at T = 11
     assert L.eqlinear_backward_is_fused(100, 8, 96, 384, L.EQL_F16) == 0     # no variant holds it
     monkeypatch.setenv("EQL_BWD_FUSED", "0")
     assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 0

@@ -53,22 +53,28 @@ def _compare(orc, inp, dt, g, tag):
         assert v <= TOL[dt], (tag, dt, k, v)
 
 
-# (T, Cin, Cout, N, bias): every group order with a built variant, every tile
-# (32x64, 64x32, 32x128, 64x64, 32x192), ragged channel counts, a split of a
-# single partial chunk, row counts spanning many splits and a ragged tail.
+# (T, Cin, Cout, N, bias, dtypes): every group order with a built variant,
+# every tile (32x64, 64x32, 32x128, 64x64, 32x192), ragged channel counts, a
+# split of a single partial chunk, row counts spanning many splits and a
+# ragged tail.
 FUSED_CASES = [
-    (1, 5, 7, 37, True), (2, 16, 16, 300, True), (3, 33, 19, 1029, False), (4, 24, 96, 2085, True),
-    (4, 24, 96, 5000, False), (4, 16, 150, 777, True), (4, 40, 64, 1500, True), (4, 48, 30, 999, True),
-    (5, 20, 60, 513, True), (6, 16, 100, 611, False), (7, 33, 40, 401, True), (8, 24, 48, 1037, True),
-    (8, 32, 64, 700, True), (9, 30, 40, 300, True), (10, 64, 32, 257, False), (11, 13, 21, 129, True),
-    (4, 1, 1, 1, True), (4, 24, 96, 31, True),
+    (1, 5, 7, 37, True, "f32 f16"), (2, 16, 16, 300, True, "f32 f16"),
+    (3, 33, 19, 1029, False, "f32 f16"), (4, 24, 96, 2085, True, "f32 f16"),
+    (4, 24, 96, 5000, False, "f32 f16"), (2, 16, 150, 777, True, "f32 f16"),
+    (4, 40, 64, 1500, True, "f32 f16"), (4, 48, 30, 999, True, "f32 f16"),
+    (5, 20, 60, 513, True, "f32 f16"), (5, 33, 40, 401, True, "f32 f16"),
+    (6, 16, 60, 611, False, "f32 f16"), (7, 30, 32, 700, True, "f32 f16"),
+    (8, 24, 30, 1037, True, "f32 f16"), (3, 16, 150, 300, True, "f32"),
+    (9, 30, 40, 300, True, "f32"), (10, 64, 32, 257, False, "f32"), (11, 13, 21, 129, True, "f32"),
+    (4, 1, 1, 1, True, "f32 f16"), (4, 24, 96, 31, True, "f32 f16"),
 ]
+FUSED_PARAMS = [(c[:5], dt) for c in FUSED_CASES for dt in c[5].split()]
 
 
-@pytest.mark.parametrize("dt", ["f32", "f16"])
-@pytest.mark.parametrize("T,Cin,Cout,N,bias", FUSED_CASES,
-                         ids=["T%d-%dx%d-N%d" % c[:4] for c in FUSED_CASES])
-def test_fused_backward_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+@pytest.mark.parametrize("case,dt", FUSED_PARAMS,
+                         ids=["T%d-%dx%d-N%d-%s" % (c[:4] + (dt,)) for c, dt in FUSED_PARAMS])
+def test_fused_backward_matches_oracle(orc, monkeypatch, case, dt):
+    T, Cin, Cout, N, bias = case
     say("fused", T, Cin, Cout, N, bias, dt)
     inp = synth.draw(T, Cin, Cout, N, bias, 4100 + 31 * T + Cin + 5 * Cout + N).rounded(dt)
     g, fused = _run_backward(inp, dt, "1", monkeypatch)
@@ -91,13 +97,25 @@ def test_two_pass_backward_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bia
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16"])
-def test_swin_stage1_full_size_plans_fused(orc, monkeypatch, dt):
-    """Swin stage 1 at its full 401,408 rows: the library's own plan takes the
-    single pass; every element of dx, dw and db against the oracle."""
+def test_swin_stage1_full_size(orc, monkeypatch, dt):
+    """Swin stage 1 at its full 401,408 rows through the library's own plan
+    (the single pass in fp16, the two kernels in fp32); every element of dx,
+    dw and db against the oracle."""
+    l = synth.LAYERS["swin_s1"]
+    say("whole backward full", l.name, dt, "N =", l.N)
+    inp = synth.draw_layer(l).rounded(dt)
+    g, fused = _run_backward(inp, dt, None, monkeypatch)
+    assert fused == (dt == "f16")
+    _compare(orc, inp, dt, g, "swin_s1 full")
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16"])
+def test_swin_stage1_full_size_forced_fused(orc, monkeypatch, dt):
+    """The same with the single pass forced (fp32 single-buffered staging)."""
     l = synth.LAYERS["swin_s1"]
     say("fused full", l.name, dt, "N =", l.N)
     inp = synth.draw_layer(l).rounded(dt)
-    g, fused = _run_backward(inp, dt, None, monkeypatch)
+    g, fused = _run_backward(inp, dt, "1", monkeypatch)
     assert fused
     _compare(orc, inp, dt, g, "swin_s1 full fused")
 
