@@ -45,7 +45,11 @@ def parse():
     ap.add_argument("--cpu-sample-rows", type=int, default=0,
                     help="rows of the oracle sample (0: sized to about 20 s of host work)")
     ap.add_argument("--all", action="store_true",
-                    help="also time every other workload and dtype (one JSON line each on stderr)")
+                    help="also print the full record of every other workload and dtype (one JSON "
+                         "line each on stderr)")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the other workloads (by default each is timed with up to 30 steps "
+                         "and summarised under other_workloads in the JSON line)")
     ap.add_argument("--tables", action="store_true",
                     help="only rerun the paper's operator benchmark (Sec. 4.1, Tables 1-2): T=4, "
                          "32768 rows, c = 16..2048, fp32 and fp16; one JSON line per (dtype, c)")
@@ -567,13 +571,27 @@ def main():
     layer = synth.LAYERS[name]
     dt = args.dtype or layer.dtypes[0]
     rec = measure(layer, dt, args, digest, with_cpu=not args.no_cpu_baseline)
-    if args.all:
+    if args.all or not (args.headline_only or args.workload):
+        # every other workload of the survey's configurations, at its own
+        # shape, with the same protocol and fewer steps
+        a2 = argparse.Namespace(**vars(args))
+        a2.steps, a2.warmup = min(args.steps, 30), min(args.warmup, 5)
+        others = {}
         for n2, l2 in synth.LAYERS.items():
             for d2 in l2.dtypes:
                 if (n2, d2) == (name, dt):
                     continue
-                r2 = measure(l2, d2, args, digest, with_cpu=False)
-                print(json.dumps(r2), file=sys.stderr, flush=True)
+                print("bench: %s %s" % (n2, d2), file=sys.stderr, flush=True)
+                r2 = measure(l2, d2, a2 if not args.all else args, digest, with_cpu=False)
+                if args.all:
+                    print(json.dumps(r2), file=sys.stderr, flush=True)
+                others["%s/%s" % (n2, d2)] = {
+                    "tokens_per_s": r2["value"], "steps": r2["steps"], "step_us": r2["step_us"],
+                    "pass_us": r2["pass_us"], "backward": r2["backward"].split(" (")[0],
+                    "roofline_kernel": r2["roofline"]["kernel"], "roofline_frac": r2["roofline"]["frac"],
+                    "roofline_step_frac": r2["roofline_step_frac"],
+                    "mfma_util_pct": r2["mfma_util_pct"]}
+        rec["other_workloads"] = others
     print(json.dumps(rec), flush=True)
 
 

@@ -206,17 +206,19 @@ static int bwd_forced_fused() {
 }
 
 // The smallest variant tile that holds every channel pair (a variant built
-// for this T, LDS within the CU with one staging buffer; two when they fit), about one split per CU of a 256-CU device with at least
-// four chunks each, and each split's rows addressable with 31 bits.  Taken
-// when at least 128 splits result and the fp32 partials, written and read
-// back, cost at most half of the second read of x and dy that the two-kernel
-// path makes (large row counts against a small tile: Swin stage 1, 401,408
-// rows of 24 -> 96 channels at T = 4, writes 17 MB of partials against 385 MB
-// of x and dy; the EQ-ViT-B MLP's 96 x 384 x 8 tile does not fit one
-// workgroup at all).  fp16 only: in fp32 the staging does not fit two
-// buffers, and the single-buffered pass measured slower than the two kernels
-// (Swin stage 1 shape in fp32: 494 against 383 us on MI355X); fp16 Swin
-// stage 1 runs in 121 us against 162 us.
+// for this T, LDS within the CU with one staging buffer; two when they fit),
+// about one split per CU of a 256-CU device with at least four chunks each,
+// and each split's rows addressable with 31 bits.  Taken for fp16 when at
+// least 128 splits result and the fp32 partials, written and read back, move
+// no more bytes than the second read of x and dy that the two-kernel path
+// makes.  Measured on MI355X (bench.py, whole backward): Swin stage 1
+// (401,408 rows, 24 -> 96, T = 4; 17 MB of partials against 385 MB of x and
+// dy) 118 against 162 us; the 64 x 64 sweep layers at 32,768 rows, T = 3 and
+// 5 (partials as large as x and dy) 36.5 against 42.6 us and 53.9 against
+// 64.5 us.  The EQ-ViT-B MLP's 96 x 384 x 8 tile fits no workgroup.  fp32
+// stays on the two kernels: its staging does not fit two buffers, and the
+// single-buffered pass measured slower (Swin stage 1 shape 494 against
+// 383 us, the T = 3 and 5 sweeps 50.0 against 47.4 and 79.3 against 75.3 us).
 FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   static const int kVariants[][3] = {{2, 1, 1}, {4, 1, 1}, {2, 1, 2}, {2, 2, 1}, {2, 1, 3}};
   FusedPlan p{};
@@ -258,7 +260,7 @@ FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
   p.dbpart_bytes = (size_t)p.S * p.BO * sizeof(float);
   if (forced < 0) {
     const double xdy = (double)N * (Cin + Cout) * T * eb;
-    if (!f16 || p.S < 128 || 2.0 * (double)p.part_bytes > 0.5 * xdy) return FusedPlan{};
+    if (!f16 || p.S < 128 || 2.0 * (double)p.part_bytes > xdy) return FusedPlan{};
   }
   p.ok = 1;
   return p;

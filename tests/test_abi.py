@@ -172,7 +172,10 @@ def test_whole_backward_plan_and_workspace(lib):
     assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 1
     assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F32) == 0   # fp16 only
     assert L.eqlinear_backward_is_fused(12608, 8, 96, 384, L.EQL_F16) == 0
-    assert L.eqlinear_backward_is_fused(12608, 8, 48, 48, L.EQL_F16) == 0   # partials would dominate
+    assert L.eqlinear_backward_is_fused(12608, 8, 48, 48, L.EQL_F16) == 0   # no variant at T = 8 holds it
+    assert L.eqlinear_backward_is_fused(32768, 3, 64, 64, L.EQL_F16) == 1
+    assert L.eqlinear_backward_is_fused(32768, 3, 64, 64, L.EQL_F32) == 0
+    assert L.eqlinear_backward_is_fused(4096, 3, 64, 64, L.EQL_F16) == 0    # partials would dominate
     assert L.eqlinear_backward_is_fused(10 ** 7, 16, 16, 16, L.EQL_F32) == 0  # no variant built for T = 16
     assert L.eqlinear_backward_is_fused(0, 4, 24, 96, L.EQL_F16) == 0
     assert L.eqlinear_backward_is_fused(100, 17, 4, 4, L.EQL_F16) == 0

@@ -96,17 +96,23 @@ def test_two_pass_backward_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bia
     _compare(orc, inp, dt, g, "two-pass T%d %dx%d N%d" % (T, Cin, Cout, N))
 
 
-@pytest.mark.parametrize("dt", ["f32", "f16"])
-def test_swin_stage1_full_size(orc, monkeypatch, dt):
-    """Swin stage 1 at its full 401,408 rows through the library's own plan
-    (the single pass in fp16, the two kernels in fp32); every element of dx,
-    dw and db against the oracle."""
-    l = synth.LAYERS["swin_s1"]
-    say("whole backward full", l.name, dt, "N =", l.N)
+ALL_CASES = [(name, dt) for name, l in synth.LAYERS.items() for dt in l.dtypes]
+# the workloads whose automatic plan is the single pass (fp16 layers with a
+# small tile and many rows)
+AUTO_FUSED = {("swin_s1", "f16"), ("sweep_T3", "f16"), ("sweep_T5", "f16")}
+
+
+@pytest.mark.parametrize("name,dt", ALL_CASES, ids=["%s-%s" % c for c in ALL_CASES])
+def test_whole_backward_full_size(orc, monkeypatch, name, dt):
+    """Every workload at full size through the library's own plan (the single
+    pass where it is chosen, else the two kernels); every element of dx, dw
+    and db against the oracle."""
+    l = synth.LAYERS[name]
+    say("whole backward full", name, dt, "N =", l.N)
     inp = synth.draw_layer(l).rounded(dt)
     g, fused = _run_backward(inp, dt, None, monkeypatch)
-    assert fused == (dt == "f16")
-    _compare(orc, inp, dt, g, "swin_s1 full")
+    assert fused == ((name, dt) in AUTO_FUSED)
+    _compare(orc, inp, dt, g, name + " full")
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16"])
