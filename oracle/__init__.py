@@ -149,3 +149,93 @@ def backward_weight(x, dy, with_bias=True):
 
 def backward_weight_entries(x, dy, j, o, c):
     return oracle().backward_weight_entries(x, dy, j, o, c)
+
+
+# ---------------------------------------------------------------------------
+# Dihedral group D_T (eqref_dihedral.c): the same weight-sharing layer over the
+# rotations and reflections of a regular T-gon.  Group index g = m*T + t
+# (t the rotation, m the reflection bit); x [N, Cin, 2T], W [2T, Cout, Cin].
+
+_DSRC = os.path.join(_HERE, "eqref_dihedral.c")
+_DLIB_PATH = os.path.join(_HERE, "libeqref_dihedral.so")
+_dlib = None
+
+
+def load_dihedral(path: str | None = None):
+    """Load the compiled dihedral oracle (building it if absent)."""
+    global _dlib
+    if path is None and _dlib is not None:
+        return _dlib
+    p = path or _DLIB_PATH
+    if path is None and (not os.path.exists(p) or os.path.getmtime(p) < os.path.getmtime(_DSRC)):
+        build(_DSRC, _DLIB_PATH)
+    lib = ctypes.CDLL(p)
+    lib.eqref_dihedral_forward.argtypes = [_D, _D, _D, _D, _i64, _int, _int, _int]
+    lib.eqref_dihedral_backward_input.argtypes = [_D, _D, _D, _i64, _int, _int, _int]
+    lib.eqref_dihedral_backward_weight.argtypes = [_D, _D, _D, _D, _i64, _int, _int, _int]
+    for f in (lib.eqref_dihedral_forward, lib.eqref_dihedral_backward_input,
+              lib.eqref_dihedral_backward_weight):
+        f.restype = None
+    lib.eqref_dihedral_mul.argtypes = [_int, _int, _int]
+    lib.eqref_dihedral_mul.restype = _int
+    lib.eqref_dihedral_inv.argtypes = [_int, _int]
+    lib.eqref_dihedral_inv.restype = _int
+    if path is None:
+        _dlib = lib
+    return lib
+
+
+class DihedralOracle:
+    """numpy front-end over the compiled D_T oracle."""
+
+    def __init__(self, lib=None):
+        self.lib = lib if lib is not None else load_dihedral()
+
+    def mul(self, a, b, T):
+        return self.lib.eqref_dihedral_mul(a, b, T)
+
+    def inv(self, a, T):
+        return self.lib.eqref_dihedral_inv(a, T)
+
+    def forward(self, x, W, b=None):
+        """y[N,Cout,2T] from x[N,Cin,2T], W[2T,Cout,Cin], b[Cout] or None."""
+        x, W = _f64(x), _f64(W)
+        b = _f64(b) if b is not None else None
+        N, Cin, G = x.shape
+        Gw, Cout, Cin_w = W.shape
+        assert Gw == G and Cin_w == Cin and G % 2 == 0
+        y = np.empty((N, Cout, G), np.float64)
+        self.lib.eqref_dihedral_forward(_ptr(x), _ptr(W), _ptr(b), _ptr(y), N, G // 2, Cin, Cout)
+        return y
+
+    def backward_input(self, dy, W):
+        """dx[N,Cin,2T] from dy[N,Cout,2T] and W[2T,Cout,Cin]."""
+        dy, W = _f64(dy), _f64(W)
+        N, Cout, G = dy.shape
+        Gw, Cout_w, Cin = W.shape
+        assert Gw == G and Cout_w == Cout
+        dx = np.empty((N, Cin, G), np.float64)
+        self.lib.eqref_dihedral_backward_input(_ptr(dy), _ptr(W), _ptr(dx), N, G // 2, Cin, Cout)
+        return dx
+
+    def backward_weight(self, x, dy, with_bias=True):
+        """(dW[2T,Cout,Cin], db[Cout] or None) from x[N,Cin,2T] and dy[N,Cout,2T]."""
+        x, dy = _f64(x), _f64(dy)
+        N, Cin, G = x.shape
+        N2, Cout, G2 = dy.shape
+        assert N2 == N and G2 == G
+        dW = np.empty((G, Cout, Cin), np.float64)
+        db = np.empty((Cout,), np.float64) if with_bias else None
+        self.lib.eqref_dihedral_backward_weight(_ptr(x), _ptr(dy), _ptr(dW), _ptr(db), N, G // 2,
+                                                Cin, Cout)
+        return dW, db
+
+
+_ddefault = None
+
+
+def dihedral_oracle() -> DihedralOracle:
+    global _ddefault
+    if _ddefault is None:
+        _ddefault = DihedralOracle()
+    return _ddefault
