@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 3
+#define EQLINEAR_ABI_VERSION 4
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
@@ -177,6 +177,33 @@ int eqlinear_backward_is_fused(int64_t N, int T, int Cin, int Cout, int dtype);
 int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx, void* dw, void* dbias,
                       void* workspace, size_t workspace_bytes, int64_t N, int T, int Cin, int Cout,
                       int dtype, void* stream);
+
+/* The equivariant linear layer over the dihedral group D_T (the T rotations
+ * and T reflections of a regular T-gon), the reflection-group generalisation
+ * that Sec. 5 names, run on the C_T entry points.  Group elements (t, m) =
+ * r^t s^m are stored at m*T + t, so x [N,Cin,2T], y [N,Cout,2T], the weight
+ * W [2T,Cout,Cin] (one Cout x Cin block per element) and b [Cout]; the layer
+ * shares weights by the group law as the C_T layer does (Sec. 3.1, Eq. 1-2):
+ *     y[n,o,g] = sum_h sum_c W[h^-1 g][o][c] x[n,c,h] + b[o].
+ * Read as [N,2Cin,T] and [N,2Cout,T] (channel 2c+m), x and y are the input and
+ * output of the C_T layer with 2Cin -> 2Cout channels and the weight
+ *     w_ct[j][2o+mg][2c+mh] = W[(mg xor mh) T + ((-1)^mh j mod T)][o][c],
+ * bias_ct[2o+mg] = b[o], so eqlinear_weight_spectrum, eqlinear_forward and
+ * eqlinear_backward with (T, 2Cin, 2Cout) compute it, at the C_T layer's
+ * T/2 saving over the dense sum.
+ *
+ * eqlinear_dihedral_expand writes w_ct [T,2Cout,2Cin] from W, and bias_ct
+ * [2Cout] from bias (both NULL, or both non-NULL).
+ * eqlinear_dihedral_fold writes the gradients with respect to W and b from
+ * those of the C_T layer: dw [2T,Cout,Cin] from dw_ct [T,2Cout,2Cin] (each W
+ * entry sums its two places in w_ct, in fp32, rounded once) and dbias [Cout]
+ * from dbias_ct [2Cout] (both NULL, or both non-NULL).
+ * Checks as for the other entry points (Cin, Cout <= 32768, element-aligned
+ * pointers, no overlap); asynchronous on `stream`. */
+int eqlinear_dihedral_expand(const void* w, const void* bias, void* w_ct, void* bias_ct, int T, int Cin,
+                             int Cout, int dtype, void* stream);
+int eqlinear_dihedral_fold(const void* dw_ct, const void* dbias_ct, void* dw, void* dbias, int T, int Cin,
+                           int Cout, int dtype, void* stream);
 
 /* eqlinear_backward_weight without a workspace argument, for callers that
  * cannot allocate device memory (code under HIP graph capture, serving loops,

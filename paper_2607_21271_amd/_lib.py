@@ -44,6 +44,8 @@ SIGNATURES = {
     "eqlinear_backward_workspace_bytes": (_sz, [_i64, _i, _i, _i, _i]),
     "eqlinear_backward_is_fused": (_i, [_i64, _i, _i, _i, _i]),
     "eqlinear_backward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i64, _i, _i, _i, _i, _vp]),
+    "eqlinear_dihedral_expand": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
+    "eqlinear_dihedral_fold": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
 }
 
 
@@ -134,3 +136,11 @@ def eqlinear_backward(x, dy, wspec, dx, dw, dbias, workspace, workspace_bytes, N
                       stream) -> int:
     return lib().eqlinear_backward(x, dy, wspec, dx, dw, dbias, workspace, workspace_bytes, N, T, Cin,
                                    Cout, dtype, stream)
+
+
+def eqlinear_dihedral_expand(w, bias, w_ct, bias_ct, T, Cin, Cout, dtype, stream) -> int:
+    return lib().eqlinear_dihedral_expand(w, bias, w_ct, bias_ct, T, Cin, Cout, dtype, stream)
+
+
+def eqlinear_dihedral_fold(dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream) -> int:
+    return lib().eqlinear_dihedral_fold(dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream)

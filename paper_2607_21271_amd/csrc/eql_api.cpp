@@ -9,6 +9,7 @@
 #include <mutex>
 
 #include "../../include/eqlinear.h"
+#include "eql_dihedral.h"
 #include "eql_launch.h"
 
 namespace eqk {
@@ -615,6 +616,76 @@ int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx
   a.CoutB = d.CoutB;
   a.stream = (hipStream_t)stream;
   return launched(eqk::launch_bwd_fused(f16, T, a, p));
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Dihedral group D_T on the C_T kernels (csrc/eql_dihedral.h): the weight
+// expansion before the forward pass and the gradient fold after the backward
+// pass.  Weight-sized gathers, grid-stride loops of 256-thread workgroups.
+namespace {
+
+int dihedral_shape(int T, int Cin, int Cout, int dtype) {
+  if (Cin < 1 || Cout < 1) return EQL_ERR_INVALID_ARG;
+  if (Cin > kMaxC / 2 || Cout > kMaxC / 2) return EQL_ERR_UNSUPPORTED;
+  return check_shape(0, T, 2 * Cin, 2 * Cout, dtype);
+}
+
+unsigned gather_grid(int64_t total) {
+  const int64_t g = (total + 255) / 256;
+  return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+}
+
+template <typename E>
+int dihedral_launch(bool expand, const void* in, const void* in_b, void* out, void* out_b, int T,
+                    int Cin, int Cout, hipStream_t s) {
+  if (expand) {
+    const int64_t total = (int64_t)T * 4 * Cin * Cout;
+    hipLaunchKernelGGL((eqk::eql_dihedral_expand_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (const E*)in_b, (E*)out, (E*)out_b, T, Cin, Cout);
+  } else {
+    const int64_t total = (int64_t)T * 2 * Cin * Cout;
+    hipLaunchKernelGGL((eqk::eql_dihedral_fold_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (const E*)in_b, (E*)out, (E*)out_b, T, Cin, Cout);
+  }
+  return launched(hipGetLastError());
+}
+
+// expand: in = W [2T,Cout,Cin], in_b = b [Cout], out = w2 [T,2Cout,2Cin], out_b = b2 [2Cout]
+// fold:   in = dw2 [T,2Cout,2Cin], in_b = db2 [2Cout], out = dW [2T,Cout,Cin], out_b = db [Cout]
+int dihedral_common(bool expand, const void* in, const void* in_b, void* out, void* out_b, int T, int Cin,
+                    int Cout, int dtype, void* stream) {
+  int st = dihedral_shape(T, Cin, Cout, dtype);
+  if (st) return st;
+  if (!in || !out || (in_b == nullptr) != (out_b == nullptr)) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if (!aligned(in, e) || !aligned(out, e) || (in_b && !aligned(in_b, e)) || (out_b && !aligned(out_b, e)))
+    return EQL_ERR_ALIGNMENT;
+  const size_t in_bytes = expand ? (size_t)2 * T * Cout * Cin * e : (size_t)4 * T * Cout * Cin * e;
+  const size_t out_bytes = expand ? (size_t)4 * T * Cout * Cin * e : (size_t)2 * T * Cout * Cin * e;
+  const size_t inb_bytes = in_b ? (expand ? (size_t)Cout : (size_t)2 * Cout) * e : 0;
+  const size_t outb_bytes = out_b ? (expand ? (size_t)2 * Cout : (size_t)Cout) * e : 0;
+  const Range r[4] = {{in, in_bytes}, {in_b, inb_bytes}, {out, out_bytes}, {out_b, outb_bytes}};
+  if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  hipStream_t s = (hipStream_t)stream;
+  return dtype == EQL_F16 ? dihedral_launch<_Float16>(expand, in, in_b, out, out_b, T, Cin, Cout, s)
+                          : dihedral_launch<float>(expand, in, in_b, out, out_b, T, Cin, Cout, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int eqlinear_dihedral_expand(const void* w, const void* bias, void* w_ct, void* bias_ct, int T, int Cin,
+                             int Cout, int dtype, void* stream) {
+  return dihedral_common(true, w, bias, w_ct, bias_ct, T, Cin, Cout, dtype, stream);
+}
+
+int eqlinear_dihedral_fold(const void* dw_ct, const void* dbias_ct, void* dw, void* dbias, int T, int Cin,
+                           int Cout, int dtype, void* stream) {
+  return dihedral_common(false, dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream);
 }
 
 }  // extern "C"

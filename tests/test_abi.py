@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 12, names
+    assert len(names) == 14, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -231,3 +231,34 @@ def test_whole_backward_argument_checks(lib):
     # N = 0: row tensors may be NULL, no workspace needed
     r = call(N=0, x=None, dy=None, dx=None, ws=None, wsb=0)
     assert r in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)
+
+
+def test_dihedral_argument_checks(lib):
+    """The dihedral weight expansion and gradient fold check shapes, pairing of
+    the bias pointers, alignment and overlap before any HIP call."""
+    T, Cin, Cout = 4, 6, 10
+    for f, nin, nout in ((L.eqlinear_dihedral_expand, 2 * T * Cin * Cout, 4 * T * Cin * Cout),
+                         (L.eqlinear_dihedral_fold, 4 * T * Cin * Cout, 2 * T * Cin * Cout)):
+        base = [A, A + 8 * MB, A + 16 * MB, A + 24 * MB, T, Cin, Cout, L.EQL_F32, None]
+
+        def call(i, v, f=f):
+            args = list(base)
+            args[i] = v
+            return f(*args)
+        assert call(4, 0) == L.EQL_ERR_INVALID_ARG
+        assert call(4, 17) == L.EQL_ERR_UNSUPPORTED
+        assert call(5, 0) == L.EQL_ERR_INVALID_ARG
+        assert call(6, -1) == L.EQL_ERR_INVALID_ARG
+        assert call(5, 40000) == L.EQL_ERR_UNSUPPORTED       # 2 Cin over 65536
+        assert call(5, 2 ** 30 + 1) == L.EQL_ERR_UNSUPPORTED  # no overflow of 2 Cin
+        assert call(7, 9) == L.EQL_ERR_INVALID_ARG
+        assert call(0, None) == L.EQL_ERR_INVALID_ARG
+        assert call(2, None) == L.EQL_ERR_INVALID_ARG
+        assert call(1, None) == L.EQL_ERR_INVALID_ARG        # one bias pointer without the other
+        assert call(3, None) == L.EQL_ERR_INVALID_ARG
+        assert call(0, A + 2) == L.EQL_ERR_ALIGNMENT
+        assert call(2, A + 4) == L.EQL_ERR_INVALID_ARG       # output overlaps input
+        assert call(2, A + nin * 4 - 4) == L.EQL_ERR_INVALID_ARG
+        assert f(A, None, A + 16 * MB, None, T, Cin, Cout, L.EQL_F32, None) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE) \
+            if not _gpu_visible() else True
+        assert nout > 0
