@@ -60,6 +60,10 @@ def parse():
                     help="only time drop-in equivariant ViT encoder blocks (Sec. 4.2; random "
                          "weights): this library's layer vs the naive unrolled layer vs a dense "
                          "ViT block; one JSON line per (model, dtype, linear)")
+    ap.add_argument("--dihedral", action="store_true",
+                    help="only time the layer over the dihedral group D_T (rotations and "
+                         "reflections, Sec. 5) on the C_T kernels against the naive dense layer; "
+                         "one JSON line per (shape, dtype)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB, 5 times (reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -545,6 +549,83 @@ def run_blocks(args):
             print(json.dumps(rec), flush=True)
 
 
+DIHEDRAL_LAYERS = [("vit_b_mlp_up_d8", 8, 48, 192, 12608), ("swin_s1_d4", 4, 12, 48, 401408)]
+
+
+def run_dihedral(args):
+    """The layer over the dihedral group D_T (rotations and reflections) on the
+    C_T kernels, against the naive layer: the dense [Cout*2T, Cin*2T] weight
+    M[(o,g),(c,h)] = W[h^-1 g][o][c] applied with F.linear (autograd folds
+    its gradient back onto W).  Two shapes whose C_T layer (2Cin -> 2Cout) is
+    the EQ-ViT-B MLP up-projection and the Swin stage-1 MLP.  Forward = one
+    layer call with the C_T weights and spectrum precomputed (a frozen weight);
+    training step = weight expansion, spectrum, forward, whole backward and
+    gradient fold (naive: dense weight gather, F.linear forward and backward).
+    Mean and median of ``--tables-runs`` event-timed runs."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+
+    from paper_2607_21271_amd import dihedral, ops
+    runs = args.tables_runs
+    for name, T, Cin, Cout, N in DIHEDRAL_LAYERS:
+        G = 2 * T
+        # index of h^-1 g for the naive dense weight: (t, m) = r^t s^m at m*T + t
+        inv = lambda a: (a // T) * T + ((a % T) if a // T else (T - a % T) % T)
+        mul = lambda a, b: ((a // T) ^ (b // T)) * T + (((a % T) - (b % T)) if a // T else
+                                                     ((a % T) + (b % T))) % T
+        idx = torch.tensor([[mul(inv(h), g) for h in range(G)] for g in range(G)], device="cuda")
+        for dt in ("f32", "f16"):
+            tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+            torch.cuda.empty_cache()
+            print("dihedral: %s %s" % (name, dt), file=sys.stderr, flush=True)
+            rs = np.random.RandomState(8100 + T)
+            x = torch.from_numpy(rs.standard_normal((N, Cin, G))).to("cuda", tdt)
+            W = torch.from_numpy(rs.standard_normal((G, Cout, Cin)) / (G * Cin) ** 0.5).to("cuda", tdt)
+            b = torch.from_numpy(0.1 * rs.standard_normal(Cout)).to("cuda", tdt)
+            gy = torch.from_numpy(rs.standard_normal((N, Cout, G))).to("cuda", tdt)
+            rec = {"table": "dihedral", "layer": name, "group": "D%d" % T, "dtype": dt, "Cin": Cin,
+                   "Cout": Cout, "rows": N, "runs": runs,
+                   "ct_layer": "T=%d %d->%d" % (T, 2 * Cin, 2 * Cout)}
+            w_ct, b_ct = dihedral.expand(W, b)
+            wspec = ops.weight_spectrum(w_ct)
+            x2 = x.view(N, 2 * Cin, T)
+            y2 = torch.empty(N, 2 * Cout, T, dtype=tdt, device="cuda")
+            rec["flash_fwd"] = _time_fn(lambda: ops.forward(x2, wspec, b_ct, T, 2 * Cin, 2 * Cout, out=y2), runs)
+            xg = x.clone().requires_grad_(True)
+            Wg = W.clone().requires_grad_(True)
+            bg = b.clone().requires_grad_(True)
+
+            def flash_train():
+                dihedral._CACHE.clear()
+                y = dihedral.DihedralEQLinearFunction.apply(xg, Wg, bg)
+                y.backward(gy)
+            rec["flash_train"] = _time_fn(flash_train, runs)
+
+            def dense(Wt):
+                return Wt[idx].permute(2, 0, 3, 1).reshape(Cout * G, Cin * G)
+            M = dense(W)
+            bd = b.repeat_interleave(G)
+            xf = x.view(N, Cin * G)
+            rec["naive_fwd"] = _time_fn(lambda: F.linear(xf, M, bd), runs)
+            xn = x.clone().requires_grad_(True)
+            Wn = W.clone().requires_grad_(True)
+            bn = b.clone().requires_grad_(True)
+
+            def naive_train():
+                y = F.linear(xn.view(N, Cin * G), dense(Wn), bn.repeat_interleave(G))
+                y.backward(gy.view(N, Cout * G))
+            rec["naive_train"] = _time_fn(naive_train, runs)
+            with torch.no_grad():
+                yf = ops.forward(x2, wspec, b_ct, T, 2 * Cin, 2 * Cout).view(N, Cout, G).float()
+                yn = F.linear(xf, M, bd).view(N, Cout, G).float()
+                rec["flash_vs_naive_rel_err"] = float((yf - yn).abs().max() / yn.abs().max())
+            rec["fwd_speedup"] = round(rec["naive_fwd"]["mean_ms"] / rec["flash_fwd"]["mean_ms"], 2)
+            rec["train_speedup"] = round(rec["naive_train"]["mean_ms"] / rec["flash_train"]["mean_ms"], 2)
+            print(json.dumps(rec), flush=True)
+            del x, W, b, gy, xg, Wg, bg, xn, Wn, bn, M, w_ct, wspec, x2, y2
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -565,6 +646,9 @@ def main():
         return
     if args.blocks:
         run_blocks(args)
+        return
+    if args.dihedral:
+        run_dihedral(args)
         return
     digest = source_digest()
     name = args.workload or synth.HEADLINE
