@@ -78,15 +78,27 @@ def short(name):
     return name.split("(")[0].replace("void ", "").replace("eqk::", "")
 
 
-def pass_of(name):
+def passes_of(name, fused):
+    """Entry points (bench.py pass names) whose launches include this kernel.
+    With a single-pass plan the split reduction serves both the weight-gradient
+    pass and the whole backward."""
     if "wspec" in name:
-        return "wspec"
+        return ["wspec"]
+    if "bwd_fused" in name:
+        return ["bwd"]
+    if "wgrad_reduce" in name:
+        return ["dw", "bwd"] if fused else ["dw"]
     if "wgrad" in name:
-        return "dw"
+        return ["dw"]
     if "gemm_kernel" in name:
         targs = name.split("<")[1].split(">")[0].split(",")
-        return "dx" if targs[2].strip() == "true" else "fwd"
-    return None
+        return ["dx"] if targs[2].strip() == "true" else ["fwd"]
+    return []
+
+
+def pass_of(name, fused=False):
+    ps = passes_of(name, fused)
+    return "/".join(ps) if ps else None
 
 
 def summarize(d, workload, dt, digest, commands):
@@ -95,7 +107,11 @@ def summarize(d, workload, dt, digest, commands):
     import synth
     from paper_2607_21271_amd import roofline as rf
     L = synth.LAYERS[workload]
+    from paper_2607_21271_amd import _lib
+    fused = bool(_lib.eqlinear_backward_is_fused(L.N, L.T, L.Cin, L.Cout,
+                                                 _lib.EQL_F16 if dt == "f16" else _lib.EQL_F32))
     tag = "%s_%s" % (workload, dt)
+    PASSES = ("wspec", "fwd", "dx", "dw") + (("bwd",) if fused else ())
     head = "Layer: T=%d, Cin=%d -> Cout=%d, N=%d, %s%s." % (L.T, L.Cin, L.Cout, L.N, dt,
                                                            ", with bias" if L.bias else "")
     # kernel trace
@@ -107,20 +123,24 @@ def summarize(d, workload, dt, digest, commands):
              "| kernel | pass | calls | avg µs | min µs | max µs | share of GPU time |",
              "|---|---|---|---|---|---|---|"]
     for name, calls, avg, mn, mx, total in st:
-        ps = pass_of(name)
+        ps = passes_of(name, fused)
         lines.append("| `%s` | %s | %d | %.2f | %.2f | %.2f | %.1f%% |" % (
-            short(name), ps or "(setup)", calls, avg, mn, mx, 100 * total / tot))
-        if ps:
-            per[ps] += avg
+            short(name), "/".join(ps) or "(setup)", calls, avg, mn, mx, 100 * total / tot))
+        for p in ps:
+            per[p] += avg
     lines += ["", "Per pass (sum of its kernels' averages): " +
-              ", ".join("%s %.2f µs" % (p, per[p]) for p in ("wspec", "fwd", "dx", "dw") if p in per), ""]
+              ", ".join("%s %.2f µs" % (p, per[p]) for p in PASSES if p in per), ""]
+    if fused:
+        lines += ["The step runs the whole backward as one pass (`bwd`: the single-pass kernel and "
+                  "the split reduction); the `dx` and `dw` passes are timed on their own entry "
+                  "points for comparison.", ""]
     open(os.path.join(PROFILES, "%s_kernel_trace.md" % tag), "w").write("\n".join(lines))
     # traffic
     rd, wr = counters(os.path.join(d, "rd")), counters(os.path.join(d, "wr"))
     crd, cwr = counters(os.path.join(d, "copy_rd")), counters(os.path.join(d, "copy_wr"))
     ck = [k for k in crd if "copy" in k.lower()][0]
     copy_bytes = 256 << 20
-    alg = {p: rf.pass_bytes(p, L.N, L.T, L.Cin, L.Cout, dt, L.bias) for p in ("wspec", "fwd", "dx", "dw")}
+    alg = {p: rf.pass_bytes(p, L.N, L.T, L.Cin, L.Cout, dt, L.bias) for p in PASSES}
     lines = ["# HBM traffic per launch: %s, %s" % (workload, dt), "", head, "",
              "Two counter passes per program (reads, then writes), and the same two on a plain "
              "256 MiB device copy:", "", "```", commands["rd"], commands["wr"], commands["copy_rd"],
@@ -137,22 +157,23 @@ def summarize(d, workload, dt, digest, commands):
              "TCC_EA0_WRREQ_64B | read MB | write MB |", "|---|---|---|---|---|---|---|---|---|"]
     ppass = collections.defaultdict(lambda: [0.0, 0.0])
     for k in rd:
-        ps = pass_of(k)
+        ps = passes_of(k, fused)
         if not ps:
             continue
         a, b = rd[k], wr.get(k, {})
         rb, wb = read_bytes(a), write_bytes(b)
-        ppass[ps][0] += rb
-        ppass[ps][1] += wb
+        for p in ps:
+            ppass[p][0] += rb
+            ppass[p][1] += wb
         lines.append("| `%s` | %s | %.0f | %.0f | %.0f | %.0f | %.0f | %.2f | %.2f |" % (
-            short(k), ps, a.get("TCC_EA0_RDREQ_sum", 0), a.get("TCC_EA0_RDREQ_32B_sum", 0),
+            short(k), "/".join(ps), a.get("TCC_EA0_RDREQ_sum", 0), a.get("TCC_EA0_RDREQ_32B_sum", 0),
             a.get("TCC_BUBBLE_sum", 0), b.get("TCC_EA0_WRREQ_sum", 0), b.get("TCC_EA0_WRREQ_64B_sum", 0),
             rb / 1e6, wb / 1e6))
     lines += ["", "| pass | HBM bytes per launch (read + write) | algorithmic bytes | ratio |",
               "|---|---|---|---|"]
     tpath = os.path.join(PROFILES, "traffic.json")
     traffic = json.load(open(tpath)) if os.path.exists(tpath) else {}
-    for ps in ("wspec", "fwd", "dx", "dw"):
+    for ps in PASSES:
         if ps not in ppass:
             continue
         rb, wb = ppass[ps]
@@ -178,7 +199,7 @@ def summarize(d, workload, dt, digest, commands):
                  "| kernel | pass | cycles µs | MFMA util | VALU issue | LDS B/CU/clk (max) | "
                  "LDS bank conflict / active | waves |", "|---|---|---|---|---|---|---|---|"]
         for k in p1:
-            ps = pass_of(k)
+            ps = pass_of(k, fused)
             if not ps:
                 continue
             a, b = p1[k], p2.get(k, {})
@@ -229,7 +250,8 @@ def main(argv):
     bench = importlib.util.module_from_spec(spec)
     spec.loader.exec_module(bench)
     digest = bench.source_digest()
-    commands = commands_for(workload, dt)
+    commands = {k: c.replace("<out>", d.rstrip("/")) + " > %s/%s.log 2>&1" % (d.rstrip("/"), k)
+                for k, c in commands_for(workload, dt).items()}
     summarize(d, workload, dt, digest, commands)
     return commands
 
