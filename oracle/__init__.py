@@ -239,3 +239,79 @@ def dihedral_oracle() -> DihedralOracle:
     if _ddefault is None:
         _ddefault = DihedralOracle()
     return _ddefault
+
+
+# ---------------------------------------------------------------------------
+# Rotation-equivariant group convolution on a square grid (eqref_gconv.c):
+# f [B, H, W, Cin, T], psi [k, k, T, Cout, Cin], out [B, H, W, Cout, T],
+# T in {1, 2, 4}, k odd.
+
+_GSRC = os.path.join(_HERE, "eqref_gconv.c")
+_GLIB_PATH = os.path.join(_HERE, "libeqref_gconv.so")
+_glib = None
+
+
+def load_gconv(path: str | None = None):
+    """Load the compiled group-convolution oracle (building it if absent)."""
+    global _glib
+    if path is None and _glib is not None:
+        return _glib
+    p = path or _GLIB_PATH
+    if path is None and (not os.path.exists(p) or os.path.getmtime(p) < os.path.getmtime(_GSRC)):
+        build(_GSRC, _GLIB_PATH)
+    lib = ctypes.CDLL(p)
+    dims = [_int] * 7
+    lib.eqref_gconv_forward.argtypes = [_D, _D, _D, _D] + dims
+    lib.eqref_gconv_backward_input.argtypes = [_D, _D, _D] + dims
+    lib.eqref_gconv_backward_weight.argtypes = [_D, _D, _D, _D] + dims
+    for f in (lib.eqref_gconv_forward, lib.eqref_gconv_backward_input, lib.eqref_gconv_backward_weight):
+        f.restype = None
+    if path is None:
+        _glib = lib
+    return lib
+
+
+class GconvOracle:
+    """numpy front-end over the compiled group-convolution oracle."""
+
+    def __init__(self, lib=None):
+        self.lib = lib if lib is not None else load_gconv()
+
+    def forward(self, f, psi, bias=None):
+        f, psi = _f64(f), _f64(psi)
+        bias = _f64(bias) if bias is not None else None
+        B, H, W, Cin, T = f.shape
+        k, k2, T2, Cout, Cin2 = psi.shape
+        assert k == k2 and k % 2 == 1 and T2 == T and Cin2 == Cin
+        out = np.empty((B, H, W, Cout, T), np.float64)
+        self.lib.eqref_gconv_forward(_ptr(f), _ptr(psi), _ptr(bias), _ptr(out), B, H, W, T, Cin, Cout, k)
+        return out
+
+    def backward_input(self, dout, psi):
+        dout, psi = _f64(dout), _f64(psi)
+        B, H, W, Cout, T = dout.shape
+        k, _, _, Cout2, Cin = psi.shape
+        assert Cout2 == Cout
+        df = np.empty((B, H, W, Cin, T), np.float64)
+        self.lib.eqref_gconv_backward_input(_ptr(dout), _ptr(psi), _ptr(df), B, H, W, T, Cin, Cout, k)
+        return df
+
+    def backward_weight(self, f, dout, k, with_bias=True):
+        f, dout = _f64(f), _f64(dout)
+        B, H, W, Cin, T = f.shape
+        Cout = dout.shape[3]
+        dpsi = np.empty((k, k, T, Cout, Cin), np.float64)
+        db = np.empty((Cout,), np.float64) if with_bias else None
+        self.lib.eqref_gconv_backward_weight(_ptr(f), _ptr(dout), _ptr(dpsi), _ptr(db), B, H, W, T, Cin,
+                                             Cout, k)
+        return dpsi, db
+
+
+_gdefault = None
+
+
+def gconv_oracle() -> GconvOracle:
+    global _gdefault
+    if _gdefault is None:
+        _gdefault = GconvOracle()
+    return _gdefault
