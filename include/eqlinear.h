@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 4
+#define EQLINEAR_ABI_VERSION 5
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
@@ -204,6 +204,37 @@ int eqlinear_dihedral_expand(const void* w, const void* bias, void* w_ct, void* 
                              int Cout, int dtype, void* stream);
 int eqlinear_dihedral_fold(const void* dw_ct, const void* dbias_ct, void* dw, void* dbias, int T, int Cin,
                            int Cout, int dtype, void* stream);
+
+/* The rotation-equivariant group convolution on a square grid, the
+ * equivariant-convolution generalisation that Sec. 5 names, run on the C_T
+ * entry points.  T in {1, 2, 4}: rotations by 360/T degrees act on the image
+ * plane and on the group axis.  Features f [B,H,W,Cin,T], output
+ * [B,H,W,Cout,T], weight psi [k,k,T,Cout,Cin] (k odd, at most 7; one
+ * Cout x Cin block per window offset (a, b) and group lag, stored at
+ * (a + k/2, b + k/2, lag)), bias [Cout]:
+ *     out[n,o,r] = sum_{(a,b)} sum_s sum_c psi[R^-r (a,b)][(s - r) mod T][o][c]
+ *                  * f[n + (a,b), c, s] + bias[o]
+ * with f zero outside the image and R(a, b) = (-b, a) (T = 4), (-a, -b)
+ * (T = 2).  Splitting the window into rotation orbits turns it into ONE C_T
+ * layer with k*k*Cin input channels: eqlinear_gconv_gather writes its input
+ * xcol [B*H*W, k*k*Cin, T] from f, eqlinear_gconv_pack_weight its weight
+ * w_ct [T, Cout, k*k*Cin] from psi; eqlinear_weight_spectrum /
+ * eqlinear_forward / eqlinear_backward with (T, k*k*Cin, Cout) then give the
+ * output and the C_T gradients, eqlinear_gconv_scatter folds the gradient of
+ * xcol back to df [B,H,W,Cin,T] (the adjoint of the gather, an fp32 sum of
+ * each pixel's k*k entries) and eqlinear_gconv_unpack_weight the gradient of
+ * w_ct back to dpsi [k,k,T,Cout,Cin] (a permutation).  The orbit order and
+ * channel layout of xcol are documented in csrc/eql_gconv.h.  Checks as for
+ * the other entry points (T not in {1, 2, 4} or k even or above 7 is
+ * EQL_ERR_UNSUPPORTED); B, H or W = 0 is a no-op for the gather and scatter. */
+int eqlinear_gconv_gather(const void* f, void* xcol, int64_t B, int H, int W, int T, int Cin, int k, int dtype,
+                          void* stream);
+int eqlinear_gconv_scatter(const void* dxcol, void* df, int64_t B, int H, int W, int T, int Cin, int k,
+                           int dtype, void* stream);
+int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int Cout, int k, int dtype,
+                               void* stream);
+int eqlinear_gconv_unpack_weight(const void* dw_ct, void* dpsi, int T, int Cin, int Cout, int k, int dtype,
+                                 void* stream);
 
 /* eqlinear_backward_weight without a workspace argument, for callers that
  * cannot allocate device memory (code under HIP graph capture, serving loops,

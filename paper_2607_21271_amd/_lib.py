@@ -46,6 +46,10 @@ SIGNATURES = {
     "eqlinear_backward": (_i, [_vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _i64, _i, _i, _i, _i, _vp]),
     "eqlinear_dihedral_expand": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
     "eqlinear_dihedral_fold": (_i, [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _vp]),
+    "eqlinear_gconv_gather": (_i, [_vp, _vp, _i64, _i, _i, _i, _i, _i, _i, _vp]),
+    "eqlinear_gconv_scatter": (_i, [_vp, _vp, _i64, _i, _i, _i, _i, _i, _i, _vp]),
+    "eqlinear_gconv_pack_weight": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "eqlinear_gconv_unpack_weight": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
 }
 
 
@@ -144,3 +148,19 @@ def eqlinear_dihedral_expand(w, bias, w_ct, bias_ct, T, Cin, Cout, dtype, stream
 
 def eqlinear_dihedral_fold(dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream) -> int:
     return lib().eqlinear_dihedral_fold(dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream)
+
+
+def eqlinear_gconv_gather(f, xcol, B, H, W, T, Cin, k, dtype, stream) -> int:
+    return lib().eqlinear_gconv_gather(f, xcol, B, H, W, T, Cin, k, dtype, stream)
+
+
+def eqlinear_gconv_scatter(dxcol, df, B, H, W, T, Cin, k, dtype, stream) -> int:
+    return lib().eqlinear_gconv_scatter(dxcol, df, B, H, W, T, Cin, k, dtype, stream)
+
+
+def eqlinear_gconv_pack_weight(psi, w_ct, T, Cin, Cout, k, dtype, stream) -> int:
+    return lib().eqlinear_gconv_pack_weight(psi, w_ct, T, Cin, Cout, k, dtype, stream)
+
+
+def eqlinear_gconv_unpack_weight(dw_ct, dpsi, T, Cin, Cout, k, dtype, stream) -> int:
+    return lib().eqlinear_gconv_unpack_weight(dw_ct, dpsi, T, Cin, Cout, k, dtype, stream)

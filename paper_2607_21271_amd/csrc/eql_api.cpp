@@ -10,6 +10,7 @@
 
 #include "../../include/eqlinear.h"
 #include "eql_dihedral.h"
+#include "eql_gconv.h"
 #include "eql_launch.h"
 
 namespace eqk {
@@ -686,6 +687,101 @@ int eqlinear_dihedral_expand(const void* w, const void* bias, void* w_ct, void* 
 int eqlinear_dihedral_fold(const void* dw_ct, const void* dbias_ct, void* dw, void* dbias, int T, int Cin,
                            int Cout, int dtype, void* stream) {
   return dihedral_common(false, dw_ct, dbias_ct, dw, dbias, T, Cin, Cout, dtype, stream);
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Rotation-equivariant group convolution on the C_T kernels
+// (csrc/eql_gconv.h): patch gather, its adjoint, weight permutation both ways.
+namespace {
+
+int gconv_shape(int T, int Cin, int Cout, int k, int dtype) {
+  if (dtype != EQL_F32 && dtype != EQL_F16) return EQL_ERR_INVALID_ARG;
+  if (Cin < 1 || Cout < 1 || k < 1) return EQL_ERR_INVALID_ARG;
+  if (T != 1 && T != 2 && T != 4) return EQL_ERR_UNSUPPORTED;
+  if (k % 2 == 0 || k > 7) return EQL_ERR_UNSUPPORTED;
+  if (Cin > kMaxC / (k * k) || Cout > kMaxC) return EQL_ERR_UNSUPPORTED;
+  return EQL_OK;
+}
+
+int gconv_image(int64_t B, int H, int W) {
+  if (B < 0 || H < 0 || W < 0) return EQL_ERR_INVALID_ARG;
+  if ((double)B * H * W > (double)kMaxN) return EQL_ERR_UNSUPPORTED;
+  return EQL_OK;
+}
+
+template <typename E>
+int gconv_launch(int op, const void* in, void* out, int64_t B, int H, int W, int T, int Cin, int Cout, int k,
+                 hipStream_t s) {
+  const int64_t n_pix = B * H * W;
+  if (op == 0) {
+    const int64_t total = n_pix * k * k * Cin * T;
+    if (total == 0) return EQL_OK;
+    hipLaunchKernelGGL((eqk::eql_gconv_gather_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (E*)out, B, H, W, T, Cin, k);
+  } else if (op == 1) {
+    const int64_t total = n_pix * Cin * T;
+    if (total == 0) return EQL_OK;
+    hipLaunchKernelGGL((eqk::eql_gconv_scatter_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (E*)out, B, H, W, T, Cin, k);
+  } else if (op == 2) {
+    const int64_t total = (int64_t)T * Cout * k * k * Cin;
+    hipLaunchKernelGGL((eqk::eql_gconv_pack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (E*)out, T, Cin, Cout, k);
+  } else {
+    const int64_t total = (int64_t)T * Cout * k * k * Cin;
+    hipLaunchKernelGGL((eqk::eql_gconv_unpack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                       (const E*)in, (E*)out, T, Cin, Cout, k);
+  }
+  return launched(hipGetLastError());
+}
+
+// op 0 gather (in f, out X), 1 scatter (in dX, out df), 2 pack (in psi, out w),
+// 3 unpack (in dw, out dpsi)
+int gconv_common(int op, const void* in, void* out, int64_t B, int H, int W, int T, int Cin, int Cout, int k,
+                 int dtype, void* stream) {
+  int st = gconv_shape(T, Cin, Cout, k, dtype);
+  if (st) return st;
+  if (op < 2 && (st = gconv_image(B, H, W))) return st;
+  const int64_t n_pix = op < 2 ? B * H * W : 0;
+  if ((op >= 2 || n_pix > 0) && (!in || !out)) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if ((in && !aligned(in, e)) || (out && !aligned(out, e))) return EQL_ERR_ALIGNMENT;
+  const size_t fb = (size_t)n_pix * Cin * T * e, xb = (size_t)n_pix * k * k * Cin * T * e;
+  const size_t wb = (size_t)T * Cout * k * k * Cin * e;
+  const size_t in_b = op == 0 ? fb : op == 1 ? xb : wb;
+  const size_t out_b = op == 0 ? xb : op == 1 ? fb : wb;
+  const Range r[2] = {{in, in_b}, {out, out_b}};
+  if (any_overlap(r, 2)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  hipStream_t s = (hipStream_t)stream;
+  return dtype == EQL_F16 ? gconv_launch<_Float16>(op, in, out, B, H, W, T, Cin, Cout, k, s)
+                          : gconv_launch<float>(op, in, out, B, H, W, T, Cin, Cout, k, s);
+}
+
+}  // namespace
+
+extern "C" {
+
+int eqlinear_gconv_gather(const void* f, void* xcol, int64_t B, int H, int W, int T, int Cin, int k, int dtype,
+                          void* stream) {
+  return gconv_common(0, f, xcol, B, H, W, T, Cin, 1, k, dtype, stream);
+}
+
+int eqlinear_gconv_scatter(const void* dxcol, void* df, int64_t B, int H, int W, int T, int Cin, int k,
+                           int dtype, void* stream) {
+  return gconv_common(1, dxcol, df, B, H, W, T, Cin, 1, k, dtype, stream);
+}
+
+int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int Cout, int k, int dtype,
+                               void* stream) {
+  return gconv_common(2, psi, w_ct, 0, 0, 0, T, Cin, Cout, k, dtype, stream);
+}
+
+int eqlinear_gconv_unpack_weight(const void* dw_ct, void* dpsi, int T, int Cin, int Cout, int k, int dtype,
+                                 void* stream) {
+  return gconv_common(3, dw_ct, dpsi, 0, 0, 0, T, Cin, Cout, k, dtype, stream);
 }
 
 }  // extern "C"

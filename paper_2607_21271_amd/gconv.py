@@ -1,0 +1,152 @@
+"""Rotation-equivariant group convolution on a square grid, on the C_T library.
+
+The rotations by 360/T degrees (T in {1, 2, 4}) act on the image plane and on
+the group axis of the features; Sec. 5 of the paper names equivariant
+convolutions as the next operators to carry the method to.  Features are
+f [B, H, W, Cin, T], the weight psi [k, k, T, Cout, Cin] holds one Cout x Cin
+block per window offset and group lag, b [Cout]:
+
+    out[n,o,r] = sum_{(a,b)} sum_s sum_c psi[R^-r (a,b)][(s - r) mod T][o][c] f[n + (a,b), c, s] + b[o]
+
+(zero padding, k odd).  Split into rotation orbits of the window, this is one
+C_T layer with k*k*Cin input channels on gathered patches
+(``eqlinear_gconv_gather``) with a permuted weight
+(``eqlinear_gconv_pack_weight``); the forward pass and the gradients run on
+the C_T kernels, and ``eqlinear_gconv_scatter`` / ``eqlinear_gconv_unpack_weight``
+take the gradients back.  This module only allocates and marshals.
+"""
+from __future__ import annotations
+
+import weakref
+
+import torch
+
+from . import _lib, ops
+
+
+def _dims(f, Cin, T):
+    if f.dim() != 5 or tuple(f.shape[-2:]) != (Cin, T):
+        raise ValueError("features must be [B, H, W, Cin=%d, T=%d], got %s" % (Cin, T, tuple(f.shape)))
+    return f.shape[0], f.shape[1], f.shape[2]
+
+
+def gather(f: torch.Tensor, T: int, k: int, stream=None) -> torch.Tensor:
+    """xcol [B*H*W, k*k*Cin, T] from f [B, H, W, Cin, T]."""
+    Cin = f.shape[-2]
+    B, H, W = _dims(f, Cin, T)
+    dt = ops._dtype_code(f)
+    f = f.contiguous()
+    ops._check_dev(f)
+    xcol = torch.empty(B * H * W, k * k * Cin, T, dtype=f.dtype, device=f.device)
+    _lib.check(_lib.eqlinear_gconv_gather(ops._ptr(f), ops._ptr(xcol), B, H, W, T, Cin, k, dt,
+                                          ops._stream(stream)), "eqlinear_gconv_gather")
+    return xcol
+
+
+def scatter(dxcol: torch.Tensor, B: int, H: int, W: int, T: int, Cin: int, k: int, stream=None) -> torch.Tensor:
+    """df [B, H, W, Cin, T] from the gradient of xcol (the gather's adjoint)."""
+    ops._check_out("dxcol", dxcol, (B * H * W, k * k * Cin, T), dxcol.dtype)
+    dt = ops._dtype_code(dxcol)
+    ops._check_dev(dxcol)
+    df = torch.empty(B, H, W, Cin, T, dtype=dxcol.dtype, device=dxcol.device)
+    _lib.check(_lib.eqlinear_gconv_scatter(ops._ptr(dxcol), ops._ptr(df), B, H, W, T, Cin, k, dt,
+                                           ops._stream(stream)), "eqlinear_gconv_scatter")
+    return df
+
+
+def pack_weight(psi: torch.Tensor, stream=None) -> torch.Tensor:
+    """w_ct [T, Cout, k*k*Cin] from psi [k, k, T, Cout, Cin]."""
+    if psi.dim() != 5 or psi.shape[0] != psi.shape[1]:
+        raise ValueError("psi must be [k, k, T, Cout, Cin], got %s" % (tuple(psi.shape),))
+    k, _, T, Cout, Cin = psi.shape
+    dt = ops._dtype_code(psi)
+    psi = psi.contiguous()
+    ops._check_dev(psi)
+    w = torch.empty(T, Cout, k * k * Cin, dtype=psi.dtype, device=psi.device)
+    _lib.check(_lib.eqlinear_gconv_pack_weight(ops._ptr(psi), ops._ptr(w), T, Cin, Cout, k, dt,
+                                               ops._stream(stream)), "eqlinear_gconv_pack_weight")
+    return w
+
+
+def unpack_weight_grad(dw_ct: torch.Tensor, k: int, stream=None) -> torch.Tensor:
+    """dpsi [k, k, T, Cout, Cin] from the gradient of w_ct [T, Cout, k*k*Cin]."""
+    T, Cout, C2 = dw_ct.shape
+    if C2 % (k * k):
+        raise ValueError("dw_ct channels %d are not a multiple of k*k = %d" % (C2, k * k))
+    Cin = C2 // (k * k)
+    ops._check_out("dw_ct", dw_ct, (T, Cout, C2), dw_ct.dtype)
+    dt = ops._dtype_code(dw_ct)
+    ops._check_dev(dw_ct)
+    dpsi = torch.empty(k, k, T, Cout, Cin, dtype=dw_ct.dtype, device=dw_ct.device)
+    _lib.check(_lib.eqlinear_gconv_unpack_weight(ops._ptr(dw_ct), ops._ptr(dpsi), T, Cin, Cout, k, dt,
+                                                 ops._stream(stream)), "eqlinear_gconv_unpack_weight")
+    return dpsi
+
+
+# C_T weights and spectrum per psi, reused while psi's storage and version
+# counter (bumped by in-place updates) and the stream are unchanged.
+_CACHE: dict = {}
+
+
+def cached_ct_weight(psi: torch.Tensor):
+    stream = torch.cuda.current_stream(psi.device).cuda_stream
+    key = (psi.data_ptr(), psi._version, tuple(psi.shape), psi.dtype, stream)
+    ent = _CACHE.get(id(psi))
+    if ent is not None and ent[0]() is psi and ent[1] == key:
+        return ent[2]
+    w_ct = pack_weight(psi)
+    val = (w_ct, ops.weight_spectrum(w_ct))
+    pid = id(psi)
+    _CACHE[pid] = (weakref.ref(psi, lambda _r, pid=pid: _CACHE.pop(pid, None)), key, val)
+    return val
+
+
+class GroupConv2dFunction(torch.autograd.Function):
+    """Autograd: f [B, H, W, Cin, T], psi [k, k, T, Cout, Cin], b [Cout] or None."""
+
+    @staticmethod
+    def forward(ctx, f, psi, b):
+        ops._check_same_dtype(f, psi=psi, b=b)
+        k, _, T, Cout, Cin = psi.shape
+        B, H, W = _dims(f, Cin, T)
+        _, wspec = cached_ct_weight(psi)
+        xcol = gather(f, T, k)
+        y = ops.forward(xcol, wspec, b, T, k * k * Cin, Cout)
+        ctx.save_for_backward(xcol)
+        ctx.wspec, ctx.dims, ctx.has_bias = wspec, (B, H, W, T, Cin, Cout, k), b is not None
+        return y.view(B, H, W, Cout, T)
+
+    @staticmethod
+    def backward(ctx, gy):
+        (xcol,) = ctx.saved_tensors
+        B, H, W, T, Cin, Cout, k = ctx.dims
+        C2 = k * k * Cin
+        gy2 = gy.contiguous().view(B * H * W, Cout, T)
+        gf = gpsi = gb = None
+        want_w = ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2])
+        dx2 = dw2 = None
+        if ctx.needs_input_grad[0] and want_w:
+            dx2, dw2, gb = ops.backward(xcol, gy2, ctx.wspec, T, C2, Cout, with_bias=ctx.has_bias)
+        elif ctx.needs_input_grad[0]:
+            dx2 = ops.backward_input(gy2, ctx.wspec, T, C2, Cout)
+        elif want_w:
+            dw2, gb = ops.backward_weight(xcol, gy2, T, C2, Cout, with_bias=ctx.has_bias)
+        if dx2 is not None:
+            gf = scatter(dx2, B, H, W, T, Cin, k)
+        if dw2 is not None:
+            gpsi = unpack_weight_grad(dw2, k)
+        return gf, gpsi, gb
+
+
+class GroupConv2d(torch.nn.Module):
+    """Rotation-equivariant k x k group convolution: [B, H, W, Cin, T] -> [B, H, W, Cout, T]."""
+
+    def __init__(self, T: int, Cin: int, Cout: int, k: int = 3, bias: bool = True, device=None, dtype=None):
+        super().__init__()
+        self.T, self.Cin, self.Cout, self.k = T, Cin, Cout, k
+        kw = {"device": device, "dtype": dtype}
+        self.weight = torch.nn.Parameter(torch.randn(k, k, T, Cout, Cin, **kw) / (k * k * T * Cin) ** 0.5)
+        self.bias = torch.nn.Parameter(torch.zeros(Cout, **kw)) if bias else None
+
+    def forward(self, f):
+        return GroupConv2dFunction.apply(f, self.weight, self.bias)

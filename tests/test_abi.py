@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 14, names
+    assert len(names) == 18, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -262,3 +262,46 @@ def test_dihedral_argument_checks(lib):
         assert f(A, None, A + 16 * MB, None, T, Cin, Cout, L.EQL_F32, None) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE) \
             if not _gpu_visible() else True
         assert nout > 0
+
+
+def test_gconv_argument_checks(lib):
+    """The group-convolution gather, scatter and weight permutations check the
+    group order, kernel size, extents, alignment and overlap before any HIP
+    call."""
+    g, sc = L.eqlinear_gconv_gather, L.eqlinear_gconv_scatter
+    pk, up = L.eqlinear_gconv_pack_weight, L.eqlinear_gconv_unpack_weight
+    B, H, W, T, Cin, Cout, k = 2, 8, 8, 4, 6, 10, 3
+    for f in (g, sc):
+        base = [A, A + 64 * MB, B, H, W, T, Cin, k, L.EQL_F32, None]
+
+        def call(i, v, f=f):
+            args = list(base)
+            args[i] = v
+            return f(*args)
+        assert call(5, 3) == L.EQL_ERR_UNSUPPORTED          # T not in {1, 2, 4}
+        assert call(7, 4) == L.EQL_ERR_UNSUPPORTED          # even kernel
+        assert call(7, 9) == L.EQL_ERR_UNSUPPORTED          # kernel above 7
+        assert call(7, 0) == L.EQL_ERR_INVALID_ARG
+        assert call(6, 0) == L.EQL_ERR_INVALID_ARG
+        assert call(6, 8000) == L.EQL_ERR_UNSUPPORTED       # k*k*Cin over 65536
+        assert call(2, -1) == L.EQL_ERR_INVALID_ARG
+        assert call(8, 5) == L.EQL_ERR_INVALID_ARG
+        assert call(0, None) == L.EQL_ERR_INVALID_ARG
+        assert call(1, None) == L.EQL_ERR_INVALID_ARG
+        assert call(0, A + 2) == L.EQL_ERR_ALIGNMENT
+        assert call(1, A + 64) == L.EQL_ERR_INVALID_ARG     # output overlaps input
+        if not _gpu_visible():
+            assert call(2, 0) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)   # empty image: no-op
+    for f in (pk, up):
+        base = [A, A + 64 * MB, T, Cin, Cout, k, L.EQL_F16, None]
+
+        def call(i, v, f=f):
+            args = list(base)
+            args[i] = v
+            return f(*args)
+        assert call(2, 8) == L.EQL_ERR_UNSUPPORTED
+        assert call(5, 2) == L.EQL_ERR_UNSUPPORTED
+        assert call(4, 0) == L.EQL_ERR_INVALID_ARG
+        assert call(0, None) == L.EQL_ERR_INVALID_ARG
+        assert call(1, A + 2) == L.EQL_ERR_INVALID_ARG      # overlap
+        assert call(0, A + 1) == L.EQL_ERR_ALIGNMENT
