@@ -64,6 +64,9 @@ def parse():
                     help="only time the layer over the dihedral group D_T (rotations and "
                          "reflections, Sec. 5) on the C_T kernels against the naive dense layer; "
                          "one JSON line per (shape, dtype)")
+    ap.add_argument("--gconv", action="store_true",
+                    help="only time the rotation-equivariant group convolution (Sec. 5) on the C_T "
+                         "kernels against the naive dense convolution; one JSON line per (shape, dtype)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MiB",
                     help="only run a plain device copy of this many MiB, 5 times (reference "
                          "kernel for scaling rocprofv3 FETCH_SIZE / WRITE_SIZE to bytes)")
@@ -626,6 +629,101 @@ def run_dihedral(args):
             del x, W, b, gy, xg, Wg, bg, xn, Wn, bn, M, w_ct, wspec, x2, y2
 
 
+GCONV_LAYERS = [("p4_c24_56px", 4, 24, 24, 3, 32, 56), ("p4_c64_28px", 4, 64, 64, 3, 32, 28)]
+
+
+def run_gconv(args):
+    """The rotation-equivariant group convolution (Sec. 5) on the C_T kernels
+    (patch gather, C_T layer with k*k*Cin input channels, and for training the
+    gradient scatter and weight permutation) against the naive dense form: the
+    [Cout*T, Cin*T, k, k] kernel Wd[(o,r),(c,s),a,b] = psi[R^-r (a,b)][(s-r) mod T][o][c]
+    applied with torch's conv2d on NCHW features (its autograd folds the
+    gradient back onto psi).  Forward = one layer call with the C_T weight and
+    spectrum precomputed (a frozen weight); training step = weight permutation,
+    spectrum, forward, backward.  Mean and median of ``--tables-runs`` runs."""
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+
+    from paper_2607_21271_amd import gconv, ops
+    runs = args.tables_runs
+    for name, T, Cin, Cout, k, B, H in GCONV_LAYERS:
+        h = k // 2
+        # index of psi used by the dense kernel entry (r, s, a, b): offset R^-r (a, b), lag (s - r)
+        def rot(n, a, b):
+            for _ in range(((n % T) + T) % T * (4 // T if T > 1 else 0)):
+                a, b = -b, a
+            return a, b
+        idx = np.zeros((T, T, k, k), np.int64)
+        for r in range(T):
+            for s_ in range(T):
+                for a in range(-h, h + 1):
+                    for b in range(-h, h + 1):
+                        ra, rb = rot(-r, a, b)
+                        idx[r, s_, a + h, b + h] = ((ra + h) * k + (rb + h)) * T + (s_ - r) % T
+        idx_t = torch.from_numpy(idx).cuda()
+        for dt in ("f32", "f16"):
+            tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+            torch.cuda.empty_cache()
+            print("gconv: %s %s" % (name, dt), file=sys.stderr, flush=True)
+            rs = np.random.RandomState(8300 + Cin)
+            f = torch.from_numpy(rs.standard_normal((B, H, H, Cin, T))).to("cuda", tdt)
+            psi = torch.from_numpy(rs.standard_normal((k, k, T, Cout, Cin)) /
+                                   np.sqrt(k * k * T * Cin)).to("cuda", tdt)
+            bias = torch.from_numpy(0.1 * rs.standard_normal(Cout)).to("cuda", tdt)
+            gy = torch.from_numpy(rs.standard_normal((B, H, H, Cout, T))).to("cuda", tdt)
+            rec = {"table": "gconv", "layer": name, "T": T, "Cin": Cin, "Cout": Cout, "k": k,
+                   "image": [B, H, H], "dtype": dt, "runs": runs,
+                   "ct_layer": "T=%d %d->%d over %d rows" % (T, k * k * Cin, Cout, B * H * H)}
+            w_ct = gconv.pack_weight(psi)
+            wspec = ops.weight_spectrum(w_ct)
+
+            def flash_fwd():
+                xcol = gconv.gather(f, T, k)
+                return ops.forward(xcol, wspec, bias, T, k * k * Cin, Cout)
+            rec["flash_fwd"] = _time_fn(flash_fwd, runs)
+            xcol = gconv.gather(f, T, k)
+            rec["gather"] = _time_fn(lambda: gconv.gather(f, T, k), runs)
+            rec["ct_forward"] = _time_fn(lambda: ops.forward(xcol, wspec, bias, T, k * k * Cin, Cout), runs)
+            rec["scatter"] = _time_fn(lambda: gconv.scatter(xcol, B, H, H, T, Cin, k), runs)
+            del xcol
+            fg = f.clone().requires_grad_(True)
+            pg = psi.clone().requires_grad_(True)
+            bg = bias.clone().requires_grad_(True)
+
+            def flash_train():
+                gconv._CACHE.clear()
+                y = gconv.GroupConv2dFunction.apply(fg, pg, bg)
+                y.backward(gy)
+            rec["flash_train"] = _time_fn(flash_train, runs)
+
+            def dense(p):
+                flat = p.reshape(k * k * T, Cout, Cin)           # [(a, b, lag), o, c]
+                g = flat[idx_t]                                   # [r, s, a, b, o, c]
+                return g.permute(4, 0, 5, 1, 2, 3).reshape(Cout * T, Cin * T, k, k)
+            xn = f.permute(0, 3, 4, 1, 2).reshape(B, Cin * T, H, H).contiguous()
+            gyn = gy.permute(0, 3, 4, 1, 2).reshape(B, Cout * T, H, H).contiguous()
+            Wd = dense(psi)
+            bd = bias.repeat_interleave(T)
+            rec["naive_fwd"] = _time_fn(lambda: F.conv2d(xn, Wd, bd, padding=h), runs)
+            xr = xn.clone().requires_grad_(True)
+            pr = psi.clone().requires_grad_(True)
+            br = bias.clone().requires_grad_(True)
+
+            def naive_train():
+                y = F.conv2d(xr, dense(pr), br.repeat_interleave(T), padding=h)
+                y.backward(gyn)
+            rec["naive_train"] = _time_fn(naive_train, runs)
+            with torch.no_grad():
+                yf = flash_fwd().view(B, H, H, Cout, T).permute(0, 3, 4, 1, 2).reshape(B, Cout * T, H, H).float()
+                yn = F.conv2d(xn, Wd, bd, padding=h).float()
+                rec["flash_vs_naive_rel_err"] = float((yf - yn).abs().max() / yn.abs().max())
+            rec["fwd_speedup"] = round(rec["naive_fwd"]["mean_ms"] / rec["flash_fwd"]["mean_ms"], 2)
+            rec["train_speedup"] = round(rec["naive_train"]["mean_ms"] / rec["flash_train"]["mean_ms"], 2)
+            print(json.dumps(rec), flush=True)
+            del f, psi, bias, gy, fg, pg, bg, xn, gyn, Wd, xr, pr, br, w_ct, wspec
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -649,6 +747,9 @@ def main():
         return
     if args.dihedral:
         run_dihedral(args)
+        return
+    if args.gconv:
+        run_gconv(args)
         return
     digest = source_digest()
     name = args.workload or synth.HEADLINE

@@ -711,30 +711,52 @@ int gconv_image(int64_t B, int H, int W) {
   return EQL_OK;
 }
 
+template <typename E, int T, int K>
+void gconv_pixels(bool scatter, const void* in, void* out, int64_t n_pix, int H, int W, int Cin, hipStream_t s) {
+  // one wave per pixel, kGconvWaves pixels per block; past 2^30 blocks the
+  // kernels stride over the pixel groups
+  const int64_t groups = (n_pix + eqk::kGconvWaves - 1) / eqk::kGconvWaves;
+  const dim3 grid((unsigned)(groups < ((int64_t)1 << 30) ? groups : ((int64_t)1 << 30)));
+  if (scatter)
+    hipLaunchKernelGGL((eqk::eql_gconv_scatter_kernel<E, T, K>), grid, dim3(256), 0, s, (const E*)in, (E*)out,
+                       n_pix, H, W, Cin);
+  else if ((uintptr_t)out % (sizeof(E) * T) == 0)
+    hipLaunchKernelGGL((eqk::eql_gconv_gather_kernel<E, T, K, true>), grid, dim3(256), 0, s, (const E*)in,
+                       (E*)out, n_pix, H, W, Cin);
+  else
+    hipLaunchKernelGGL((eqk::eql_gconv_gather_kernel<E, T, K, false>), grid, dim3(256), 0, s, (const E*)in,
+                       (E*)out, n_pix, H, W, Cin);
+}
+
+template <typename E, int T>
+int gconv_launch_t(int op, const void* in, void* out, int64_t B, int H, int W, int Cin, int Cout, int k,
+                   hipStream_t s) {
+  const int64_t n_pix = B * H * W;
+  if (op < 2) {
+    if (n_pix == 0) return EQL_OK;
+    const bool sc = op == 1;
+    if (k == 1) gconv_pixels<E, T, 1>(sc, in, out, n_pix, H, W, Cin, s);
+    else if (k == 3) gconv_pixels<E, T, 3>(sc, in, out, n_pix, H, W, Cin, s);
+    else if (k == 5) gconv_pixels<E, T, 5>(sc, in, out, n_pix, H, W, Cin, s);
+    else gconv_pixels<E, T, 7>(sc, in, out, n_pix, H, W, Cin, s);  // gconv_shape admits odd k <= 7
+  } else {
+    const int64_t total = (int64_t)T * Cout * k * k * Cin;
+    if (op == 2)
+      hipLaunchKernelGGL((eqk::eql_gconv_pack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                         (const E*)in, (E*)out, T, Cin, Cout, k);
+    else
+      hipLaunchKernelGGL((eqk::eql_gconv_unpack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
+                         (const E*)in, (E*)out, T, Cin, Cout, k);
+  }
+  return launched(hipGetLastError());
+}
+
 template <typename E>
 int gconv_launch(int op, const void* in, void* out, int64_t B, int H, int W, int T, int Cin, int Cout, int k,
                  hipStream_t s) {
-  const int64_t n_pix = B * H * W;
-  if (op == 0) {
-    const int64_t total = n_pix * k * k * Cin * T;
-    if (total == 0) return EQL_OK;
-    hipLaunchKernelGGL((eqk::eql_gconv_gather_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
-                       (const E*)in, (E*)out, B, H, W, T, Cin, k);
-  } else if (op == 1) {
-    const int64_t total = n_pix * Cin * T;
-    if (total == 0) return EQL_OK;
-    hipLaunchKernelGGL((eqk::eql_gconv_scatter_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
-                       (const E*)in, (E*)out, B, H, W, T, Cin, k);
-  } else if (op == 2) {
-    const int64_t total = (int64_t)T * Cout * k * k * Cin;
-    hipLaunchKernelGGL((eqk::eql_gconv_pack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
-                       (const E*)in, (E*)out, T, Cin, Cout, k);
-  } else {
-    const int64_t total = (int64_t)T * Cout * k * k * Cin;
-    hipLaunchKernelGGL((eqk::eql_gconv_unpack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
-                       (const E*)in, (E*)out, T, Cin, Cout, k);
-  }
-  return launched(hipGetLastError());
+  if (T == 4) return gconv_launch_t<E, 4>(op, in, out, B, H, W, Cin, Cout, k, s);
+  if (T == 2) return gconv_launch_t<E, 2>(op, in, out, B, H, W, Cin, Cout, k, s);
+  return gconv_launch_t<E, 1>(op, in, out, B, H, W, Cin, Cout, k, s);
 }
 
 // op 0 gather (in f, out X), 1 scatter (in dX, out df), 2 pack (in psi, out w),

@@ -28,8 +28,8 @@
 //
 // Layouts: f, df [N = B*H*W pixels, Cin, T]; X, dX [N, k*k*Cin, T];
 // psi, dpsi [k, k, T, Cout, Cin] at (a + k/2, b + k/2, lag); w, dw
-// [T, Cout, k*k*Cin].  Every kernel is a grid-stride gather (each output
-// element written once, no atomics).
+// [T, Cout, k*k*Cin].  Every kernel gathers (each output element written
+// once, no atomics).
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -112,76 +112,129 @@ __device__ __forceinline__ void gconv_orbit_of(const GconvDims& d, int a, int b,
   }
 }
 
-// X[n][c'][j] from f (zero outside the image)
-template <typename E>
-__global__ __launch_bounds__(256) void eql_gconv_gather_kernel(const E* __restrict__ f, E* __restrict__ X,
-                                                               int64_t B, int H, int W, int T, int Cin,
-                                                               int k) {
-  const GconvDims d = gconv_dims(T, k, Cin);
-  const int64_t total = B * H * W * d.Cin2 * T;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-    const int j = (int)(i % T);
-    const int64_t r = i / T;
-    const int cc = (int)(r % d.Cin2);
-    const int64_t n = r / d.Cin2;
-    const int x = (int)(n % W);
-    const int y = (int)((n / W) % H);
-    const int64_t bimg = n / ((int64_t)W * H);
-    int a = 0, b = 0, c, s;
-    const int ob = d.n_orb * Cin * T;
-    if (cc < ob) {
-      const int O = cc / (Cin * T);
-      const int rem = cc - O * Cin * T;
-      c = rem / T;
-      const int u = rem - c * T;
-      gconv_base(d, O, a, b);
+// Gather and scatter run one wave per output pixel, T and k fixed at compile
+// time: the channel split (c, u) = (q / T, q % T) is shifts, the orbit loops
+// unroll and their offsets fold to constants; the pixel is wave-uniform.  Blocks are ordered so that
+// each XCD (blocks dealt round-robin over the 8 of them) takes one contiguous
+// run of pixels: neighbouring pixels, which read the same halo rows, then
+// share that XCD's L2.
+constexpr int kGconvWaves = 4;  // waves (pixels) per 256-thread block
+
+__device__ __forceinline__ int64_t gconv_xcd_block(int64_t bid, int64_t G) {
+  const int64_t q = G / 8, r = G % 8, xcd = bid % 8, idx = bid / 8;
+  return xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+}
+
+template <typename E, int T>
+struct alignas(sizeof(E) * T) GconvVec {
+  E v[T];
+};
+
+// X[p][c'][j] for one pixel p per wave: orbit blocks X[p][O*Cin*T + c*T + u][j]
+// = f[p + R^j d0_O][c][(u + j) mod T] (zero outside the image), one vector of
+// T entries per lane and channel; then the centre block, a copy of f[p].  VEC:
+// X is aligned to T elements, so each lane stores its T entries at once.
+template <typename E, int T, int K, bool VEC>
+__device__ __forceinline__ void gconv_gather_pixel(const E* __restrict__ f, E* __restrict__ X, int64_t p, int H,
+                                                   int W, int Cin, const GconvDims& d) {
+  const int lane = threadIdx.x & 63;
+  const int CT = Cin * T;
+  const int x = (int)(p % W);
+  const int64_t ny = p / W;
+  const int y = (int)(ny % H);
+  const int64_t img = (ny / H) * H * W;  // first pixel of p's image
+  E* const row = X + p * d.Cin2 * T;
+#pragma unroll
+  for (int O = 0; O < (K * K - 1) / T; ++O) {
+    int a0, b0;
+    gconv_base(d, O, a0, b0);
+    int64_t src[T];
+    bool ok[T];
+#pragma unroll
+    for (int j = 0; j < T; ++j) {
+      int a = a0, b = b0;
       gconv_rot(j, T, a, b);
-      s = (u + j) % T;
-    } else {
-      c = cc - ob;
-      s = j;
+      const int yy = y + a, xx = x + b;
+      ok[j] = yy >= 0 && yy < H && xx >= 0 && xx < W;
+      src[j] = ok[j] ? (img + (int64_t)yy * W + xx) * CT : 0;
     }
-    const int yy = y + a, xx = x + b;
-    E v = (E)0.0f;
-    if (yy >= 0 && yy < H && xx >= 0 && xx < W)
-      v = f[(((bimg * H + yy) * W + xx) * Cin + c) * T + s];
-    X[i] = v;
+    E* const dst = row + (int64_t)O * CT * T;
+    for (int q = lane; q < CT; q += 64) {
+      const int c = q / T, u = q % T;
+      GconvVec<E, T> v;
+#pragma unroll
+      for (int j = 0; j < T; ++j) v.v[j] = ok[j] ? f[src[j] + c * T + (u + j) % T] : (E)0.0f;
+      if constexpr (VEC) {
+        *reinterpret_cast<GconvVec<E, T>*>(dst + (int64_t)q * T) = v;
+      } else {
+#pragma unroll
+        for (int j = 0; j < T; ++j) dst[(int64_t)q * T + j] = v.v[j];
+      }
+    }
+  }
+  const E* const fs = f + p * CT;
+  E* const dc = row + (int64_t)d.n_orb * CT * T;
+  for (int q = lane; q < CT; q += 64) dc[q] = fs[q];
+}
+
+// pixel groups of kGconvWaves pixels, one per block, block-strided when the
+// grid is capped
+template <typename E, int T, int K, bool VEC>
+__global__ __launch_bounds__(256) void eql_gconv_gather_kernel(const E* __restrict__ f, E* __restrict__ X,
+                                                               int64_t n_pix, int H, int W, int Cin) {
+  const GconvDims d = gconv_dims(T, K, Cin);
+  for (int64_t g = gconv_xcd_block(blockIdx.x, gridDim.x); g * kGconvWaves < n_pix; g += gridDim.x) {
+    const int64_t p = g * kGconvWaves + (threadIdx.x >> 6);
+    if (p < n_pix) gconv_gather_pixel<E, T, K, VEC>(f, X, p, H, W, Cin, d);
   }
 }
 
-// df[n][c][s] = sum over the entries of X that read f[n][c][s] of dX (the
-// adjoint of the gather), summed in fp32 in a fixed order
-template <typename E>
-__global__ __launch_bounds__(256) void eql_gconv_scatter_kernel(const E* __restrict__ dX, E* __restrict__ df,
-                                                                int64_t B, int H, int W, int T, int Cin,
-                                                                int k) {
-  const GconvDims d = gconv_dims(T, k, Cin);
-  const int64_t total = B * H * W * Cin * T;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int ob = d.n_orb * Cin * T;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-    const int s = (int)(i % T);
-    const int64_t r = i / T;
-    const int c = (int)(r % Cin);
-    const int64_t n = r / Cin;
-    const int x = (int)(n % W);
-    const int y = (int)((n / W) % H);
-    const int64_t bimg = n / ((int64_t)W * H);
-    float acc = (float)dX[(n * d.Cin2 + ob + c) * T + s];  // centre
-    for (int O = 0; O < d.n_orb; ++O) {
+// df[p][c][s] = sum of the entries of dX that the gather filled from
+// f[p][c][s] (its adjoint): the centre entry, then for each orbit O and turn j
+// the entry of the pixel p - R^j d0_O at channel (O, c, (s - j) mod T), group
+// index j; summed in fp32 in that fixed order.  One wave per pixel p.  Every
+// load is issued (an entry outside the image reads p's own row and adds
+// zero), so the loads of all orbits are in flight together.
+template <typename E, int T, int K>
+__device__ __forceinline__ void gconv_scatter_pixel(const E* __restrict__ dX, E* __restrict__ df, int64_t p,
+                                                    int H, int W, int Cin, const GconvDims& d) {
+  const int lane = threadIdx.x & 63;
+  const int CT = Cin * T;
+  const int64_t rowlen = (int64_t)d.Cin2 * T;
+  const int x = (int)(p % W);
+  const int64_t ny = p / W;
+  const int y = (int)(ny % H);
+  const int64_t img = (ny / H) * H * W;
+  for (int q = lane; q < CT; q += 64) {
+    const int c = q / T, s = q % T;
+    float acc = (float)dX[p * rowlen + (int64_t)d.n_orb * CT * T + q];  // centre
+#pragma unroll
+    for (int O = 0; O < (K * K - 1) / T; ++O) {
+      int a0, b0;
+      gconv_base(d, O, a0, b0);
+#pragma unroll
       for (int j = 0; j < T; ++j) {
-        int a, b;
-        gconv_base(d, O, a, b);
+        int a = a0, b = b0;
         gconv_rot(j, T, a, b);
-        const int ys = y - a, xs = x - b;  // the pixel whose row read (y, x) at this entry
-        if (ys < 0 || ys >= H || xs < 0 || xs >= W) continue;
-        const int u = ((s - j) % T + T) % T;
-        const int64_t ns = (bimg * H + ys) * W + xs;
-        acc += (float)dX[(ns * d.Cin2 + O * Cin * T + c * T + u) * T + j];
+        const int ys = y - a, xs = x - b;  // the pixel whose row read p at this entry
+        const bool ok = ys >= 0 && ys < H && xs >= 0 && xs < W;
+        const int64_t ps = ok ? img + (int64_t)ys * W + xs : p;
+        const int u = (s - j + T) % T;
+        const float v = (float)dX[ps * rowlen + (int64_t)O * CT * T + (c * T + u) * T + j];
+        acc += ok ? v : 0.0f;
       }
     }
-    df[i] = (E)acc;
+    df[p * CT + q] = (E)acc;
+  }
+}
+
+template <typename E, int T, int K>
+__global__ __launch_bounds__(256) void eql_gconv_scatter_kernel(const E* __restrict__ dX, E* __restrict__ df,
+                                                                int64_t n_pix, int H, int W, int Cin) {
+  const GconvDims d = gconv_dims(T, K, Cin);
+  for (int64_t g = gconv_xcd_block(blockIdx.x, gridDim.x); g * kGconvWaves < n_pix; g += gridDim.x) {
+    const int64_t p = g * kGconvWaves + (threadIdx.x >> 6);
+    if (p < n_pix) gconv_scatter_pixel<E, T, K>(dX, df, p, H, W, Cin, d);
   }
 }
 
