@@ -164,12 +164,16 @@ class Workload:
             fn(torch.cuda.current_stream())
         return g
 
-    def run_graph(self, steps, warmup):
+    def run_graph(self, steps, warmup, block=10):
         """Whole-step time with each input set's step (the same launches as the
         eager path) captured once in a HIP graph and replayed.  Exactly
-        ``steps`` steps are timed, bracketed by device synchronisation (their
-        mean is the reported step time); HIP events around every replay, on
-        the stream the replays run on, give the per-step distribution."""
+        ``steps`` steps are timed, bracketed by device synchronisation and by
+        HIP events on the replay stream at their two ends only (an event
+        recorded between replays costs the GPU about 11 us at the headline, so
+        none sits inside the timed run); their mean is the reported step time.
+        A second run of ``steps`` replays with an event after every ``block``
+        replays gives the distribution of block means (the event cost spread
+        over ``block`` steps)."""
         import torch
         graphs = [self._graph(lambda st, r=r: self.step(r, stream=st))
                   for r in range(len(self.sets))]
@@ -177,23 +181,34 @@ class Workload:
             graphs[i % len(graphs)].replay()
         torch.cuda.synchronize()
         st = torch.cuda.current_stream()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
-        ev[0].record(st)
+        e0.record(st)
         for i in range(steps):
             graphs[(warmup + i) % len(graphs)].replay()
-            ev[i + 1].record(st)
+        e1.record(st)
         torch.cuda.synchronize()
         t1 = time.perf_counter()
-        per = [ev[i].elapsed_time(ev[i + 1]) * 1e3 for i in range(steps)]  # us
+        ev_mean = e0.elapsed_time(e1) * 1e3 / steps  # us
+        block = max(1, min(block, steps))
+        nb = max(1, steps // block)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(nb + 1)]
+        ev[0].record(st)
+        for b in range(nb):
+            for i in range(block):
+                graphs[(b * block + i) % len(graphs)].replay()
+            ev[b + 1].record(st)
+        torch.cuda.synchronize()
+        per = [ev[b].elapsed_time(ev[b + 1]) * 1e3 / block for b in range(nb)]  # us per step
         del graphs
-        return (t1 - t0) / steps, per
+        return (t1 - t0) / steps, ev_mean, per
 
-    def run_passes(self, reps):
+    def run_passes(self, reps, settle_s=0.05):
         """Average duration of one launch of each entry point: per pass, one HIP
         graph holds one call per input set back to back (no host time between
-        the launches) and is replayed until ``reps`` calls have run; HIP
-        events on the replay stream bracket all of them."""
+        the launches) and is replayed until ``reps`` calls have run (after
+        untimed replays for at least ``settle_s`` seconds); HIP events on the
+        replay stream bracket all of them."""
         import torch
         l, ops = self.layer, self.ops
         R = len(self.sets)
@@ -218,8 +233,15 @@ class Workload:
         for kind in ("wspec", "fwd", "bwd", "dx", "dw"):
             g = self._graph(lambda st: [launch(kind, r, st) for r in range(R)])
             n = max(1, reps // R)
-            g.replay()
-            torch.cuda.synchronize()
+            # untimed replays of the same launches for at least settle_s, so
+            # the GPU clocks have left their idle state when timing starts
+            t_end = time.perf_counter() + settle_s
+            while True:
+                for _ in range(n):
+                    g.replay()
+                torch.cuda.synchronize()
+                if time.perf_counter() >= t_end:
+                    break
             st = torch.cuda.current_stream()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(st)
@@ -307,10 +329,12 @@ def measure(layer, dt, args, digest, with_cpu):
     from paper_2607_21271_amd import roofline as rf
     l = layer
     wl = Workload(l, dt, max(1, args.rotate))
-    # the step: HIP-graph replays of whole steps (reported step time and its
-    # distribution); the passes: back-to-back launches of each entry point
-    sec, per_step = wl.run_graph(args.steps, args.warmup)
+    # the passes: back-to-back launches of each entry point (run first, which
+    # also brings the GPU out of its idle clocks before the timed steps); the
+    # step: HIP-graph replays of whole steps (reported step time and its
+    # distribution)
     per = wl.run_passes(max(args.steps, 4 * max(1, args.rotate)))
+    sec, ev_mean_us, per_step = wl.run_graph(args.steps, args.warmup)
     N = l.N
     flops = 3 * rf.pass_flops(N, l.T, l.Cin, l.Cout)
     dense = 3 * rf.dense_equiv_flops(N, l.T, l.Cin, l.Cout)
@@ -348,15 +372,18 @@ def measure(layer, dt, args, digest, with_cpu):
         "mfma_util_pct": round(100 * flops / sec / (rf.PEAK_MFMA_TFLOPS[dt] * 1e12), 2),
         "tflops_actual": round(flops / sec / 1e12, 2),
         "tflops_dense_equiv": round(dense / sec / 1e12, 2),
-        "step_us": {"mean": round(sec * 1e6, 2), "median": round(_pct(per_step, 50), 2),
-                    "p10": round(_pct(per_step, 10), 2), "p90": round(_pct(per_step, 90), 2)},
+        "step_us": {"mean": round(sec * 1e6, 2), "event_mean": round(ev_mean_us, 2),
+                    "median": round(_pct(per_step, 50), 2),
+                    "p10": round(_pct(per_step, 10), 2), "p90": round(_pct(per_step, 90), 2),
+                    "distribution": "means of %d-step blocks" % max(1, min(10, args.steps))},
         "backward": "single pass (eqlinear_backward: eql_bwd_fused_kernel + reduction)" if wl.fused
                     else "two passes (eqlinear_backward: input-gradient kernel, then weight-gradient "
                          "kernel + reduction)",
         "timing": "step = one replay of a HIP graph holding one input set's launches (weight "
                   "spectrum, forward, whole backward); ms_per_step is the mean "
-                  "over the timed replays (host clock around all of them), step_us its "
-                  "distribution from HIP events around each replay; pass_us = average launch "
+                  "over the timed replays (host clock around all of them, HIP events only at "
+                  "their two ends: event_mean), step_us median/p10/p90 the distribution of "
+                  "10-step block means from a second run; pass_us = average launch "
                   "of each entry point, timed with HIP events around graph replays of "
                   "back-to-back launches on the replay stream",
         "pass_us": {k: round(v, 2) for k, v in per.items()},
