@@ -18,7 +18,8 @@
  * axis: w[j] = W_paper[(T - j) mod T].
  *
  * Common rules for every entry point:
- *   - dtype is EQL_F32 or EQL_F16 and applies to every tensor of the call.
+ *   - dtype is EQL_F32, EQL_F16 or EQL_BF16 and applies to every tensor of
+ *     the call.
  *     EQL_F32: every transform, product and accumulation is fp32.
  *     EQL_F16 (IEEE binary16): the forward real DFTs of the activations x and
  *     of the output gradients dy run in packed fp16 arithmetic (two signals per
@@ -27,6 +28,12 @@
  *     transforms and the bias are fp32.  db sums each pair of rows' fp16 bin 0
  *     into fp32.  A transform partial sum above 65504 in magnitude overflows
  *     to +-inf, so |x| and |dy| must stay below about 65504 / T.
+ *     EQL_BF16 (bfloat16: fp32's exponent range, 8 significand bits): the
+ *     forward real DFTs run in fp32 on the exactly widened inputs and each
+ *     spectrum value is rounded once to bf16 as an MFMA operand; the weight
+ *     spectrum, accumulation, inverse transforms and bias (db from the fp32
+ *     bin 0) are fp32.  eqlinear_backward always takes the two passes for
+ *     bf16.
  *     Each output is rounded once (round-to-nearest-even).
  *   - All pointers are device pointers owned by the caller.  The library never
  *     allocates, frees or synchronises; work is enqueued on `stream` (a
@@ -60,10 +67,10 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 5
+#define EQLINEAR_ABI_VERSION 6
 #define EQLINEAR_MAX_T 16
 
-typedef enum { EQL_F32 = 0, EQL_F16 = 1 } eql_dtype_t;
+typedef enum { EQL_F32 = 0, EQL_F16 = 1, EQL_BF16 = 2 } eql_dtype_t;
 
 typedef enum {
   EQL_OK = 0,
@@ -99,8 +106,8 @@ size_t eqlinear_weight_spectrum_bytes(int T, int Cin, int Cout, int dtype);
  * paper's kernels keep their weights in (Sec. 3.5).  w is [T,Cout,Cin] in
  * `dtype`; wspec is an opaque device buffer of
  * eqlinear_weight_spectrum_bytes() bytes, fully overwritten (padding
- * included).  For EQL_F16 the spectrum is computed in fp32 and rounded once to
- * fp16.  It stays valid until w changes and serves eqlinear_forward and
+ * included).  For EQL_F16 and EQL_BF16 the spectrum is computed in fp32 and
+ * rounded once to the 16-bit type.  It stays valid until w changes and serves eqlinear_forward and
  * eqlinear_backward_input of the same (T, Cin, Cout, dtype). */
 int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cout, int dtype,
                              void* stream);

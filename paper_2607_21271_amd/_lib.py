@@ -15,6 +15,7 @@ LIB_PATH = os.path.join(HERE, "libeqlinear.so")
 
 EQL_F32 = 0
 EQL_F16 = 1
+EQL_BF16 = 2
 
 EQL_OK = 0
 EQL_ERR_INVALID_ARG = 1

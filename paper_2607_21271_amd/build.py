@@ -2,7 +2,7 @@
 
 Each translation unit is compiled in its own hipcc process (in parallel), then
 linked into ``paper_2607_21271_amd/libeqlinear.so``.  The kernel instantiations
-are one object per (group order T, dtype): ``eql_inst.hip`` compiled 32 times.  Always rebuilds.  The
+are one object per (group order T, dtype): ``eql_inst.hip`` compiled 48 times.  Always rebuilds.  The
 device assembly is kept (-save-temps) and scanned by isa_check before the
 library is installed; a finding fails the build.
 Usage: ``python -m paper_2607_21271_amd.build`` or ``build()``.
@@ -24,8 +24,8 @@ HOST_SOURCES = ["eql_api.cpp", "eql_dispatch.cpp"]
 MAX_T = 16
 # (source, object stem, extra defines)
 UNITS = [(s, os.path.splitext(s)[0], []) for s in HOST_SOURCES] + [
-    ("eql_inst.hip", "inst_%s_t%02d" % ("f16" if f16 else "f32", t), ["-DEQK_T=%d" % t, "-DEQK_F16=%d" % f16])
-    for t in range(MAX_T, 0, -1) for f16 in (1, 0)]
+    ("eql_inst.hip", "inst_%s_t%02d" % (name, t), ["-DEQK_T=%d" % t, "-DEQK_DT=%d" % dt])
+    for t in range(MAX_T, 0, -1) for dt, name in ((1, "f16"), (0, "f32"), (2, "bf16"))]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

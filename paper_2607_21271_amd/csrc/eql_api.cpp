@@ -19,7 +19,7 @@ namespace eqk {
 // fp32 partials (written once, read once) at most half the bytes of x and dy,
 // at least two row chunks per split, and each split's rows addressable with
 // 31 bits.  Returns the rows per split (0 when N <= 0) and sets S.
-static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool f16, int KR, int64_t tiles,
+static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool w16, int KR, int64_t tiles,
                             int Cin_pad, int Cout_pad, int& S) {
   if (N <= 0) {
     S = 0;
@@ -28,7 +28,7 @@ static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool f16, int K
   int64_t target = 256;
   if (const char* e = getenv("EQL_WGRAD_TARGET")) target = atoi(e) > 0 ? atoi(e) : 256;
   int64_t s = (target + tiles - 1) / tiles;
-  const double eb = f16 ? 2.0 : 4.0;
+  const double eb = w16 ? 2.0 : 4.0;
   const double in_bytes = (double)N * (Cin + Cout) * T * eb;
   const double part_per_split = (double)T * Cout_pad * Cin_pad * 4.0;
   const int64_t s_budget = (int64_t)(in_bytes / (2.0 * part_per_split));
@@ -55,16 +55,16 @@ static int64_t wgrad_splits(int64_t N, int T, int Cin, int Cout, bool f16, int K
 // L2-to-CU time and the transform (VALU) time of every workgroup loading its
 // rows for its channel tile, and the MFMA time, each spread over the CUs the
 // grid occupies.
-static WgradPlan wgrad_plan_rd(int64_t N, int T, int Cin, int Cout, bool f16) {
+static WgradPlan wgrad_plan_rd(int64_t N, int T, int Cin, int Cout, bool w16) {
   static const int kTiles[][2] = {{1, 1}, {1, 2}, {2, 1}, {2, 2}, {2, 4}, {4, 2}};
   const int cus = 256;
-  const int KR = f16 ? 32 : 16;
-  const double eb = f16 ? 2.0 : 4.0;
+  const int KR = w16 ? 32 : 16;
+  const double eb = w16 ? 2.0 : 4.0;
   const int R = 1 + (T % 2 == 0), K = (T - 1) / 2;
   const double n = (double)(N > 0 ? N : 0);
   // VALU cycles per transformed element (packed fp16: two rows per operation)
   const double log2t = T <= 1 ? 1.0 : (T <= 2 ? 1.0 : (T <= 4 ? 2.0 : (T <= 8 ? 3.0 : 4.0)));
-  const double cyc = (f16 ? 0.05 : 0.10) * (log2t + 1.0);
+  const double cyc = (w16 ? 0.05 : 0.10) * (log2t + 1.0);
   int fc = 0, fo = 0;
   if (const char* e = getenv("EQL_WGRAD_TILE")) {
     if (sscanf(e, "%d,%d", &fc, &fo) != 2) fc = 0;
@@ -89,7 +89,7 @@ static WgradPlan wgrad_plan_rd(int64_t N, int T, int Cin, int Cout, bool f16) {
     const double vals = n * T * ((double)nct * BC * not_ + (double)not_ * BO * nct);
     const double l2 = vals * eb / (busy * 154e9);
     const double valu = vals * cyc / (busy * 4.0 * 2.4e9);
-    const double mfma = 2.0 * (R + 4 * K) * n * (nct * BC) * (not_ * BO) / ((f16 ? 2.5e15 : 1.573e14) * busy / cus);
+    const double mfma = 2.0 * (R + 4 * K) * n * (nct * BC) * (not_ * BO) / ((w16 ? 2.5e15 : 1.573e14) * busy / cus);
     double t = hbm;
     if (l2 > t) t = l2;
     if (valu > t) t = valu;
@@ -123,7 +123,7 @@ static int wgrad_forced_kind() {
   return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
 }
 
-static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16);
+static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16);
 
 // Kernel choice.  The register-direct kernel writes few partials but reads
 // every row once per channel tile and transforms it there; the staged kernel
@@ -136,15 +136,17 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
 // 32768 rows, whole backward: 1.8 vs 2.7 ms at 512 fp32, 28 vs 121 ms at
 // 2048 fp32, 7.6 vs 26.8 ms at 2048 fp16), level at 96 x 384 and 256 x 256,
 // and slower on Swin stage 1 (24 x 96: 120 vs 79 us) and the 64 x 64 sweep.
-WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+// bf16 always takes the staged kernel, whose bias sum reads the fp32 bin 0.
+WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt) {
+  const bool w16 = dt != kF32;  // 16-bit elements: same shapes for fp16 and bf16
   const int forced = wgrad_forced_kind();
   const int lo = Cin < Cout ? Cin : Cout, hi = Cin < Cout ? Cout : Cin;
-  if (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512)))
-    return wgrad_plan_rd(N, T, Cin, Cout, f16);
-  return wgrad_plan_staged(N, T, Cin, Cout, f16);
+  if (dt != kBF16 && (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512))))
+    return wgrad_plan_rd(N, T, Cin, Cout, w16);
+  return wgrad_plan_staged(N, T, Cin, Cout, w16);
 }
 
-static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16) {
+static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16) {
   // Variants (wave grid rows, c-tiles, o-tiles per wave) with at most 96
   // accumulator floats per lane: CT * OTW * T * 4 <= 96.  Pick the one with the
   // smallest estimated time: HBM bytes (x and dy once, the partials written
@@ -161,8 +163,8 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
   if (const char* e = getenv("EQL_WGRAD_VARIANT")) {
     if (sscanf(e, "%d,%d,%d", &fw, &fc, &fo) != 3) fw = 0;
   }
-  const int KR = f16 ? 32 : 16;
-  const double eb = f16 ? 2.0 : 4.0;
+  const int KR = w16 ? 32 : 16;
+  const double eb = w16 ? 2.0 : 4.0;
   const int R = 1 + (T % 2 == 0), K = (T - 1) / 2;
   const double n = (double)(N > 0 ? N : 0);
   for (const auto& v : kVariants) {
@@ -174,12 +176,12 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
     const int nct = (Cin + BC - 1) / BC, not_ = (Cout + BO - 1) / BO;
     const int64_t tiles = (int64_t)nct * not_;
     int S = 0;
-    wgrad_splits(N, T, Cin, Cout, f16, KR, tiles, nct * BC, not_ * BO, S);
+    wgrad_splits(N, T, Cin, Cout, w16, KR, tiles, nct * BC, not_ * BO, S);
     const double part = (double)S * T * (nct * BC) * (not_ * BO) * 4.0;
     const double hbm = n * (Cin + Cout) * T * eb + 2.0 * part;
     const double l2 = n * T * eb * ((double)Cin * not_ + (double)Cout * nct);
     const double flops = 2.0 * (R + 4 * K) * n * (nct * BC) * (not_ * BO);
-    const double mfma_bytes = flops / (f16 ? 2.5e15 : 1.573e14) * 8.0e12;  // as HBM-time bytes
+    const double mfma_bytes = flops / (w16 ? 2.5e15 : 1.573e14) * 8.0e12;  // as HBM-time bytes
     double mem = hbm + 0.25 * l2;
     if (mfma_bytes > mem) mem = mfma_bytes;
     double fill = (double)S * tiles / 256.0;
@@ -193,7 +195,7 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool f16
   p.KR = KR;
   p.Cin_pad = p.n_ct * p.BC;
   p.Cout_pad = p.n_ot * p.BO;
-  p.rows_per_split = wgrad_splits(N, T, Cin, Cout, f16, KR, (int64_t)p.n_ct * p.n_ot, p.Cin_pad,
+  p.rows_per_split = wgrad_splits(N, T, Cin, Cout, w16, KR, (int64_t)p.n_ct * p.n_ot, p.Cin_pad,
                                   p.Cout_pad, p.S);
   p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
   p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
@@ -221,11 +223,12 @@ static int bwd_forced_fused() {
 // stays on the two kernels: its staging does not fit two buffers, and the
 // single-buffered pass measured slower (Swin stage 1 shape 494 against
 // 383 us, the T = 3 and 5 sweeps 50.0 against 47.4 and 79.3 against 75.3 us).
-FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16) {
+FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, int dt) {
   static const int kVariants[][3] = {{2, 1, 1}, {4, 1, 1}, {2, 1, 2}, {2, 2, 1}, {2, 1, 3}};
   FusedPlan p{};
   const int forced = bwd_forced_fused();
-  if (forced == 0 || N <= 0) return p;
+  if (forced == 0 || N <= 0 || dt == kBF16) return p;  // fp32 and fp16 only
+  const bool f16 = dt == kF16;
   const int KR = f16 ? 32 : 16;
   const int C16 = round_up(Cin, 16);
   const int nks = (Cout + KR - 1) / KR;
@@ -275,7 +278,8 @@ namespace {
 constexpr int64_t kMaxN = (int64_t)1 << 36;
 constexpr int kMaxC = 65536;
 
-size_t elem_bytes(int dtype) { return dtype == EQL_F16 ? 2 : 4; }
+size_t elem_bytes(int dtype) { return dtype == EQL_F32 ? 4 : 2; }
+bool valid_dtype(int dtype) { return dtype == EQL_F32 || dtype == EQL_F16 || dtype == EQL_BF16; }
 
 size_t align256(size_t v) { return (v + 255) / 256 * 256; }
 
@@ -301,11 +305,11 @@ bool any_overlap(const Range* r, int n) {
 bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 int check_shape(int64_t N, int T, int Cin, int Cout, int dtype) {
-  if (dtype != EQL_F32 && dtype != EQL_F16) return EQL_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return EQL_ERR_INVALID_ARG;
   if (T < 1 || Cin < 1 || Cout < 1 || N < 0) return EQL_ERR_INVALID_ARG;
   if (T > EQLINEAR_MAX_T || Cin > kMaxC || Cout > kMaxC || N > kMaxN) return EQL_ERR_UNSUPPORTED;
   // the weight spectrum (two padded copies) must stay under 2^31 bytes
-  if ((double)T * 2.0 * (Cin + 127) * (Cout + 127) * (dtype == EQL_F16 ? 2 : 4) >= 2147483648.0)
+  if ((double)T * 2.0 * (Cin + 127) * (Cout + 127) * elem_bytes(dtype) >= 2147483648.0)
     return EQL_ERR_UNSUPPORTED;
   return EQL_OK;
 }
@@ -382,7 +386,7 @@ const char* eqlinear_status_string(int status) {
 
 size_t eqlinear_weight_spectrum_bytes(int T, int Cin, int Cout, int dtype) {
   if (check_shape(0, T, Cin, Cout, dtype) != EQL_OK) return 0;
-  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype == EQL_F16);
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype != EQL_F32);
   const size_t bytes =
       (size_t)T * ((size_t)d.CoF * d.CiF + (size_t)d.CinB * d.CoutB) * elem_bytes(dtype);
   return bytes < ((size_t)1 << 31) ? bytes : 0;  // kernels address the spectrum with 31-bit offsets
@@ -400,7 +404,7 @@ int eqlinear_weight_spectrum(const void* w, void* wspec, int T, int Cin, int Cou
   if (any_overlap(r, 2)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   hipStream_t s = (hipStream_t)stream;
-  return launched(eqk::launch_wspec(dtype == EQL_F16, T, w, wspec, Cin, Cout, s));
+  return launched(eqk::launch_wspec(dtype, T, w, wspec, Cin, Cout, s));
 }
 
 static int gemm_common(const void* in, const void* wspec, const void* bias, void* out, int64_t N,
@@ -422,7 +426,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   if (N == 0) return EQL_OK;
-  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype == EQL_F16);
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype != EQL_F32);
   eqk::GemmArgs a{};
   a.in = in;
   a.bias = bias;
@@ -431,8 +435,8 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   a.Ci = Ci;
   a.Co = Co;
   a.stream = (hipStream_t)stream;
-  a.plan = eqk::gemm_plan(T, Ci, Co, dtype == EQL_F16);
-  eqk::gemm_plan_rows(a.plan, N, T, dtype == EQL_F16, eqk::device_cu_count());
+  a.plan = eqk::gemm_plan(T, Ci, Co, dtype != EQL_F32);
+  eqk::gemm_plan_rows(a.plan, N, T, dtype != EQL_F32, eqk::device_cu_count());
   if (!bwd) {
     a.wsp = wspec;
     a.Ci_pad = d.CiF;
@@ -440,7 +444,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
     a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
     a.Ci_pad = d.CoutB;
   }
-  return launched(eqk::launch_gemm(dtype == EQL_F16, T, bwd, a));
+  return launched(eqk::launch_gemm(dtype, T, bwd, a));
 }
 
 int eqlinear_forward(const void* x, const void* wspec, const void* bias, void* y, int64_t N,
@@ -455,7 +459,7 @@ int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t
 
 size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype) {
   if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK || N == 0) return 0;
-  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype);
   return align256(p.part_bytes) + align256(p.dbpart_bytes);
 }
 
@@ -533,7 +537,7 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
     workspace = device_scratch();
     if (!workspace) return EQL_ERR_LAUNCH;
   }
-  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype);
   eqk::WgradArgs a{};
   a.x = x;
   a.dy = dy;
@@ -545,7 +549,7 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
   a.Cin = Cin;
   a.Cout = Cout;
   a.stream = (hipStream_t)stream;
-  return launched(eqk::launch_wgrad(dtype == EQL_F16, T, a, p));
+  return launched(eqk::launch_wgrad(dtype, T, a, p));
 }
 
 
@@ -560,12 +564,12 @@ extern "C" {
 
 int eqlinear_backward_is_fused(int64_t N, int T, int Cin, int Cout, int dtype) {
   if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK) return 0;
-  return eqk::fused_plan(N, T, Cin, Cout, dtype == EQL_F16).ok ? 1 : 0;
+  return eqk::fused_plan(N, T, Cin, Cout, dtype).ok ? 1 : 0;
 }
 
 size_t eqlinear_backward_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype) {
   if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK || N == 0) return 0;
-  const eqk::FusedPlan f = eqk::fused_plan(N, T, Cin, Cout, dtype == EQL_F16);
+  const eqk::FusedPlan f = eqk::fused_plan(N, T, Cin, Cout, dtype);
   if (f.ok) return align256(f.part_bytes) + align256(f.dbpart_bytes);
   return eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dtype);
 }
@@ -592,15 +596,14 @@ int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx
                       {workspace, need}};
   if (any_overlap(r, 7)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
-  const bool f16 = dtype == EQL_F16;
-  const eqk::FusedPlan p = eqk::fused_plan(N, T, Cin, Cout, f16);
+  const eqk::FusedPlan p = eqk::fused_plan(N, T, Cin, Cout, dtype);
   if (!p.ok) {
     st = eqlinear_backward_input(dy, wspec, dx, N, T, Cin, Cout, dtype, stream);
     if (st) return st;
     return eqlinear_backward_weight(x, dy, dw, dbias, workspace, workspace_bytes, N, T, Cin, Cout, dtype,
                                     stream);
   }
-  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, f16);
+  const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype != EQL_F32);
   eqk::FusedArgs a{};
   a.x = x;
   a.dy = dy;
@@ -616,7 +619,7 @@ int eqlinear_backward(const void* x, const void* dy, const void* wspec, void* dx
   a.CinB = d.CinB;
   a.CoutB = d.CoutB;
   a.stream = (hipStream_t)stream;
-  return launched(eqk::launch_bwd_fused(f16, T, a, p));
+  return launched(eqk::launch_bwd_fused(dtype, T, a, p));
 }
 
 }  // extern "C"
@@ -671,8 +674,9 @@ int dihedral_common(bool expand, const void* in, const void* in_b, void* out, vo
   if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   hipStream_t s = (hipStream_t)stream;
-  return dtype == EQL_F16 ? dihedral_launch<_Float16>(expand, in, in_b, out, out_b, T, Cin, Cout, s)
-                          : dihedral_launch<float>(expand, in, in_b, out, out_b, T, Cin, Cout, s);
+  if (dtype == EQL_F16) return dihedral_launch<_Float16>(expand, in, in_b, out, out_b, T, Cin, Cout, s);
+  if (dtype == EQL_BF16) return dihedral_launch<__bf16>(expand, in, in_b, out, out_b, T, Cin, Cout, s);
+  return dihedral_launch<float>(expand, in, in_b, out, out_b, T, Cin, Cout, s);
 }
 
 }  // namespace
@@ -697,7 +701,7 @@ int eqlinear_dihedral_fold(const void* dw_ct, const void* dbias_ct, void* dw, vo
 namespace {
 
 int gconv_shape(int T, int Cin, int Cout, int k, int dtype) {
-  if (dtype != EQL_F32 && dtype != EQL_F16) return EQL_ERR_INVALID_ARG;
+  if (!valid_dtype(dtype)) return EQL_ERR_INVALID_ARG;
   if (Cin < 1 || Cout < 1 || k < 1) return EQL_ERR_INVALID_ARG;
   if (T != 1 && T != 2 && T != 4) return EQL_ERR_UNSUPPORTED;
   if (k % 2 == 0 || k > 7) return EQL_ERR_UNSUPPORTED;
@@ -778,8 +782,9 @@ int gconv_common(int op, const void* in, void* out, int64_t B, int H, int W, int
   if (any_overlap(r, 2)) return EQL_ERR_INVALID_ARG;
   if ((st = check_device())) return st;
   hipStream_t s = (hipStream_t)stream;
-  return dtype == EQL_F16 ? gconv_launch<_Float16>(op, in, out, B, H, W, T, Cin, Cout, k, s)
-                          : gconv_launch<float>(op, in, out, B, H, W, T, Cin, Cout, k, s);
+  if (dtype == EQL_F16) return gconv_launch<_Float16>(op, in, out, B, H, W, T, Cin, Cout, k, s);
+  if (dtype == EQL_BF16) return gconv_launch<__bf16>(op, in, out, B, H, W, T, Cin, Cout, k, s);
+  return gconv_launch<float>(op, in, out, B, H, W, T, Cin, Cout, k, s);
 }
 
 }  // namespace

@@ -41,11 +41,14 @@
 
 namespace eqk {
 
-template <int T, bool F16, int WGC, int CT, int OTW>
+template <int T, int DT, int WGC, int CT, int OTW>
 __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
     const void* __restrict__ x, const void* __restrict__ dy, const void* __restrict__ wsp,
     void* __restrict__ dx, float* __restrict__ part, float* __restrict__ dbpart, int64_t N, int Cin,
     int Cout, int64_t rows_per_split, int n_splits, int CinB, int CoutB, int nks, int dbuf) {
+  // fp32 and fp16 (bf16 layers take the two-pass backward)
+  static_assert(DT != kBF16, "single-pass backward: fp32 or fp16");
+  constexpr bool F16 = DT == kF16;
   using Bn = Bins<T>;
   constexpr int WGO = 8 / WGC;
   constexpr int EB = F16 ? 2 : 4;
@@ -272,16 +275,16 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
         FR A[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) A[p] = lds_frag<FB, RB>(&xs[p * BC * RB], cl, g);
-        frag_mma<F16, KW>(acc[0][a][b], A[0], Bf[0]);
-        if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a][b], A[1], Bf[1]);
+        frag_mma<DT, KW>(acc[0][a][b], A[0], Bf[0]);
+        if constexpr (Bn::kEven) frag_mma<DT, KW>(acc[1][a][b], A[1], Bf[1]);
         static_for<Bn::K>([&](auto ki) {
           constexpr int k = decltype(ki)::value + 1;
           constexpr int r = Bn::re(k);
           constexpr int i = Bn::im(k);
-          frag_mma<F16, KW>(acc[r][a][b], A[r], Bf[r]);
-          frag_mma<F16, KW>(acc[i][a][b], A[r], Bf[i]);
-          frag_mma<F16, KW>(acc[r][a][b], A[i], Bf[i]);
-          frag_mma<F16, KW>(acc[i][a][b], frag_neg<F16, FB>(A[i]), Bf[r]);
+          frag_mma<DT, KW>(acc[r][a][b], A[r], Bf[r]);
+          frag_mma<DT, KW>(acc[i][a][b], A[r], Bf[i]);
+          frag_mma<DT, KW>(acc[r][a][b], A[i], Bf[i]);
+          frag_mma<DT, KW>(acc[i][a][b], frag_neg<DT, FB>(A[i]), Bf[r]);
         });
       }
     }
@@ -318,17 +321,17 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
         const char* const wb = wl + s * T * C16 * RB;
         auto A = [&](int p) __attribute__((always_inline)) { return lds_frag<FB, RB>(ab + p * KR * RB, rt * 16 + li, g); };
         auto W = [&](int p) __attribute__((always_inline)) { return lds_frag<FB, RB>(wb + p * C16 * RB, cti * 16 + li, g); };
-        frag_mma<F16, KW>(ax[0], A(0), W(0));
-        if constexpr (Bn::kEven) frag_mma<F16, KW>(ax[1], A(1), W(1));
+        frag_mma<DT, KW>(ax[0], A(0), W(0));
+        if constexpr (Bn::kEven) frag_mma<DT, KW>(ax[1], A(1), W(1));
         static_for<Bn::K>([&](auto ki) {
           constexpr int k = decltype(ki)::value + 1;
           constexpr int r = Bn::re(k);
           constexpr int i = Bn::im(k);
           const FR ar = A(r), ai = A(i), wr = W(r), wi = W(i);
-          frag_mma<F16, KW>(ax[r], ar, wr);
-          frag_mma<F16, KW>(ax[i], ai, wr);
-          frag_mma<F16, KW>(ax[r], ai, wi);
-          frag_mma<F16, KW>(ax[i], frag_neg<F16, FB>(ar), wi);
+          frag_mma<DT, KW>(ax[r], ar, wr);
+          frag_mma<DT, KW>(ax[i], ai, wr);
+          frag_mma<DT, KW>(ax[r], ai, wi);
+          frag_mma<DT, KW>(ax[i], frag_neg<DT, FB>(ar), wi);
         });
       }
 #pragma unroll
@@ -347,7 +350,7 @@ __global__ __launch_bounds__(512) void eql_bwd_fused_kernel(
   };
   auto dx_store = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) store_run_rsrc<F16, T>(dxrs, dxoff[q], dxv[q]);
+    for (int q = 0; q < 4; ++q) store_run_rsrc<DT, T>(dxrs, dxoff[q], dxv[q]);
   };
 #pragma unroll
   for (int q = 0; q < 4; ++q) {

@@ -25,6 +25,8 @@
 #include <type_traits>
 #include <utility>
 
+#include "eql_config.h"
+
 namespace eqk {
 
 // ---------------------------------------------------------------------------
@@ -347,18 +349,25 @@ __device__ __forceinline__ void irdft(const float (&P)[T], float (&u)[T]) {
 }
 
 // ---------------------------------------------------------------------------
-// Element types.  F16 tensors hold IEEE binary16.  Their forward transforms
-// run in packed fp16 arithmetic (H2Ops); products accumulate in fp32 and the
-// inverse transforms and the weight spectrum are computed in fp32.
-template <bool F16>
+// Element types, by their codes (eql_config.h).  Products accumulate in
+// fp32; the inverse transforms and the weight spectrum are computed in fp32.
+// Forward transforms of fp16 data run in packed fp16 arithmetic (H2Ops);
+// those of bf16 data (8 significand bits, too few for transform arithmetic)
+// in fp32, each result rounded once to bf16 as an MFMA operand.
+template <int DT>
 struct Elem;
 template <>
-struct Elem<true> {
+struct Elem<kF16> {
   using T = _Float16;
   static constexpr int bytes = 2;
 };
 template <>
-struct Elem<false> {
+struct Elem<kBF16> {
+  using T = __bf16;
+  static constexpr int bytes = 2;
+};
+template <>
+struct Elem<kF32> {
   using T = float;
   static constexpr int bytes = 4;
 };
@@ -403,21 +412,29 @@ __device__ __forceinline__ void f16x2_to_f32(uint32_t w, float& lo, float& hi) {
       : "=&v"(lo), "=v"(hi)
       : "v"(w));
 }
-template <bool F16, int NW>
-__device__ __forceinline__ void raw_to_floats(const uint32_t* r, float (&f)[F16 ? 2 * NW : NW]) {
+// bf16 word -> the floats of its two halves (low half first); exact
+__device__ __forceinline__ void bf16x2_to_f32(uint32_t w, float& lo, float& hi) {
+  lo = __builtin_bit_cast(float, w << 16);
+  hi = __builtin_bit_cast(float, w & 0xffff0000u);
+}
+template <int DT, int NW>
+__device__ __forceinline__ void raw_to_floats(const uint32_t* r, float (&f)[DT != kF32 ? 2 * NW : NW]) {
 #pragma unroll
   for (int v = 0; v < NW; ++v) {
-    if constexpr (F16) f16x2_to_f32(r[v], f[2 * v], f[2 * v + 1]);
+    if constexpr (DT == kF16) f16x2_to_f32(r[v], f[2 * v], f[2 * v + 1]);
+    else if constexpr (DT == kBF16) bf16x2_to_f32(r[v], f[2 * v], f[2 * v + 1]);
     else f[v] = __builtin_bit_cast(float, r[v]);
   }
 }
 
-// Two floats rounded to fp16 (round to nearest even) and packed, a in the low half.
-template <bool F16>
+// Two floats rounded to the 16-bit type (round to nearest even) and packed,
+// a in the low half; fp32: a alone.
+template <int DT>
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
-  if constexpr (F16) {
-    const uint16_t lo = __builtin_bit_cast(uint16_t, (_Float16)a);
-    const uint16_t hi = __builtin_bit_cast(uint16_t, (_Float16)b);
+  if constexpr (DT != kF32) {
+    using E = typename Elem<DT>::T;
+    const uint16_t lo = __builtin_bit_cast(uint16_t, (E)a);
+    const uint16_t hi = __builtin_bit_cast(uint16_t, (E)b);
     return (uint32_t)lo | ((uint32_t)hi << 16);
   } else {
     return __builtin_bit_cast(uint32_t, a);
@@ -428,15 +445,15 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 // Contiguous store of L elements at an element offset, converting from float.
 // VEC is the widest power-of-two byte width (<= 16) that divides L * elem
 // bytes; the caller states whether the start is VEC-aligned.
-template <bool F16, int L>
+template <int DT, int L>
 __device__ __forceinline__ void store_run(void* base, int64_t elem_off, bool vec_ok, int n_valid,
                                           const float (&v)[L]) {
-  using E = typename Elem<F16>::T;
-  constexpr int NB = L * Elem<F16>::bytes;
+  using E = typename Elem<DT>::T;
+  constexpr int NB = L * Elem<DT>::bytes;
   constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
   E* p = reinterpret_cast<E*>(base) + elem_off;
   if (vec_ok && n_valid >= L && VEC >= 4) {
-    constexpr int PER = VEC / Elem<F16>::bytes;
+    constexpr int PER = VEC / Elem<DT>::bytes;
 #pragma unroll
     for (int s = 0; s < L / PER; ++s) {
       E tmp[PER];

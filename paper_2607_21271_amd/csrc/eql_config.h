@@ -12,4 +12,8 @@ constexpr int kGemmPairs = EQL_GEMM_PAIRS;
 constexpr int kGemmThreads = 128 * kGemmPairs;
 constexpr int kGemmRoundRows = 16 * kGemmPairs;
 
+// Element type codes, equal to the C ABI's dtype values: IEEE binary32,
+// IEEE binary16, bfloat16.
+constexpr int kF32 = 0, kF16 = 1, kBF16 = 2;
+
 }  // namespace eqk

@@ -5,11 +5,11 @@
 namespace eqk {
 namespace {
 
-template <bool F16, typename F>
+template <int DT, typename F>
 hipError_t by_t(int T, F&& f) {
   switch (T) {
 #define EQK_CASE(t) \
-  case t: return f(Inst<t, F16>{});
+  case t: return f(Inst<t, DT>{});
     EQK_CASE(1) EQK_CASE(2) EQK_CASE(3) EQK_CASE(4) EQK_CASE(5) EQK_CASE(6) EQK_CASE(7)
     EQK_CASE(8) EQK_CASE(9) EQK_CASE(10) EQK_CASE(11) EQK_CASE(12) EQK_CASE(13) EQK_CASE(14)
     EQK_CASE(15) EQK_CASE(16)
@@ -19,26 +19,29 @@ hipError_t by_t(int T, F&& f) {
 }
 
 template <typename F>
-hipError_t by_type(bool f16, int T, F&& f) {
-  return f16 ? by_t<true>(T, f) : by_t<false>(T, f);
+hipError_t by_type(int dt, int T, F&& f) {
+  if (dt == kF16) return by_t<kF16>(T, f);
+  if (dt == kBF16) return by_t<kBF16>(T, f);
+  if (dt == kF32) return by_t<kF32>(T, f);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_wspec(bool f16, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s) {
-  return by_type(f16, T, [&](auto inst) { return decltype(inst)::wspec(w, wspec, Cin, Cout, s); });
+hipError_t launch_wspec(int dt, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s) {
+  return by_type(dt, T, [&](auto inst) { return decltype(inst)::wspec(w, wspec, Cin, Cout, s); });
 }
 
-hipError_t launch_gemm(bool f16, int T, bool bwd, const GemmArgs& a) {
-  return by_type(f16, T, [&](auto inst) { return decltype(inst)::gemm(bwd, a); });
+hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a) {
+  return by_type(dt, T, [&](auto inst) { return decltype(inst)::gemm(bwd, a); });
 }
 
-hipError_t launch_wgrad(bool f16, int T, const WgradArgs& a, const WgradPlan& p) {
-  return by_type(f16, T, [&](auto inst) { return decltype(inst)::wgrad(a, p); });
+hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p) {
+  return by_type(dt, T, [&](auto inst) { return decltype(inst)::wgrad(a, p); });
 }
 
-hipError_t launch_bwd_fused(bool f16, int T, const FusedArgs& a, const FusedPlan& p) {
-  return by_type(f16, T, [&](auto inst) { return decltype(inst)::bwd_fused(a, p); });
+hipError_t launch_bwd_fused(int dt, int T, const FusedArgs& a, const FusedPlan& p) {
+  return by_type(dt, T, [&](auto inst) { return decltype(inst)::bwd_fused(a, p); });
 }
 
 }  // namespace eqk

@@ -31,11 +31,12 @@
 
 namespace eqk {
 
-template <int T, bool F16>
+template <int T, int DT>
 struct GemmShape {
-  static constexpr int EB = F16 ? 2 : 4;
+  static constexpr bool W16 = DT != kF32;  // 16-bit elements (fp16 or bf16)
+  static constexpr int EB = W16 ? 2 : 4;
   static constexpr int kw_fit = 128 / (T * EB);  // channels whose T values fill <= 128 bytes
-  static constexpr int KW = F16 ? (kw_fit >= 8 ? 8 : 4)
+  static constexpr int KW = W16 ? (kw_fit >= 8 ? 8 : 4)
                                 : (kw_fit >= 8 ? 8 : kw_fit >= 4 ? 4 : kw_fit >= 2 ? 2 : 1);
   static constexpr int KSTEP = 4 * KW;  // contraction channels per step (4 lane groups)
   static constexpr int FB = KW * EB;    // operand fragment bytes per lane
@@ -51,20 +52,32 @@ struct Frag {
   uint32_t w[FB / 4];
 };
 
-template <bool F16, int KW>
-__device__ __forceinline__ void frag_mma(floatx4& acc, const Frag<KW*(F16 ? 2 : 4)>& a,
-                                         const Frag<KW*(F16 ? 2 : 4)>& b) {
-  if constexpr (F16 && KW == 8) {
+template <int DT, int KW>
+__device__ __forceinline__ void frag_mma(floatx4& acc, const Frag<KW*(DT != kF32 ? 2 : 4)>& a,
+                                         const Frag<KW*(DT != kF32 ? 2 : 4)>& b) {
+  if constexpr (DT == kF16 && KW == 8) {
     const u32x4 av = {a.w[0], a.w[1], a.w[2], a.w[3]};
     const u32x4 bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
     acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, av),
                                                  __builtin_bit_cast(half8, bv), acc, 0, 0, 0);
-  } else if constexpr (F16 && KW == 4) {
+  } else if constexpr (DT == kF16 && KW == 4) {
     typedef _Float16 half4 __attribute__((ext_vector_type(4)));
     const u32x2 av = {a.w[0], a.w[1]};
     const u32x2 bv = {b.w[0], b.w[1]};
     acc = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(half4, av),
                                                 __builtin_bit_cast(half4, bv), acc, 0, 0, 0);
+  } else if constexpr (DT == kBF16 && KW == 8) {
+    typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+    const u32x4 av = {a.w[0], a.w[1], a.w[2], a.w[3]};
+    const u32x4 bv = {b.w[0], b.w[1], b.w[2], b.w[3]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                  __builtin_bit_cast(bf16x8, bv), acc, 0, 0, 0);
+  } else if constexpr (DT == kBF16 && KW == 4) {
+    typedef short short4v __attribute__((ext_vector_type(4)));
+    const u32x2 av = {a.w[0], a.w[1]};
+    const u32x2 bv = {b.w[0], b.w[1]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4v, av),
+                                                    __builtin_bit_cast(short4v, bv), acc, 0, 0, 0);
   } else {
 #pragma unroll
     for (int s = 0; s < KW; ++s)
@@ -73,11 +86,12 @@ __device__ __forceinline__ void frag_mma(floatx4& acc, const Frag<KW*(F16 ? 2 : 
   }
 }
 
-template <bool F16, int FB>
+// sign flip of every element (the sign is the top bit of fp16, bf16 and fp32)
+template <int DT, int FB>
 __device__ __forceinline__ Frag<FB> frag_neg(const Frag<FB>& a) {
   Frag<FB> r;
 #pragma unroll
-  for (int j = 0; j < FB / 4; ++j) r.w[j] = a.w[j] ^ (F16 ? 0x80008000u : 0x80000000u);
+  for (int j = 0; j < FB / 4; ++j) r.w[j] = a.w[j] ^ (DT != kF32 ? 0x80008000u : 0x80000000u);
   return r;
 }
 
@@ -119,10 +133,10 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
 // No branch skips a store, so every path through a loop issues the same
 // memory operations and the compiler's memory-counter waits stay exact.
 constexpr uint32_t kDropOffset = 0x80000000u;
-template <bool F16, int L>
+template <int DT, int L>
 __device__ __forceinline__ void store_run_rsrc(__amdgpu_buffer_rsrc_t rs, uint32_t off, const float (&v)[L]) {
-  using E = typename Elem<F16>::T;
-  constexpr int EBY = Elem<F16>::bytes;
+  using E = typename Elem<DT>::T;
+  constexpr int EBY = Elem<DT>::bytes;
   constexpr int NB = L * EBY;
   constexpr int VEC = (NB % 16 == 0) ? 16 : (NB % 8 == 0) ? 8 : (NB % 4 == 0) ? 4 : 2;
   constexpr int PER = VEC / EBY;
@@ -203,12 +217,12 @@ __device__ __forceinline__ void mask_raw(int nvalid_elems, uint32_t (&r)[NB / 4]
 }
 
 // Transform the HKW channels held raw by one lane; P[p][j] is plane p of channel j.
-template <int T, bool F16, int HKW>
-__device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (F16 ? 2 : 4) / 4],
+template <int T, int DT, int HKW>
+__device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (DT != kF32 ? 2 : 4) / 4],
                                               float (&P)[T][HKW]) {
-  constexpr int NW = HKW * T * (F16 ? 2 : 4) / 4;
-  float f[F16 ? 2 * NW : NW];
-  raw_to_floats<F16, NW>(r, f);
+  constexpr int NW = HKW * T * (DT != kF32 ? 2 : 4) / 4;
+  float f[DT != kF32 ? 2 * NW : NW];
+  raw_to_floats<DT, NW>(r, f);
 #pragma unroll
   for (int j = 0; j < HKW; ++j) {
     float v[T], q[T];
@@ -252,9 +266,9 @@ __device__ __forceinline__ void raw_to_packed_planes(const uint32_t (&r)[HKW * T
 enum GemmMode { kStream = 0, kRes = 1, kStat = 2 };
 
 // LDS arena of one workgroup: two spectrum buffers, then the weight blocks.
-template <int T, bool F16, int OT>
+template <int T, int DT, int OT>
 struct GemmLds {
-  static constexpr int RB = GemmShape<T, F16>::RB;
+  static constexpr int RB = GemmShape<T, DT>::RB;
   static constexpr int XBLK = kGemmPairs * T * 16 * RB;  // pairs x T planes x 16 rows
   static constexpr int WBLK = T * 32 * OT * RB; // T planes x OC channels
   static constexpr int bytes(int n_wblocks) { return 2 * XBLK + n_wblocks * WBLK; }
@@ -270,17 +284,17 @@ struct GemmLds {
 // barrier both waves read complete MFMA operands from it.  Weight blocks are
 // double buffered in LDS: the next block is loaded into registers while the
 // current one feeds the MFMAs, then written to the idle buffer.
-template <int T, bool F16, bool BWD, int OT, int MODE, int NKR, bool NARROW>
+template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW>
 __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __restrict__ in,
                                                        const void* __restrict__ wsp,
                                                        const void* __restrict__ bias,
                                                        void* __restrict__ out, int64_t N, int Ci,
                                                        int Co, int Ci_pad, int Co_pad, int n_oc,
                                                        int n_ks) {
-  using S = GemmShape<T, F16>;
+  using S = GemmShape<T, DT>;
   using Bn = Bins<T>;
   using FR = Frag<S::FB>;
-  using E = typename Elem<F16>::T;
+  using E = typename Elem<DT>::T;
   constexpr int EB = S::EB;
   constexpr int KW = S::KW;
   constexpr int HKW = KW / 2;
@@ -290,11 +304,11 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   constexpr int NBH = S::NBH;           // raw activation bytes per lane per step
   constexpr int OC = 32 * OT;
   constexpr bool RES = MODE == kRes;
-  constexpr int WBLK = GemmLds<T, F16, OT>::WBLK;  // bytes of one weight block
+  constexpr int WBLK = GemmLds<T, DT, OT>::WBLK;  // bytes of one weight block
   constexpr int NU = WBLK / 16;         // 16-byte units per block
   constexpr int NTH = kGemmThreads;
   constexpr int UPT = (NU + NTH - 1) / NTH; // weight units per thread
-  constexpr int XBLK = GemmLds<T, F16, OT>::XBLK;  // bytes of one spectrum buffer
+  constexpr int XBLK = GemmLds<T, DT, OT>::XBLK;  // bytes of one spectrum buffer
   static_assert(KW >= 2, "contraction split");
 
   // dynamic LDS: xl[2][XBLK], then the weight blocks (2 streamed, 2 * NKR with a
@@ -385,9 +399,18 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     constexpr int X = decltype(set)::value;
     mask_raw<NBH, EB>(xr_valid[X], xr[X]);
     const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
-    if constexpr (F16) {
+    if constexpr (DT != kF32) {
       uint32_t W[T][HKW / 2];
-      raw_to_packed_planes<T, HKW>(xr[X], W);
+      if constexpr (DT == kF16) {
+        raw_to_packed_planes<T, HKW>(xr[X], W);
+      } else {
+        float P[T][HKW];
+        raw_to_planes<T, DT, HKW>(xr[X], P);
+#pragma unroll
+        for (int p = 0; p < T; ++p)
+#pragma unroll
+          for (int j = 0; j < HKW / 2; ++j) W[p][j] = pack2<DT>(P[p][2 * j], P[p][2 * j + 1]);
+      }
 #pragma unroll
       for (int p = 0; p < T; ++p) {
         char* dst = xlb + xb * XBLK + (rg * T + p) * 16 * RB + wl_off<RB>(li, byte);
@@ -397,7 +420,7 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
       return;
     }
     float P[T][HKW];
-    raw_to_planes<T, F16, HKW>(xr[X], P);
+    raw_to_planes<T, DT, HKW>(xr[X], P);
 #pragma unroll
     for (int p = 0; p < T; ++p) {
       {
@@ -442,7 +465,7 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     if constexpr (!RES) {
       static_for<Bn::K>([&](auto ki) {
         constexpr int k = decltype(ki)::value + 1;
-        Xneg[k - 1] = frag_neg<F16, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
+        Xneg[k - 1] = frag_neg<DT, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
       });
     }
 #pragma unroll
@@ -452,32 +475,32 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
       FR W[T];
 #pragma unroll
       for (int p = 0; p < T; ++p) W[p] = lds_frag<FB, RB>(wlb + blk * WBLK + p * OC * RB, ot * 16 + li, g);
-      frag_mma<F16, KW>(acc[0][a], X[0], W[0]);
-      if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a], X[1], W[1]);
+      frag_mma<DT, KW>(acc[0][a], X[0], W[0]);
+      if constexpr (Bn::kEven) frag_mma<DT, KW>(acc[1][a], X[1], W[1]);
       static_for<Bn::K>([&](auto ki) {
         constexpr int k = decltype(ki)::value + 1;
         constexpr int r = Bn::re(k);
         constexpr int i = Bn::im(k);
         if constexpr (RES && !BWD) {
-          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
-          frag_mma<F16, KW>(acc[i][a], X[r], W[i]);
-          frag_mma<F16, KW>(accx[k - 1][a], X[i], W[i]);   // subtracted from Re
-          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<DT, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<DT, KW>(acc[i][a], X[r], W[i]);
+          frag_mma<DT, KW>(accx[k - 1][a], X[i], W[i]);   // subtracted from Re
+          frag_mma<DT, KW>(acc[i][a], X[i], W[r]);
         } else if constexpr (RES) {
-          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
-          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
-          frag_mma<F16, KW>(acc[r][a], X[i], W[i]);
-          frag_mma<F16, KW>(accx[k - 1][a], X[r], W[i]);   // subtracted from Im
+          frag_mma<DT, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<DT, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<DT, KW>(acc[r][a], X[i], W[i]);
+          frag_mma<DT, KW>(accx[k - 1][a], X[r], W[i]);   // subtracted from Im
         } else if constexpr (!BWD) {
-          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
-          frag_mma<F16, KW>(acc[i][a], X[r], W[i]);
-          frag_mma<F16, KW>(acc[r][a], Xneg[k - 1], W[i]);
-          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<DT, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<DT, KW>(acc[i][a], X[r], W[i]);
+          frag_mma<DT, KW>(acc[r][a], Xneg[k - 1], W[i]);
+          frag_mma<DT, KW>(acc[i][a], X[i], W[r]);
         } else {
-          frag_mma<F16, KW>(acc[r][a], X[r], W[r]);
-          frag_mma<F16, KW>(acc[i][a], X[i], W[r]);
-          frag_mma<F16, KW>(acc[r][a], X[i], W[i]);
-          frag_mma<F16, KW>(acc[i][a], Xneg[k - 1], W[i]);
+          frag_mma<DT, KW>(acc[r][a], X[r], W[r]);
+          frag_mma<DT, KW>(acc[i][a], X[i], W[r]);
+          frag_mma<DT, KW>(acc[r][a], X[i], W[i]);
+          frag_mma<DT, KW>(acc[i][a], Xneg[k - 1], W[i]);
         }
       });
     }
@@ -524,7 +547,7 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
           irdft<T>(Pl, ul);
         }
         const uint32_t off = (active && q < len && o < Co) ? (uint32_t)((q * Co + o) * T * EB) : kDropOffset;
-        store_run_rsrc<F16, T>(ors, off, ul);
+        store_run_rsrc<DT, T>(ors, off, ul);
       }
     }
   };

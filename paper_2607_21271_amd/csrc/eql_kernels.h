@@ -18,7 +18,7 @@ namespace eqk {
 //   forward  layout  F[p][o][c], dims [T][CoF][CiF]     (operand of the forward)
 //   backward layout  B[p][c][o], dims [T][CinB][CoutB]  (operand of the input gradient)
 // A workgroup of 256 threads owns a tile of kWsC = 64 input channels x WO
-// output channels (WO = 256 * VEC / 64: 32 for fp16, 16 for fp32).  Thread
+// output channels (WO = 256 * VEC / 64: 32 for 16-bit elements, 16 for fp32).  Thread
 // (o, chunk) loads VEC = 16 / EB consecutive input channels of one output
 // channel at every lag, all T loads in flight at once (one memory round
 // trip), transforms them in fp32, rounds once, writes the VEC entries of F as
@@ -28,12 +28,12 @@ namespace eqk {
 // layouts' extents, and entries past Cout or Cin are zero.  Inputs whose base
 // or row stride is not a multiple of 16 bytes are read element by element.
 constexpr int kWsC = 64;
-template <int T, bool F16>
+template <int T, int DT>
 __global__ __launch_bounds__(256) void eql_wspec_kernel(const void* __restrict__ w,
                                                         void* __restrict__ wspec, int Cin, int Cout,
                                                         int CoF, int CiF, int CinB, int CoutB) {
-  using E = typename Elem<F16>::T;
-  constexpr int EB = F16 ? 2 : 4;
+  using E = typename Elem<DT>::T;
+  constexpr int EB = Elem<DT>::bytes;
   constexpr int VEC = 16 / EB;             // channels per 16-byte run
   constexpr int CPR = kWsC / VEC;          // threads per output channel of the tile
   constexpr int WO = 256 / CPR;            // output channels per tile

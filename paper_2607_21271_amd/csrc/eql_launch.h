@@ -27,43 +27,44 @@ struct GemmPlan {
   int lds_bytes;   // dynamic LDS of one workgroup
 };
 constexpr int kLdsBytes = 160 * 1024;
-constexpr int gemm_kw_c(int T, bool f16) {
-  const int fit = 128 / (T * (f16 ? 2 : 4));
-  if (f16) return fit >= 8 ? 8 : 4;
+// w16: 16-bit elements (fp16 or bf16), which share every shape and layout.
+constexpr int gemm_kw_c(int T, bool w16) {
+  const int fit = 128 / (T * (w16 ? 2 : 4));
+  if (w16) return fit >= 8 ? 8 : 4;
   return fit >= 8 ? 8 : fit >= 4 ? 4 : fit >= 2 ? 2 : 1;
 }
-inline int gemm_kw(int T, bool f16) { return gemm_kw_c(T, f16); }
-constexpr int gemm_rb_c(int T, bool f16) { return 4 * gemm_kw_c(T, f16) * (f16 ? 2 : 4); }
+inline int gemm_kw(int T, bool w16) { return gemm_kw_c(T, w16); }
+constexpr int gemm_rb_c(int T, bool w16) { return 4 * gemm_kw_c(T, w16) * (w16 ? 2 : 4); }
 // LDS of one workgroup with n_wblocks weight blocks: two spectrum buffers of
 // 16*pairs*T rows and the blocks of 32*OT*T rows, each row RB bytes.
-constexpr int gemm_lds_c(int T, bool f16, int OT, int n_wblocks) {
-  return (2 * kGemmRoundRows * T + n_wblocks * 32 * OT * T) * gemm_rb_c(T, f16);
+constexpr int gemm_lds_c(int T, bool w16, int OT, int n_wblocks) {
+  return (2 * kGemmRoundRows * T + n_wblocks * 32 * OT * T) * gemm_rb_c(T, w16);
 }
 // o-tiles per wave: at most 96 accumulator floats per lane (T*OT*4), and two
 // weight blocks plus the spectrum buffers within the LDS.
-constexpr int gemm_otmax_c(int T, bool f16) {
+constexpr int gemm_otmax_c(int T, bool w16) {
   const int by_acc = 24 / T > 8 ? 8 : (24 / T < 1 ? 1 : 24 / T);
   int by_lds = 1;
-  while (by_lds < 8 && gemm_lds_c(T, f16, by_lds + 1, 2) <= kLdsBytes) ++by_lds;
+  while (by_lds < 8 && gemm_lds_c(T, w16, by_lds + 1, 2) <= kLdsBytes) ++by_lds;
   return by_acc < by_lds ? by_acc : by_lds;
 }
-inline int gemm_otmax(int T, bool f16) { return gemm_otmax_c(T, f16); }
-inline int gemm_otres(int T, bool f16) {
-  return gemm_otmax(T, f16) / 2 < 1 ? 1 : gemm_otmax(T, f16) / 2;
+inline int gemm_otmax(int T, bool w16) { return gemm_otmax_c(T, w16); }
+inline int gemm_otres(int T, bool w16) {
+  return gemm_otmax(T, w16) / 2 < 1 ? 1 : gemm_otmax(T, w16) / 2;
 }
 // o-tile counts that have a kernel instantiation: 1, 2, 3, 4, 6, 8 up to the maximum.
-constexpr bool gemm_ot_inst(int T, bool f16, int OT) {
-  return OT >= 1 && OT <= gemm_otmax_c(T, f16) && (OT <= 4 || OT == 6 || OT == 8);
+constexpr bool gemm_ot_inst(int T, bool w16, int OT) {
+  return OT >= 1 && OT <= gemm_otmax_c(T, w16) && (OT <= 4 || OT == 6 || OT == 8);
 }
-inline int gemm_ot_round(int T, bool f16, int want) {
-  for (int ot = want; ot <= gemm_otmax(T, f16); ++ot)
-    if (gemm_ot_inst(T, f16, ot)) return ot;
-  return gemm_otmax(T, f16);
+inline int gemm_ot_round(int T, bool w16, int want) {
+  for (int ot = want; ot <= gemm_otmax(T, w16); ++ot)
+    if (gemm_ot_inst(T, w16, ot)) return ot;
+  return gemm_otmax(T, w16);
 }
 // Widest activation load of one lane's run (KW/2 channels x T elements); the
 // row stride Ci*T*EB must be a multiple of it (eql_gemm.h GemmShape::WV).
-constexpr int gemm_wide_load_c(int T, bool f16) {
-  const int nbh = gemm_kw_c(T, f16) / 2 * T * (f16 ? 2 : 4);
+constexpr int gemm_wide_load_c(int T, bool w16) {
+  const int nbh = gemm_kw_c(T, w16) / 2 * T * (w16 ? 2 : 4);
   return nbh % 16 == 0 ? 16 : nbh % 8 == 0 ? 8 : 4;
 }
 // Weight blocks held in LDS: two streamed blocks, two regions of n_ks blocks
@@ -73,22 +74,22 @@ constexpr int gemm_wblocks(int mode, int n_oc, int n_ks) {
 }
 // EQL_GEMM_MODE=0/1/2 forces a weight mode where it is valid (tests, A/B timing).
 int gemm_forced_mode();
-inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
+inline GemmPlan gemm_plan(int T, int Ci, int Co, bool w16) {
   GemmPlan p{};
-  p.kw = gemm_kw(T, f16);
+  p.kw = gemm_kw(T, w16);
   p.kstep = 4 * p.kw;
   p.n_ks = (Ci + p.kstep - 1) / p.kstep;
   const int per_wave = ((Co + 15) / 16 + 1) / 2;  // o-tiles per wave for one chunk
-  const int otmax = gemm_otmax(T, f16);
+  const int otmax = gemm_otmax(T, w16);
   // resident spectrum: two LDS regions of n_ks weight blocks each
-  const bool res_ok = T <= 8 && p.n_ks <= 3 && p.kw * (f16 ? 2 : 4) <= 16 &&
-                      gemm_lds_c(T, f16, gemm_otres(T, f16), 2 * p.n_ks) <= kLdsBytes;
+  const bool res_ok = T <= 8 && p.n_ks <= 3 && p.kw * (w16 ? 2 : 4) <= 16 &&
+                      gemm_lds_c(T, w16, gemm_otres(T, w16), 2 * p.n_ks) <= kLdsBytes;
   if (per_wave <= otmax) {
-    p.OT = gemm_ot_round(T, f16, per_wave);
+    p.OT = gemm_ot_round(T, w16, per_wave);
     p.n_oc = 1;
     p.mode = 0;
   } else if (res_ok) {
-    p.OT = gemm_otres(T, f16);
+    p.OT = gemm_otres(T, w16);
     p.n_oc = (Co + 32 * p.OT - 1) / (32 * p.OT);
     p.mode = 1;
   } else {
@@ -97,10 +98,10 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
     p.mode = 0;
   }
   // every weight block resident when they all fit
-  if (gemm_lds_c(T, f16, p.OT, p.n_oc * p.n_ks) <= kLdsBytes) p.mode = 2;
+  if (gemm_lds_c(T, w16, p.OT, p.n_oc * p.n_ks) <= kLdsBytes) p.mode = 2;
   const int forced = gemm_forced_mode();
-  if (forced == 0 || (forced == 1 && res_ok && p.OT == gemm_otres(T, f16))) p.mode = forced;
-  p.narrow = ((int64_t)Ci * T * (f16 ? 2 : 4)) % gemm_wide_load_c(T, f16) != 0;
+  if (forced == 0 || (forced == 1 && res_ok && p.OT == gemm_otres(T, w16))) p.mode = forced;
+  p.narrow = ((int64_t)Ci * T * (w16 ? 2 : 4)) % gemm_wide_load_c(T, w16) != 0;
   if (p.narrow) {
     p.OT = 1;
     p.n_oc = (Co + 31) / 32;
@@ -108,7 +109,7 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
   }
   p.OC = 32 * p.OT;
   p.Co_pad = p.n_oc * p.OC;
-  p.lds_bytes = gemm_lds_c(T, f16, p.OT, gemm_wblocks(p.mode, p.n_oc, p.n_ks));
+  p.lds_bytes = gemm_lds_c(T, w16, p.OT, gemm_wblocks(p.mode, p.n_oc, p.n_ks));
   return p;
 }
 
@@ -117,10 +118,10 @@ inline GemmPlan gemm_plan(int T, int Ci, int Co, bool f16) {
 // with at most one round per CU the streamed mode overlaps that load with the
 // MFMAs.  Changes only the mode (never OT or the chunking), so the weight
 // spectrum layout is the same either way.
-inline void gemm_plan_rows(GemmPlan& p, int64_t N, int T, bool f16, int cus) {
+inline void gemm_plan_rows(GemmPlan& p, int64_t N, int T, bool w16, int cus) {
   if (p.mode == 2 && gemm_forced_mode() < 0 && N < (int64_t)2 * 64 * cus) {
     p.mode = 0;
-    p.lds_bytes = gemm_lds_c(T, f16, p.OT, gemm_wblocks(0, p.n_oc, p.n_ks));
+    p.lds_bytes = gemm_lds_c(T, w16, p.OT, gemm_wblocks(0, p.n_oc, p.n_ks));
   }
 }
 
@@ -130,9 +131,9 @@ constexpr int kColPad = 32;
 struct WspecDims {
   int CoF, CiF, CinB, CoutB;
 };
-inline WspecDims wspec_dims(int T, int Cin, int Cout, bool f16) {
-  return {gemm_plan(T, Cin, Cout, f16).Co_pad, round_up(Cin, kColPad),
-          gemm_plan(T, Cout, Cin, f16).Co_pad, round_up(Cout, kColPad)};
+inline WspecDims wspec_dims(int T, int Cin, int Cout, bool w16) {
+  return {gemm_plan(T, Cin, Cout, w16).Co_pad, round_up(Cin, kColPad),
+          gemm_plan(T, Cout, Cin, w16).Co_pad, round_up(Cout, kColPad)};
 }
 
 // Compute units of the current device (cached); 256 if unknown.
@@ -159,7 +160,7 @@ struct WgradPlan {
   int Cin_pad, Cout_pad;
   size_t part_bytes, dbpart_bytes;
 };
-WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, bool f16);
+WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt);  // dt: element type code
 
 // Shape of the partial reduction: NTHR threads per workgroup, runs of IPW
 // items (IPW * 16 bytes per split and plane), G = NTHR / (IPW * T) split
@@ -201,9 +202,9 @@ struct FusedPlan {
   int64_t rows_per_split;
   size_t part_bytes, dbpart_bytes;
 };
-FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, bool f16);
+FusedPlan fused_plan(int64_t N, int T, int Cin, int Cout, int dt);  // none for bf16
 // Variants of eql_bwd_fused_kernel built for group order T and element
-// type: those that fit the 256 registers of a lane at two waves per SIMD
+// type (fp16 or fp32): those that fit the 256 registers of a lane at two waves per SIMD
 // without spilling (the weight-gradient accumulators, the input-gradient
 // tile, two chunks of prefetched raw rows and the transforms; found by
 // compiling every variant, and the post-build check refuses a spilling one).
@@ -269,7 +270,7 @@ struct FusedArgs {
 
 // Launches of one group order and element type (eql_inst.hip, one object per
 // (T, dtype) so the instantiations build in parallel).
-template <int T, bool F16>
+template <int T, int DT>
 struct Inst {
   static hipError_t wspec(const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
   static hipError_t gemm(bool bwd, const GemmArgs& a);
@@ -277,10 +278,10 @@ struct Inst {
   static hipError_t bwd_fused(const FusedArgs& a, const FusedPlan& p);
 };
 
-// Dispatch over T (eql_dispatch.cpp).
-hipError_t launch_wspec(bool f16, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
-hipError_t launch_gemm(bool f16, int T, bool bwd, const GemmArgs& a);
-hipError_t launch_wgrad(bool f16, int T, const WgradArgs& a, const WgradPlan& p);
-hipError_t launch_bwd_fused(bool f16, int T, const FusedArgs& a, const FusedPlan& p);
+// Dispatch over T and the element type code dt (eql_dispatch.cpp).
+hipError_t launch_wspec(int dt, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
+hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a);
+hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p);
+hipError_t launch_bwd_fused(int dt, int T, const FusedArgs& a, const FusedPlan& p);
 
 }  // namespace eqk

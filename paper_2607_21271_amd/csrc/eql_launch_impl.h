@@ -12,13 +12,13 @@
 
 namespace eqk {
 
-template <int T, bool F16>
+template <int T, int DT>
 hipError_t wspec_t(const void* w, void* wspec, int Cin, int Cout, hipStream_t s) {
-  const WspecDims d = wspec_dims(T, Cin, Cout, F16);
+  const WspecDims d = wspec_dims(T, Cin, Cout, DT != kF32);
   const int omax = d.CoF > d.CoutB ? d.CoF : d.CoutB;  // tiles cover both layouts
   const int cmax = d.CiF > d.CinB ? d.CiF : d.CinB;
-  constexpr int WO = 256 * (F16 ? 8 : 4) / kWsC;  // output channels per tile (eql_wspec_kernel)
-  hipLaunchKernelGGL((eql_wspec_kernel<T, F16>),
+  constexpr int WO = 256 * (DT != kF32 ? 8 : 4) / kWsC;  // output channels per tile (eql_wspec_kernel)
+  hipLaunchKernelGGL((eql_wspec_kernel<T, DT>),
                      dim3((unsigned)((omax + WO - 1) / WO), (unsigned)((cmax + kWsC - 1) / kWsC)),
                      dim3(256), 0, s, w, wspec, Cin, Cout, d.CoF, d.CiF, d.CinB, d.CoutB);
   return hipGetLastError();
@@ -61,12 +61,12 @@ inline int persistent_grid(const void* kernel, int threads, int lds, int64_t N, 
   return (int)g;
 }
 
-template <int T, bool F16, bool BWD, int OT, int MODE, int NKR, bool NARROW = false>
+template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW = false>
 hipError_t gemm_variant(const GemmArgs& a) {
-  static_assert(GemmShape<T, F16>::WV == gemm_wide_load_c(T, F16), "host and kernel load widths");
-  auto k = eql_gemm_kernel<T, F16, BWD, OT, MODE, NKR, NARROW>;
+  static_assert(GemmShape<T, DT>::WV == gemm_wide_load_c(T, DT != kF32), "host and kernel load widths");
+  auto k = eql_gemm_kernel<T, DT, BWD, OT, MODE, NKR, NARROW>;
   const int lds = a.plan.lds_bytes;
-  if (lds != gemm_lds_c(T, F16, OT, gemm_wblocks(MODE, a.plan.n_oc, a.plan.n_ks)) || lds > kLdsBytes ||
+  if (lds != gemm_lds_c(T, DT != kF32, OT, gemm_wblocks(MODE, a.plan.n_oc, a.plan.n_ks)) || lds > kLdsBytes ||
       (MODE == kRes && a.plan.n_ks != NKR))
     return hipErrorInvalidValue;
   if (lds > 64 * 1024) {
@@ -75,59 +75,59 @@ hipError_t gemm_variant(const GemmArgs& a) {
   }
   // input and output rows are addressed with 31-bit offsets per workgroup
   const int grid = persistent_grid((const void*)k, kGemmThreads, lds, a.N,
-                                   (int64_t)(a.Ci > a.Co ? a.Ci : a.Co) * T * (F16 ? 2 : 4));
+                                   (int64_t)(a.Ci > a.Co ? a.Ci : a.Co) * T * (DT != kF32 ? 2 : 4));
   hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kGemmThreads), lds, a.stream, a.in, a.wsp, a.bias, a.out,
                      a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
   return hipGetLastError();
 }
 
-template <int T, bool F16, bool BWD, int MODE>
+template <int T, int DT, bool BWD, int MODE>
 hipError_t gemm_ot(const GemmArgs& a) {
   hipError_t r = hipErrorInvalidValue;
   static_for<8>([&](auto oi) {
     constexpr int OT = decltype(oi)::value + 1;
-    if constexpr (gemm_ot_inst(T, F16, OT)) {
-      if (a.plan.OT == OT) r = gemm_variant<T, F16, BWD, OT, MODE, 0>(a);
+    if constexpr (gemm_ot_inst(T, DT != kF32, OT)) {
+      if (a.plan.OT == OT) r = gemm_variant<T, DT, BWD, OT, MODE, 0>(a);
     }
   });
   return r;
 }
 
-template <int T, bool F16, bool BWD>
+template <int T, int DT, bool BWD>
 hipError_t gemm_t(const GemmArgs& a) {
-  constexpr int OTR = gemm_otmax_c(T, F16) / 2 < 1 ? 1 : gemm_otmax_c(T, F16) / 2;
-  constexpr bool kResOk = T <= 8 && GemmShape<T, F16>::FB <= 16;
+  constexpr int OTR = gemm_otmax_c(T, DT != kF32) / 2 < 1 ? 1 : gemm_otmax_c(T, DT != kF32) / 2;
+  constexpr bool kResOk = T <= 8 && GemmShape<T, DT>::FB <= 16;
   const GemmPlan& p = a.plan;
   if (p.narrow) {
     if (p.OT != 1 || p.mode != kStream) return hipErrorInvalidValue;
-    return gemm_variant<T, F16, BWD, 1, kStream, 0, true>(a);
+    return gemm_variant<T, DT, BWD, 1, kStream, 0, true>(a);
   }
-  if (((int64_t)a.Ci * T * (F16 ? 2 : 4)) % GemmShape<T, F16>::WV != 0) return hipErrorInvalidValue;
+  if (((int64_t)a.Ci * T * (DT != kF32 ? 2 : 4)) % GemmShape<T, DT>::WV != 0) return hipErrorInvalidValue;
   if (p.mode == kRes) {
     if constexpr (kResOk) {
       if (p.OT != OTR) return hipErrorInvalidValue;
-      if (p.n_ks == 1) return gemm_variant<T, F16, BWD, OTR, kRes, 1>(a);
-      if (p.n_ks == 2) return gemm_variant<T, F16, BWD, OTR, kRes, 2>(a);
-      if (p.n_ks == 3) return gemm_variant<T, F16, BWD, OTR, kRes, 3>(a);
+      if (p.n_ks == 1) return gemm_variant<T, DT, BWD, OTR, kRes, 1>(a);
+      if (p.n_ks == 2) return gemm_variant<T, DT, BWD, OTR, kRes, 2>(a);
+      if (p.n_ks == 3) return gemm_variant<T, DT, BWD, OTR, kRes, 3>(a);
     }
     return hipErrorInvalidValue;
   }
-  if (p.mode == kStat) return gemm_ot<T, F16, BWD, kStat>(a);
-  if (p.mode == kStream) return gemm_ot<T, F16, BWD, kStream>(a);
+  if (p.mode == kStat) return gemm_ot<T, DT, BWD, kStat>(a);
+  if (p.mode == kStream) return gemm_ot<T, DT, BWD, kStream>(a);
   return hipErrorInvalidValue;
 }
 
 // The split-partial reduction (both weight-gradient kernels write the same
 // partial layout).
-template <int T, bool F16>
+template <int T, int DT>
 hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p);
 
-template <int T, bool F16, int CT, int OT>
+template <int T, int DT, int CT, int OT>
 hipError_t wgrad_rd_variant(const WgradArgs& a, const WgradPlan& p) {
   if (p.S > 0) {
     constexpr int NW = kRdWaves;
     const int lds = (NW - 1) * rd_wave_acc_bytes<T, CT, OT>() + NW * OT * 16 * 4;
-    auto k = eql_wgrad_rd_kernel<T, F16, CT, OT, NW>;
+    auto k = eql_wgrad_rd_kernel<T, DT, CT, OT, NW>;
     if (lds > kLdsBytes) return hipErrorInvalidValue;
     if (lds > 64 * 1024) {
       hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
@@ -141,25 +141,25 @@ hipError_t wgrad_rd_variant(const WgradArgs& a, const WgradPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return wgrad_reduce<T, F16>(a, p);
+  return wgrad_reduce<T, DT>(a, p);
 }
 
-template <int T, bool F16, int WGC, int CT, int OTW>
+template <int T, int DT, int WGC, int CT, int OTW>
 hipError_t wgrad_variant(const WgradArgs& a, const WgradPlan& p) {
   if (p.S > 0) {
     // whole groups of 8 splits (see the tile order in eql_wgrad_kernel)
     const int64_t n_blocks = (int64_t)(p.S + 7) / 8 * 8 * p.n_ct * p.n_ot;
-    hipLaunchKernelGGL((eql_wgrad_kernel<T, F16, WGC, 8 / WGC, CT, OTW>), dim3((unsigned)n_blocks),
+    hipLaunchKernelGGL((eql_wgrad_kernel<T, DT, WGC, 8 / WGC, CT, OTW>), dim3((unsigned)n_blocks),
                        dim3(512), 0, a.stream, a.x, a.dy, a.part, a.db ? a.dbpart : nullptr, a.N,
                        a.Cin, a.Cout, p.rows_per_split, p.n_ct, p.n_ot, p.S, p.Cin_pad,
                        p.Cout_pad);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return wgrad_reduce<T, F16>(a, p);
+  return wgrad_reduce<T, DT>(a, p);
 }
 
-template <int T, bool F16>
+template <int T, int DT>
 hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p) {
   // threads, items per workgroup and split groups of eql_wgrad_reduce_kernel
   const int64_t items = (int64_t)(p.Cin_pad / 4) * p.Cout_pad;
@@ -169,20 +169,20 @@ hipError_t wgrad_reduce(const WgradArgs& a, const WgradPlan& p) {
   const unsigned blocks =
       (unsigned)((items + ipw - 1) / ipw + (a.db ? (a.Cout + NS - 1) / NS : 0));
   if (nthr == 256)
-    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16, 256>), dim3(blocks), dim3(256), 0, a.stream,
+    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, DT, 256>), dim3(blocks), dim3(256), 0, a.stream,
                        a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
   else
-    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, F16, 1024>), dim3(blocks), dim3(1024), 0, a.stream,
+    hipLaunchKernelGGL((eql_wgrad_reduce_kernel<T, DT, 1024>), dim3(blocks), dim3(1024), 0, a.stream,
                        a.part, a.dbpart, a.dw, a.db, p.S, a.Cin, a.Cout, p.Cin_pad, p.Cout_pad, ipw, G);
   return hipGetLastError();
 }
 
 // Single-pass backward: the fused kernel (one workgroup per row split), then
 // the split-partial reduction of the weight gradient.
-template <int T, bool F16, int WGC, int CT, int OTW>
+template <int T, int DT, int WGC, int CT, int OTW>
 hipError_t fused_variant(const FusedArgs& f, const FusedPlan& p) {
   constexpr int BC = WGC * 16 * CT, BO = (8 / WGC) * 16 * OTW;
-  constexpr int KR = F16 ? 32 : 16;
+  constexpr int KR = DT != kF32 ? 32 : 16;
   if (p.BC != BC || p.BO != BO || p.KR != KR || p.nks * KR > BO || p.C16 > BC ||
       p.lds != fused_lds_bytes(T, BC, BO, KR, p.nks, p.C16, p.dbuf != 0) || p.lds > kLdsBytes)
     return hipErrorInvalidValue;
@@ -202,7 +202,7 @@ hipError_t fused_variant(const FusedArgs& f, const FusedPlan& p) {
   wp.Cin_pad = BC;
   wp.Cout_pad = BO;
   if (p.S > 0) {
-    auto k = eql_bwd_fused_kernel<T, F16, WGC, CT, OTW>;
+    auto k = eql_bwd_fused_kernel<T, DT, WGC, CT, OTW>;
     if (p.lds > 64 * 1024) {
       hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, p.lds);
       if (e != hipSuccess) return e;
@@ -213,16 +213,16 @@ hipError_t fused_variant(const FusedArgs& f, const FusedPlan& p) {
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  return wgrad_reduce<T, F16>(a, wp);
+  return wgrad_reduce<T, DT>(a, wp);
 }
 
-template <int T, bool F16>
+template <int T, int DT>
 hipError_t fused_t(const FusedArgs& f, const FusedPlan& p) {
   // the variants of fused_plan that fit the registers (fused_variant_ok)
 #define EQK_FU(W_, C_, O_)                                                  \
-  if constexpr (fused_variant_ok(T, F16, W_, C_, O_)) {                    \
+  if constexpr (DT != kBF16 && fused_variant_ok(T, DT == kF16, W_, C_, O_)) { \
     if (p.wgc == (W_) && p.ct == (C_) && p.otw == (O_))                    \
-      return fused_variant<T, F16, W_, C_, O_>(f, p);                       \
+      return fused_variant<T, DT, W_, C_, O_>(f, p);                       \
   }
   EQK_FU(2, 1, 1)
   EQK_FU(4, 1, 1)
@@ -233,12 +233,12 @@ hipError_t fused_t(const FusedArgs& f, const FusedPlan& p) {
   return hipErrorInvalidValue;
 }
 
-template <int T, bool F16>
+template <int T, int DT>
 hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
   if (p.kind == 1) {
 #define EQK_RD(C_, O_)                                             \
-  if constexpr (rd_fits(T, C_, O_)) {                              \
-    if (p.ct == (C_) && p.otw == (O_)) return wgrad_rd_variant<T, F16, C_, O_>(a, p); \
+  if constexpr (DT != kBF16 && rd_fits(T, C_, O_)) {              \
+    if (p.ct == (C_) && p.otw == (O_)) return wgrad_rd_variant<T, DT, C_, O_>(a, p); \
   }
     EQK_RD(1, 1)
     EQK_RD(1, 2)
@@ -254,7 +254,7 @@ hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
   if constexpr ((C_) * (O_) * T * 4 <= 96 &&                                                 \
                 T * ((W_) * 16 * (C_) + (8 / (W_)) * 16 * (O_)) * 64 <= 160 * 1024 - 4096) {   \
     if (p.wgc == (W_) && p.ct == (C_) && p.otw == (O_))                                      \
-      return wgrad_variant<T, F16, W_, C_, O_>(a, p);                                         \
+      return wgrad_variant<T, DT, W_, C_, O_>(a, p);                                         \
   }
   EQK_WG(2, 1, 1)
   EQK_WG(2, 2, 1)

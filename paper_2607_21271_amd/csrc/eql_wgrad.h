@@ -62,6 +62,22 @@ __device__ __forceinline__ void transform_pair(const uint32_t (&r)[2 * ((2 * T +
   });
   rdft<T, H2Ops>(v, P);
 }
+// bf16: both rows widened to fp32 (exact) and transformed in fp32; the
+// caller rounds plane p of the two rows into one staged word.
+template <int T>
+__device__ __forceinline__ void transform_pair_f32(const uint32_t (&r)[2 * ((2 * T + 3) / 4)], float (&P0)[T],
+                                                   float (&P1)[T]) {
+  constexpr int WPR = (2 * T + 3) / 4;
+  float v0[T], v1[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int sh = (t % 2) ? 0 : 16;  // half t % 2 of word t / 2 into the top 16 bits
+    v0[t] = __builtin_bit_cast(float, (r[t / 2] << sh) & 0xffff0000u);
+    v1[t] = __builtin_bit_cast(float, (r[WPR + t / 2] << sh) & 0xffff0000u);
+  }
+  rdft<T>(v0, P0);
+  rdft<T>(v1, P1);
+}
 template <int T>
 __device__ __forceinline__ void transform_rows(const uint32_t (&r)[2 * T], float (&P0)[T], float (&P1)[T]) {
   float v0[T], v1[T];
@@ -85,7 +101,7 @@ __device__ __forceinline__ void wgrad_item(int item, int& ch, int& rp) {
   rp = (hi / (B / 8)) * 8 + (lo >> 3);
 }
 
-template <int T, bool F16, int WGC, int WGO, int CT, int OTW>
+template <int T, int DT, int WGC, int WGO, int CT, int OTW>
 __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__ x,
                                                         const void* __restrict__ dy,
                                                         float* __restrict__ part,
@@ -94,8 +110,9 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
                                                         int n_ct, int n_ot, int n_splits, int Cin_pad,
                                                         int Cout_pad) {
   using Bn = Bins<T>;
-  constexpr int EB = F16 ? 2 : 4;
-  constexpr int KW = F16 ? 8 : 4;            // rows per lane group per fragment
+  constexpr bool W16 = DT != kF32;           // 16-bit elements (fp16 or bf16)
+  constexpr int EB = W16 ? 2 : 4;
+  constexpr int KW = W16 ? 8 : 4;            // rows per lane group per fragment
   constexpr int KR = 4 * KW;                 // rows per chunk (one MFMA contraction step)
   constexpr int FB = KW * EB;                // 16 bytes
   constexpr int RB = KR * EB;                // 64 bytes: one channel's chunk of rows
@@ -214,12 +231,18 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       if (NIX % 512 != 0 && item >= NIX) continue;
       int c, rp;
       wgrad_item<BC>(item, c, rp);
-      if constexpr (F16) {
+      if constexpr (DT == kF16) {
         half2v P[T];
         transform_pair<T>(rx[u], P);
 #pragma unroll
         for (int p = 0; p < T; ++p)
           *reinterpret_cast<uint32_t*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) = __builtin_bit_cast(uint32_t, P[p]);
+      } else if constexpr (DT == kBF16) {
+        float P0[T], P1[T];
+        transform_pair_f32<T>(rx[u], P0, P1);
+#pragma unroll
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<uint32_t*>(&xs[p * BC * RB + wl_off<RB>(c, rp * 2 * EB)]) = pack2<DT>(P0[p], P1[p]);
       } else {
         float P0[T], P1[T];
         transform_rows<T>(rx[u], P0, P1);
@@ -235,7 +258,7 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
       if (NID % 512 != 0 && item >= NID) continue;
       int o, rp;
       wgrad_item<BO>(item, o, rp);
-      if constexpr (F16) {
+      if constexpr (DT == kF16) {
         half2v P[T];
         transform_pair<T>(rd[u], P);
         // bin 0 of both rows, summed in fp32
@@ -243,6 +266,13 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
 #pragma unroll
         for (int p = 0; p < T; ++p)
           *reinterpret_cast<uint32_t*>(&ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)]) = __builtin_bit_cast(uint32_t, P[p]);
+      } else if constexpr (DT == kBF16) {
+        float P0[T], P1[T];
+        transform_pair_f32<T>(rd[u], P0, P1);
+        dbacc[u] += P0[0] + P1[0];
+#pragma unroll
+        for (int p = 0; p < T; ++p)
+          *reinterpret_cast<uint32_t*>(&ds[p * BO * RB + wl_off<RB>(o, rp * 2 * EB)]) = pack2<DT>(P0[p], P1[p]);
       } else {
         float P0[T], P1[T];
         transform_rows<T>(rd[u], P0, P1);
@@ -278,16 +308,16 @@ __global__ __launch_bounds__(512) void eql_wgrad_kernel(const void* __restrict__
         FR A[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) A[p] = lds_frag<FB, RB>(&xs[p * BC * RB], cl, g);
-        frag_mma<F16, KW>(acc[0][a][b], A[0], Bf[0]);
-        if constexpr (Bn::kEven) frag_mma<F16, KW>(acc[1][a][b], A[1], Bf[1]);
+        frag_mma<DT, KW>(acc[0][a][b], A[0], Bf[0]);
+        if constexpr (Bn::kEven) frag_mma<DT, KW>(acc[1][a][b], A[1], Bf[1]);
         static_for<Bn::K>([&](auto ki) {
           constexpr int k = decltype(ki)::value + 1;
           constexpr int r = Bn::re(k);
           constexpr int i = Bn::im(k);
-          frag_mma<F16, KW>(acc[r][a][b], A[r], Bf[r]);
-          frag_mma<F16, KW>(acc[i][a][b], A[r], Bf[i]);
-          frag_mma<F16, KW>(acc[r][a][b], A[i], Bf[i]);
-          frag_mma<F16, KW>(acc[i][a][b], frag_neg<F16, FB>(A[i]), Bf[r]);
+          frag_mma<DT, KW>(acc[r][a][b], A[r], Bf[r]);
+          frag_mma<DT, KW>(acc[i][a][b], A[r], Bf[i]);
+          frag_mma<DT, KW>(acc[r][a][b], A[i], Bf[i]);
+          frag_mma<DT, KW>(acc[i][a][b], frag_neg<DT, FB>(A[i]), Bf[r]);
         });
       }
     }
@@ -399,14 +429,14 @@ __device__ __forceinline__ floatx4 sum_splits(const float* src, int64_t stride, 
   return acc;
 }
 
-template <int T, bool F16, int NTHR>
+template <int T, int DT, int NTHR>
 __global__ __launch_bounds__(NTHR) void eql_wgrad_reduce_kernel(const float* __restrict__ part,
                                                                        const float* __restrict__ dbpart,
                                                                        void* __restrict__ dw,
                                                                        void* __restrict__ db, int S,
                                                                        int Cin, int Cout, int Cin_pad,
                                                                        int Cout_pad, int IPW, int G) {
-  using E = typename Elem<F16>::T;
+  using E = typename Elem<DT>::T;
   __shared__ floatx4 red[NTHR];
   const int NS = NTHR / G;         // slot lanes (>= IPW * T)
   const int CQ = Cin_pad / 4;

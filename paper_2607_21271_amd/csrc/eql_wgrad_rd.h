@@ -37,14 +37,15 @@
 
 namespace eqk {
 
-template <int T, bool F16, int CT, int OT>
+template <int T, int DT, int CT, int OT>
 struct RdShape {
-  static constexpr int EB = F16 ? 2 : 4;
-  static constexpr int KR = F16 ? 32 : 16;        // rows per chunk
+  static constexpr bool W16 = DT != kF32;
+  static constexpr int EB = W16 ? 2 : 4;
+  static constexpr int KR = W16 ? 32 : 16;        // rows per chunk
   static constexpr int RPL = KR / 4;              // rows per lane
   static constexpr int WPR = (T * EB + 3) / 4;    // raw words of one (row, channel)
   static constexpr int RAW = RPL * WPR;           // raw words of one block per lane
-  static constexpr int OPW = F16 ? 4 : 4;         // operand words per plane per lane
+  static constexpr int OPW = 4;                   // operand words per plane per lane
   static constexpr int BLK = CT + OT;             // blocks loaded per chunk
   static constexpr int BC = 16 * CT, BO = 16 * OT;
 };
@@ -54,12 +55,16 @@ struct RdShape {
 template <int T, int CT, int OT>
 constexpr int rd_wave_acc_bytes() { return T * CT * OT * 64 * 16; }
 
-template <int T, bool F16, int CT, int OT, int NW>
+template <int T, int DT, int CT, int OT, int NW>
 __global__ __launch_bounds__(64 * NW) void eql_wgrad_rd_kernel(
     const void* __restrict__ x, const void* __restrict__ dy, float* __restrict__ part,
     float* __restrict__ dbpart, int64_t N, int Cin, int Cout, int64_t rows_per_split, int n_ct,
     int n_ot, int n_splits, int Cin_pad, int Cout_pad) {
-  using S = RdShape<T, F16, CT, OT>;
+  // fp32 and fp16 only: the bias sum of this kernel reads the rounded bin-0
+  // operands, too coarse in bf16 (the staged kernel serves bf16)
+  static_assert(DT != kBF16, "register-direct weight gradient: fp32 or fp16");
+  constexpr bool F16 = DT == kF16;
+  using S = RdShape<T, DT, CT, OT>;
   using Bn = Bins<T>;
   constexpr int EB = S::EB, KR = S::KR, RPL = S::RPL, WPR = S::WPR, RAW = S::RAW;
   constexpr int ITB = T * EB;  // bytes of one (row, channel)

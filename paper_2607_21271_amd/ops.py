@@ -9,12 +9,14 @@ w [T, Cout, Cin], bias [Cout]; see include/eqlinear.h.
 
 The C ABI receives raw device addresses only, so every check that needs the
 tensors themselves happens here, before any launch: all tensors of a call live
-on one GPU and share one dtype (float32 or float16), outputs that the caller
+on one GPU and share one dtype (float32, float16 or bfloat16), outputs that the caller
 passes in are contiguous with exactly the expected shape, and a weight
 spectrum is a contiguous uint8 buffer of exactly
 ``eqlinear_weight_spectrum_bytes`` bytes for the call's (T, Cin, Cout, dtype)
-(an fp32 spectrum is twice the size of an fp16 one, so a spectrum of the wrong
-dtype is refused).
+(an fp32 spectrum is twice the size of a 16-bit one, so a spectrum of the
+wrong width is refused; fp16 and bf16 spectra have the same size, so the
+caller keeps a spectrum with the dtype it was computed for, as
+``EQLinearFunction`` does).
 """
 from __future__ import annotations
 
@@ -24,12 +26,12 @@ import torch
 
 from . import _lib
 
-_DT = {torch.float32: _lib.EQL_F32, torch.float16: _lib.EQL_F16}
+_DT = {torch.float32: _lib.EQL_F32, torch.float16: _lib.EQL_F16, torch.bfloat16: _lib.EQL_BF16}
 
 
 def _dtype_code(t: torch.Tensor) -> int:
     if t.dtype not in _DT:
-        raise TypeError("eqlinear supports float32 and float16, got %s" % t.dtype)
+        raise TypeError("eqlinear supports float32, float16 and bfloat16, got %s" % t.dtype)
     return _DT[t.dtype]
 
 

@@ -9,8 +9,8 @@ which are not available): ``numpy.random.RandomState(seed).standard_normal``
 in float64, drawn in the order x (N*Cin*T), w (T*Cout*Cin) scaled by
 1/sqrt(T*Cin), b (Cout) scaled by 0.1 when the layer has a bias, dy (N*Cout*T).
 The N(0, s) of each workload description is read with s the variance.  Each
-tensor is then rounded to the run dtype (round-to-nearest-even) and the oracle
-consumes exactly those rounded values.
+tensor is then rounded to the run dtype (round-to-nearest-even; bfloat16 via
+float32) and the oracle consumes exactly those rounded values.
 
 Layer shapes follow the paper's EQ-ViT / EQ-Swin configurations (Table 6) and
 its operator benchmark rows (Sec. 4.1): 64*197 = 12608 tokens for a ViT batch
@@ -24,6 +24,26 @@ from dataclasses import dataclass, field, replace
 import numpy as np
 
 DTYPES = {"f32": np.float32, "f16": np.float16}
+# bfloat16 has no numpy type: its values are held in float32 arrays
+STORAGE = {"f32": np.float32, "f16": np.float16, "bf16": np.float32}
+
+
+def _to_bf16(a) -> np.ndarray:
+    """float32 array of the bfloat16 numbers nearest to ``a`` (rounded to float32
+    first, then to 8 significand bits, round-to-nearest-even on the bit
+    pattern).  Finite inputs only."""
+    f = np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+    bits = f.view(np.uint32).astype(np.uint64)
+    bits = (bits + 0x7FFF + ((bits >> 16) & 1)) & 0xFFFF0000
+    return bits.astype(np.uint32).view(np.float32).reshape(f.shape)
+
+
+def round_to(a, dtype: str) -> np.ndarray:
+    """``a`` rounded to the values of ``dtype`` (f32, f16 or bf16), in the
+    array type that holds them (``STORAGE``)."""
+    if dtype == "bf16":
+        return _to_bf16(a)
+    return np.asarray(a).astype(DTYPES[dtype])
 
 
 @dataclass(frozen=True)
@@ -77,10 +97,9 @@ class Inputs:
     extra: dict = field(default_factory=dict)
 
     def rounded(self, dtype: str) -> "Inputs":
-        """The same draw rounded to ``dtype`` (kept in that numpy dtype)."""
-        nd = DTYPES[dtype]
-        return Inputs(self.x.astype(nd), self.w.astype(nd),
-                      None if self.b is None else self.b.astype(nd), self.dy.astype(nd))
+        """The same draw rounded to ``dtype`` (held as ``STORAGE[dtype]``)."""
+        r = lambda a: round_to(a, dtype)
+        return Inputs(r(self.x), r(self.w), None if self.b is None else r(self.b), r(self.dy))
 
 
 def draw(T: int, Cin: int, Cout: int, N: int, bias: bool, seed: int) -> Inputs:

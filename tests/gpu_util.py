@@ -8,12 +8,14 @@ import numpy as np
 
 import synth
 
-TOL = {"f32": 1e-5, "f16": 5e-3}   # max|gpu - ref| / max|ref|, per output tensor
+# max|gpu - ref| / max|ref|, per output tensor.  bf16 (unit roundoff 2^-8)
+# takes the fp16 bar (unit roundoff 2^-11) scaled by the ratio, 8.
+TOL = {"f32": 1e-5, "f16": 5e-3, "bf16": 4e-2}
 
 
 def torch_dtype(dt):
     import torch
-    return {"f32": torch.float32, "f16": torch.float16}[dt]
+    return {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
 
 
 def rel_err(gpu, ref):
@@ -34,8 +36,11 @@ def say(*a):
 
 
 def to_dev(a, dt):
+    """``a`` rounded to dt on the GPU (bf16: the float32-held bf16 values,
+    converted exactly)."""
     import torch
-    return torch.from_numpy(np.ascontiguousarray(a.astype(synth.DTYPES[dt]))).to("cuda")
+    t = torch.from_numpy(np.ascontiguousarray(synth.round_to(a, dt))).to("cuda")
+    return t.to(torch.bfloat16) if dt == "bf16" else t
 
 
 def run_gpu(inp: synth.Inputs, dt: str, want=("y", "dx", "dw")):

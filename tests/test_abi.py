@@ -60,7 +60,10 @@ def test_weight_spectrum_bytes(lib):
     # T real planes, two padded layouts (rows to whole output-channel chunks, columns to 32)
     assert L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_F16) == 8 * (384 * 96 + 96 * 384) * 2
     assert L.eqlinear_weight_spectrum_bytes(4, 16, 16, L.EQL_F32) == 4 * (32 * 32 * 2) * 4
-    for bad in [(0, 4, 4, 0), (17, 4, 4, 0), (4, 0, 4, 0), (4, 4, 0, 0), (4, 4, 4, 2),
+    # bf16 shares every shape and layout of fp16
+    assert L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_BF16) == \
+        L.eqlinear_weight_spectrum_bytes(8, 96, 384, L.EQL_F16)
+    for bad in [(0, 4, 4, 0), (17, 4, 4, 0), (4, 0, 4, 0), (4, 4, 0, 0), (4, 4, 4, 3), (4, 4, 4, -1),
                 (4, 65537, 4, 0)]:
         assert L.eqlinear_weight_spectrum_bytes(*bad) == 0, bad
 
@@ -71,6 +74,8 @@ def test_workspace_bytes(lib):
     assert a > 0 and a % 256 == 0
     assert L.eqlinear_backward_weight_workspace_bytes(-1, 8, 96, 384, L.EQL_F16) == 0
     assert L.eqlinear_backward_weight_workspace_bytes(10, 17, 4, 4, L.EQL_F16) == 0
+    assert L.eqlinear_backward_weight_workspace_bytes(12608, 8, 96, 384, L.EQL_BF16) > 0
+    assert L.eqlinear_backward_weight_workspace_bytes(12608, 8, 96, 384, 3) == 0
 
 
 A = 0x10000000  # fake, 16-byte aligned device addresses: never dereferenced on these paths
@@ -185,6 +190,10 @@ def test_whole_backward_plan_and_workspace(lib):
     assert L.eqlinear_backward_workspace_bytes(401408, 4, 24, 96, L.EQL_F16) == \
         256 * 4 * 32 * 128 * 4 + 256 * 128 * 4
     assert L.eqlinear_backward_workspace_bytes(0, 4, 24, 96, L.EQL_F16) == 0
+    # bf16 always runs the two passes
+    assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_BF16) == 0
+    assert L.eqlinear_backward_workspace_bytes(401408, 4, 24, 96, L.EQL_BF16) == \
+        L.eqlinear_backward_weight_workspace_bytes(401408, 4, 24, 96, L.EQL_BF16)
 
 
 def test_whole_backward_forced_plan(lib, monkeypatch):
@@ -194,6 +203,7 @@ def test_whole_backward_forced_plan(lib, monkeypatch):
     assert L.eqlinear_backward_is_fused(100, 11, 13, 21, L.EQL_F32) == 1
     assert L.eqlinear_backward_is_fused(100, 11, 13, 21, L.EQL_F16) == 0   # no fp16 variant at T = 11
     assert L.eqlinear_backward_is_fused(100, 8, 96, 384, L.EQL_F16) == 0     # no variant holds it
+    assert L.eqlinear_backward_is_fused(100, 4, 24, 96, L.EQL_BF16) == 0     # never for bf16
     monkeypatch.setenv("EQL_BWD_FUSED", "0")
     assert L.eqlinear_backward_is_fused(401408, 4, 24, 96, L.EQL_F16) == 0
 

@@ -67,7 +67,7 @@ def test_forward_refuses_bad_out():
 def test_forward_refuses_wrong_activation_shape_and_dtype():
     with pytest.raises(ValueError, match="x must be"):
         ops.forward(torch.zeros(N, CIN + 1, T, dtype=torch.float16), spec(), None, T, CIN, COUT)
-    with pytest.raises(TypeError, match="float32 and float16"):
+    with pytest.raises(TypeError, match="float32, float16 and bfloat16"):
         ops.forward(torch.zeros(N, CIN, T, dtype=torch.float64), spec(), None, T, CIN, COUT)
 
 

@@ -34,7 +34,7 @@ extern "C" void run(int T, int fwd, const float* in, float* out, int n) {
 def txlib():
     src = open(HDR).read()
     a = src.index("namespace eqk {")
-    b = src.index("// ---------------------------------------------------------------------------\n// Element types.")
+    b = src.index("// ---------------------------------------------------------------------------\n// Element types")
     body = (src[a:b].replace("__host__ __device__ __forceinline__", "inline")
             .replace("__device__ __forceinline__", "inline") + "}\n")
     d = tempfile.mkdtemp()
@@ -134,7 +134,7 @@ extern "C" void run_h2(int T, const double* lo, const double* hi, double* plo, d
 def h2lib():
     src = open(HDR).read()
     a = src.index("namespace eqk {")
-    b = src.index("// ---------------------------------------------------------------------------\n// Element types.")
+    b = src.index("// ---------------------------------------------------------------------------\n// Element types")
     body = (src[a:b].replace("__host__ __device__ __forceinline__", "inline")
             .replace("__device__ __forceinline__", "inline") + "}\n")
     d = tempfile.mkdtemp()
