@@ -39,7 +39,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=None, help="layer name from synth.LAYERS")
-    ap.add_argument("--dtype", default=None, choices=["f32", "f16"])
+    ap.add_argument("--dtype", default=None, choices=["f32", "f16", "bf16"])
     ap.add_argument("--rotate", type=int, default=4, help="input sets used in turn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=0,
@@ -117,11 +117,12 @@ class Workload:
         import synth
         from paper_2607_21271_amd import ops
         self.layer, self.dt, self.ops = layer, dt, ops
-        tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+        tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
         l = layer
         inp = synth.draw_layer(l).rounded(dt)
         self.inp = inp
-        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda")
+        # bf16 values arrive held in float32 and convert exactly
+        dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(tdt)
         self.w = dev(inp.w)
         self.b = dev(inp.b) if inp.b is not None else None
         x0, dy0 = dev(inp.x), dev(inp.dy)
@@ -440,12 +441,12 @@ def run_tables(args):
     from paper_2607_21271_amd import roofline as rf
     T, N = 4, 32768
     runs = args.tables_runs
-    for dt in ("f32", "f16"):
-        tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+    for dt in ("f32", "f16", "bf16"):
+        tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
         for c in [int(v) for v in args.tables_c.split(",")]:
             torch.cuda.empty_cache()
             inp = synth.draw(T, c, c, N, True, 6000 + c).rounded(dt)
-            dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda()
+            dev = lambda a: torch.from_numpy(np.ascontiguousarray(a)).cuda().to(tdt)
             x, w, b, dy = dev(inp.x), dev(inp.w), dev(inp.b), dev(inp.dy)
             rec = {"table": "operator", "dtype": dt, "c": c, "T": T, "rows": N, "runs": runs}
             print("tables: %s c=%d" % (dt, c), file=sys.stderr, flush=True)
@@ -751,6 +752,10 @@ def run_gconv(args):
             del f, psi, bias, gy, fg, pg, bg, xn, gyn, Wd, xr, pr, br, w_ct, wspec
 
 
+# bf16 runs of the headline and Swin stage-1 shapes, reported beside the rest
+EXTRA_DTYPES = {"vit_b_mlp_up": ("bf16",), "swin_s1": ("bf16",)}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -790,7 +795,7 @@ def main():
         a2.steps, a2.warmup = min(args.steps, 30), min(args.warmup, 5)
         others = {}
         for n2, l2 in synth.LAYERS.items():
-            for d2 in l2.dtypes:
+            for d2 in l2.dtypes + EXTRA_DTYPES.get(n2, ()):
                 if (n2, d2) == (name, dt):
                     continue
                 print("bench: %s %s" % (n2, d2), file=sys.stderr, flush=True)

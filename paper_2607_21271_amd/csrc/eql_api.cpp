@@ -136,12 +136,12 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16
 // 32768 rows, whole backward: 1.8 vs 2.7 ms at 512 fp32, 28 vs 121 ms at
 // 2048 fp32, 7.6 vs 26.8 ms at 2048 fp16), level at 96 x 384 and 256 x 256,
 // and slower on Swin stage 1 (24 x 96: 120 vs 79 us) and the 64 x 64 sweep.
-// bf16 always takes the staged kernel, whose bias sum reads the fp32 bin 0.
+// bf16 plans as fp16 (same shapes and tiles).
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt) {
   const bool w16 = dt != kF32;  // 16-bit elements: same shapes for fp16 and bf16
   const int forced = wgrad_forced_kind();
   const int lo = Cin < Cout ? Cin : Cout, hi = Cin < Cout ? Cout : Cin;
-  if (dt != kBF16 && (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512))))
+  if (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512)))
     return wgrad_plan_rd(N, T, Cin, Cout, w16);
   return wgrad_plan_staged(N, T, Cin, Cout, w16);
 }

@@ -237,7 +237,7 @@ template <int T, int DT>
 hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
   if (p.kind == 1) {
 #define EQK_RD(C_, O_)                                             \
-  if constexpr (DT != kBF16 && rd_fits(T, C_, O_)) {              \
+  if constexpr (rd_fits(T, C_, O_)) {                              \
     if (p.ct == (C_) && p.otw == (O_)) return wgrad_rd_variant<T, DT, C_, O_>(a, p); \
   }
     EQK_RD(1, 1)

@@ -60,10 +60,8 @@ __global__ __launch_bounds__(64 * NW) void eql_wgrad_rd_kernel(
     const void* __restrict__ x, const void* __restrict__ dy, float* __restrict__ part,
     float* __restrict__ dbpart, int64_t N, int Cin, int Cout, int64_t rows_per_split, int n_ct,
     int n_ot, int n_splits, int Cin_pad, int Cout_pad) {
-  // fp32 and fp16 only: the bias sum of this kernel reads the rounded bin-0
-  // operands, too coarse in bf16 (the staged kernel serves bf16)
-  static_assert(DT != kBF16, "register-direct weight gradient: fp32 or fp16");
   constexpr bool F16 = DT == kF16;
+  constexpr bool W16 = DT != kF32;
   using S = RdShape<T, DT, CT, OT>;
   using Bn = Bins<T>;
   constexpr int EB = S::EB, KR = S::KR, RPL = S::RPL, WPR = S::WPR, RAW = S::RAW;
@@ -149,9 +147,23 @@ __global__ __launch_bounds__(64 * NW) void eql_wgrad_rd_kernel(
 #pragma unroll
   for (int b = 0; b < OT; ++b) dbacc[b] = 0.0f;
 
-  // Transform one block of the chunk into its T operand planes.
-  auto transform = [&](int bl, u32x4 (&op)[T]) __attribute__((always_inline)) {
-    if constexpr (F16) {
+  // Transform one block of the chunk into its T operand planes.  bf16: fp32
+  // transforms, each plane value rounded once; the block's fp32 bin 0 is
+  // added to dbs (output-gradient blocks pass their bias sum, others a dummy).
+  auto transform = [&](int bl, u32x4 (&op)[T], float& dbs) __attribute__((always_inline)) {
+    if constexpr (DT == kBF16) {
+#pragma unroll
+      for (int m = 0; m < RPL / 2; ++m) {
+        uint32_t two[2 * WPR];
+#pragma unroll
+        for (int q = 0; q < 2 * WPR; ++q) two[q] = raw[bl][2 * m * WPR + q];
+        float P0[T], P1[T];
+        transform_pair_f32<T>(two, P0, P1);
+        dbs += P0[0] + P1[0];
+#pragma unroll
+        for (int p = 0; p < T; ++p) op[p][m] = pack2<DT>(P0[p], P1[p]);
+      }
+    } else if constexpr (F16) {
 #pragma unroll
       for (int m = 0; m < RPL / 2; ++m) {
         uint32_t two[2 * WPR];
@@ -178,6 +190,10 @@ __global__ __launch_bounds__(64 * NW) void eql_wgrad_rd_kernel(
     if constexpr (F16) {
       d = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8, A),
                                                  __builtin_bit_cast(half8, B), d, 0, 0, 0);
+    } else if constexpr (DT == kBF16) {
+      typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+      d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, A),
+                                                  __builtin_bit_cast(bf16x8, B), d, 0, 0, 0);
     } else {
       // (elements copied to scalars first: __builtin_bit_cast of a vector
       // element expression read element 0 whatever the index)
@@ -198,28 +214,32 @@ __global__ __launch_bounds__(64 * NW) void eql_wgrad_rd_kernel(
     u32x4 opd[OT][T];
 #pragma unroll
     for (int b = 0; b < OT; ++b) {
-      transform(CT + b, opd[b]);
+      transform(CT + b, opd[b], dbacc[b]);
       issue_block(CT + b, next_chunk);
       // keep the loads here: sunk below the MFMAs they would leave only the
       // MFMA time to cover their latency
       __builtin_amdgcn_sched_barrier(0);
-      // bias gradient: bin 0 of the output-gradient rows
+      // bias gradient: bin 0 of the output-gradient rows (bf16: summed in the
+      // transform, from fp32)
       // (vector elements are copied to scalars before a bit cast, see mma)
+      if constexpr (DT != kBF16) {
 #pragma unroll
-      for (int m = 0; m < 4; ++m) {
-        const uint32_t w0 = opd[b][0][m];
-        if constexpr (F16)
-          dbacc[b] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, w0),
-                                            half2v{(_Float16)1.0f, (_Float16)1.0f}, dbacc[b], false);
-        else
-          dbacc[b] += __builtin_bit_cast(float, w0);
+        for (int m = 0; m < 4; ++m) {
+          const uint32_t w0 = opd[b][0][m];
+          if constexpr (F16)
+            dbacc[b] = __builtin_amdgcn_fdot2(__builtin_bit_cast(half2v, w0),
+                                              half2v{(_Float16)1.0f, (_Float16)1.0f}, dbacc[b], false);
+          else
+            dbacc[b] += __builtin_bit_cast(float, w0);
+        }
       }
     }
-    constexpr uint32_t kSign = F16 ? 0x80008000u : 0x80000000u;
+    constexpr uint32_t kSign = W16 ? 0x80008000u : 0x80000000u;
 #pragma unroll
     for (int a = 0; a < CT; ++a) {
       u32x4 X[T];
-      transform(a, X);
+      float unused = 0.0f;  // activation blocks add nothing to the bias
+      transform(a, X, unused);
       issue_block(a, next_chunk);
       __builtin_amdgcn_sched_barrier(0);
       // -Xi of every complex bin (sign bits)

@@ -13,9 +13,9 @@ MI355X peaks are the vendor's published dense figures.
 from __future__ import annotations
 
 PEAK_HBM_GBS = 8000.0          # HBM3E, GB/s
-PEAK_MFMA_TFLOPS = {"f16": 2516.6, "f32": 157.3}   # dense matrix peaks, TFLOP/s
+PEAK_MFMA_TFLOPS = {"f16": 2516.6, "bf16": 2516.6, "f32": 157.3}   # dense matrix peaks, TFLOP/s
 PEAK_FP32_VALU_TFLOPS = 157.3
-ELEM_BYTES = {"f32": 4, "f16": 2}
+ELEM_BYTES = {"f32": 4, "f16": 2, "bf16": 2}
 
 
 def bins(T: int):
