@@ -342,12 +342,42 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   // register sets of prefetched weight blocks: 2 when streamed (a block is
   // issued two steps before it is stored to LDS), NKR with a resident
   // spectrum (block (oc, kc) always uses set kc)
-  constexpr int NWS = RES ? (NKR > 1 ? NKR : 1) : 2;
-  u32x4 wr[NWS][UPT];
-  int goff[UPT];
-  int loff[UPT];
+  // Streamed weights whose blocks split into whole wave-loads of 64 x 16
+  // bytes go from global memory straight into LDS (buffer_load ... lds): no
+  // staging registers, no LDS store instructions.  Lane l of a wave-load
+  // writes LDS bytes [16 l, 16 l + 16) of the wave's 1 KB slice, so each lane
+  // loads the 16-byte chunk that the swizzled layout puts there.
+  constexpr int NWV = NTH / 64;
+  // (not at T = 4 and 8, where the EQ-ViT and EQ-Swin layers measured level
+  // per pass and 1-2% slower per training step with it)
+  constexpr bool DMA = MODE == kStream && NU % (64 * NWV) == 0 && T != 4 && T != 8;
+  // Operand reads of the next o-tile ahead of the current tile's MFMAs, where
+  // that measured faster (16-bit types at T = 3 and 16: 6-10% on the input
+  // gradient, and at T = 16 on the forward; at T = 5, 8 and 12 level or
+  // slower per pass, at T = 4 6% faster per forward pass but 2% slower per
+  // training step; with a resident spectrum the registers are not there).
+  constexpr bool PIPE = !RES && DT != kF32 && (T == 3 || T == 16);
+  constexpr int UPD = DMA ? NU / (64 * NWV) : 1;  // wave-loads per wave and block
+  int gdma[UPD];
+  if constexpr (DMA) {
 #pragma unroll
-  for (int u = 0; u < UPT; ++u) {
+    for (int u = 0; u < UPD; ++u) {
+      const int unit = (u * NWV + wave) * 64 + lane;  // LDS slot of the block
+      const int p = unit / (OC * RB / 16);
+      const int rem = unit - p * (OC * RB / 16);
+      const int row = rem / (RB / 16);
+      const int cs = rem - row * (RB / 16);
+      const int ch = cs ^ ((row >> 1) & (RB / 16 - 1));  // source chunk swizzled to slot cs
+      gdma[u] = (int)(p * wplane + (int64_t)row * Ci_pad * EB + ch * 16);
+    }
+  }
+  constexpr int NWS = DMA ? 1 : RES ? (NKR > 1 ? NKR : 1) : 2;
+  constexpr int UPTR = DMA ? 1 : UPT;  // staging registers per set
+  u32x4 wr[NWS][UPTR];
+  int goff[UPTR];
+  int loff[UPTR];
+#pragma unroll
+  for (int u = 0; u < UPTR; ++u) {
     const int unit = tid + NTH * u;
     const int p = unit / (OC * RB / 16);
     const int rem = unit - p * (OC * RB / 16);
@@ -365,15 +395,31 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     constexpr int S = decltype(set)::value;
     const int boff = (oc * OC * Ci_pad + kc * KSTEP) * EB;
 #pragma unroll
-    for (int u = 0; u < UPT; ++u)
+    for (int u = 0; u < UPTR; ++u)
       if (NU % NTH == 0 || tid + NTH * u < NU)
         wr[S][u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wrs, goff[u], boff, 0));
   };
   auto store_w = [&](auto set, int blk) __attribute__((always_inline)) {
     constexpr int S = decltype(set)::value;
 #pragma unroll
-    for (int u = 0; u < UPT; ++u)
+    for (int u = 0; u < UPTR; ++u)
       if (NU % NTH == 0 || tid + NTH * u < NU) *reinterpret_cast<u32x4*>(wlb + blk * WBLK + loff[u]) = wr[S][u];
+  };
+  // weight block (oc, kc) straight into LDS block blk (each wave its slices).
+  // The builtin exists for the device pass only (the host pass, which never
+  // runs kernel code, emits unusable IR for it when intermediate files are
+  // kept, as this build does for the post-build check).
+  auto dma_w = [&](int blk, int oc, int kc) __attribute__((always_inline)) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int boff = (oc * OC * Ci_pad + kc * KSTEP) * EB;
+#pragma unroll
+    for (int u = 0; u < UPD; ++u)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          wrs, (__attribute__((address_space(3))) void*)(wlb + blk * WBLK + (u * NWV + wave) * 1024), 16,
+          gdma[u], boff, 0, 0);
+#else
+    (void)blk; (void)oc; (void)kc;
+#endif
   };
 
   // ---- raw activations of (round m, step kc): HKW channels of this lane's row.
@@ -468,13 +514,10 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
         Xneg[k - 1] = frag_neg<DT, FB>(X[BWD ? Bn::re(k) : Bn::im(k)]);
       });
     }
-#pragma unroll
-    for (int a = 0; a < OT; ++a) {
-      const int ot = oh * OT + a;                 // o-tile within the chunk
-      if (oc * OC + ot * 16 >= Co) continue;      // uniform across the wave
-      FR W[T];
-#pragma unroll
-      for (int p = 0; p < T; ++p) W[p] = lds_frag<FB, RB>(wlb + blk * WBLK + p * OC * RB, ot * 16 + li, g);
+    // With PIPE the operand reads of tile a + 1 are issued before the MFMAs of
+    // tile a; otherwise each tile reads its operands just before its MFMAs.
+    // Tiles past Co skip their MFMAs.
+    auto tile_mma = [&](int a, const FR (&W)[T]) __attribute__((always_inline)) {
       frag_mma<DT, KW>(acc[0][a], X[0], W[0]);
       if constexpr (Bn::kEven) frag_mma<DT, KW>(acc[1][a], X[1], W[1]);
       static_for<Bn::K>([&](auto ki) {
@@ -503,6 +546,31 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
           frag_mma<DT, KW>(acc[i][a], Xneg[k - 1], W[i]);
         }
       });
+    };
+    if constexpr (PIPE) {
+      FR Wb[2][T];
+      auto load_w = [&](int a, FR (&W)[T]) __attribute__((always_inline)) {
+        const int ot = oh * OT + a;
+#pragma unroll
+        for (int p = 0; p < T; ++p) W[p] = lds_frag<FB, RB>(wlb + blk * WBLK + p * OC * RB, ot * 16 + li, g);
+      };
+      load_w(0, Wb[0]);
+#pragma unroll
+      for (int a = 0; a < OT; ++a) {
+        if (a + 1 < OT) load_w(a + 1, Wb[(a + 1) & 1]);
+        if (oc * OC + (oh * OT + a) * 16 >= Co) continue;  // uniform across the wave
+        tile_mma(a, Wb[a & 1]);
+      }
+    } else {
+#pragma unroll
+      for (int a = 0; a < OT; ++a) {
+        const int ot = oh * OT + a;                 // o-tile within the chunk
+        if (oc * OC + ot * 16 >= Co) continue;      // uniform across the wave
+        FR W[T];
+#pragma unroll
+        for (int p = 0; p < T; ++p) W[p] = lds_frag<FB, RB>(wlb + blk * WBLK + p * OC * RB, ot * 16 + li, g);
+        tile_mma(a, W);
+      }
     }
   };
 
@@ -681,10 +749,15 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
     // so each weight load has two steps to arrive.
     const int total = rounds * n_oc * nks;
     int s = 0, m = 0, oc = 0, kc = 0;
-    issue_w(I0{}, 0, 0);
-    issue_x(I0{}, 0, 0);
-    if (total > 1) issue_w(I1{}, nks > 1 ? 0 : (n_oc > 1 ? 1 : 0), nks > 1 ? 1 : 0);
-    store_w(I0{}, 0);
+    if constexpr (DMA) {
+      dma_w(0, 0, 0);
+      issue_x(I0{}, 0, 0);
+    } else {
+      issue_w(I0{}, 0, 0);
+      issue_x(I0{}, 0, 0);
+      if (total > 1) issue_w(I1{}, nks > 1 ? 0 : (n_oc > 1 ? 1 : 0), nks > 1 ? 1 : 0);
+      store_w(I0{}, 0);
+    }
     auto step = [&](auto par) __attribute__((always_inline)) {
       constexpr int P = decltype(par)::value;
       if (kc == 0) zero_acc();
@@ -693,12 +766,24 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
       int oc2 = oc1, kc2 = kc1 + 1;        // weight block of step s+2
       if (kc2 == nks) { kc2 = 0; if (++oc2 == n_oc) oc2 = 0; }
       publish_x(I0{}, P);
-      __syncthreads();
-      if (s + 2 < total) issue_w(par, oc2, kc2);
+      if constexpr (DMA) {
+        // W(s), loaded into LDS block P during step s-1, complete for this
+        // wave (vmcnt 0; the compiler does not track LDS-direct loads), then
+        // visible to all after the barrier, which also frees block 1 - P
+        // (read in step s-1) for W(s+1)
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+        dma_w(1 - P, oc1, kc1);  // past the last step: a valid block, never read
+      } else {
+        __syncthreads();
+        if (s + 2 < total) issue_w(par, oc2, kc2);
+      }
       issue_x(I0{}, m1, kc1);
       read_x(P, bcur);
       mma_step(oc, P, bcur);
-      if (s + 1 < total) store_w(std::integral_constant<int, 1 - P>{}, 1 - P);
+      if constexpr (!DMA) {
+        if (s + 1 < total) store_w(std::integral_constant<int, 1 - P>{}, 1 - P);
+      }
       if (kc == nks - 1) epilogue(m, oc);
       m = m1; oc = oc1; kc = kc1; ++s;
     };
