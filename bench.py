@@ -667,8 +667,9 @@ def run_gconv(args):
     [Cout*T, Cin*T, k, k] kernel Wd[(o,r),(c,s),a,b] = psi[R^-r (a,b)][(s-r) mod T][o][c]
     applied with torch's conv2d on NCHW features (its autograd folds the
     gradient back onto psi).  Forward = one layer call with the C_T weight and
-    spectrum precomputed (a frozen weight); training step = weight permutation,
-    spectrum, forward, backward.  Mean and median of ``--tables-runs`` runs."""
+    spectrum precomputed (a frozen weight), reading the patches straight from
+    the features where the channel count allows, else gather + layer call;
+    training step = weight permutation, spectrum, forward, backward.  Mean and median of ``--tables-runs`` runs."""
     import numpy as np
     import torch
     import torch.nn.functional as F
@@ -690,8 +691,8 @@ def run_gconv(args):
                         ra, rb = rot(-r, a, b)
                         idx[r, s_, a + h, b + h] = ((ra + h) * k + (rb + h)) * T + (s_ - r) % T
         idx_t = torch.from_numpy(idx).cuda()
-        for dt in ("f32", "f16"):
-            tdt = {"f32": torch.float32, "f16": torch.float16}[dt]
+        for dt in ("f32", "f16", "bf16"):
+            tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
             torch.cuda.empty_cache()
             print("gconv: %s %s" % (name, dt), file=sys.stderr, flush=True)
             rs = np.random.RandomState(8300 + Cin)
@@ -706,9 +707,17 @@ def run_gconv(args):
             w_ct = gconv.pack_weight(psi)
             wspec = ops.weight_spectrum(w_ct)
 
-            def flash_fwd():
+            def explicit_fwd():
                 xcol = gconv.gather(f, T, k)
                 return ops.forward(xcol, wspec, bias, T, k * k * Cin, Cout)
+            if gconv.implicit_ok(Cin):
+                def flash_fwd():
+                    return gconv.forward_implicit(f, wspec, bias, T, Cout, k)
+                rec["forward_kind"] = "implicit gather"
+                rec["explicit_fwd"] = _time_fn(explicit_fwd, runs)
+            else:
+                flash_fwd = explicit_fwd
+                rec["forward_kind"] = "gather + C_T forward"
             rec["flash_fwd"] = _time_fn(flash_fwd, runs)
             xcol = gconv.gather(f, T, k)
             rec["gather"] = _time_fn(lambda: gconv.gather(f, T, k), runs)

@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 6
+#define EQLINEAR_ABI_VERSION 7
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1, EQL_BF16 = 2 } eql_dtype_t;
@@ -242,6 +242,18 @@ int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int 
                                void* stream);
 int eqlinear_gconv_unpack_weight(const void* dw_ct, void* dpsi, int T, int Cin, int Cout, int k, int dtype,
                                  void* stream);
+
+/* The group convolution's forward pass without the patch buffer: y
+ * [B,H,W,Cout,T] = eqlinear_forward of the gathered patches (T, k*k*Cin ->
+ * Cout) with wspec the spectrum of eqlinear_gconv_pack_weight's w_ct and the
+ * optional bias [Cout], the forward kernel reading each patch straight from f
+ * [B,H,W,Cin,T] (Sec. 5's equivariant convolution on the method's kernels).
+ * Same arithmetic, bit for bit, as eqlinear_gconv_gather followed by
+ * eqlinear_forward.  Requires Cin a multiple of 4 and f below 2^31 bytes
+ * (else EQL_ERR_UNSUPPORTED); f, y and wspec 16-byte aligned; other checks as
+ * for eqlinear_forward and the gather.  B, H or W = 0 is a no-op. */
+int eqlinear_gconv_forward(const void* f, const void* wspec, const void* bias, void* y, int64_t B, int H, int W,
+                           int T, int Cin, int Cout, int k, int dtype, void* stream);
 
 /* eqlinear_backward_weight without a workspace argument, for callers that
  * cannot allocate device memory (code under HIP graph capture, serving loops,

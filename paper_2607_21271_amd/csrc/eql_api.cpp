@@ -801,6 +801,54 @@ int eqlinear_gconv_scatter(const void* dxcol, void* df, int64_t B, int H, int W,
   return gconv_common(1, dxcol, df, B, H, W, T, Cin, 1, k, dtype, stream);
 }
 
+int eqlinear_gconv_forward(const void* f, const void* wspec, const void* bias, void* y, int64_t B, int H, int W,
+                           int T, int Cin, int Cout, int k, int dtype, void* stream) {
+  int st = gconv_shape(T, Cin, Cout, k, dtype);
+  if (st) return st;
+  if ((st = gconv_image(B, H, W))) return st;
+  if (Cin % 4 != 0) return EQL_ERR_UNSUPPORTED;  // a lane's four gathered channels stay in one block
+  const int64_t N = B * H * W;
+  const int Ci = k * k * Cin;
+  if ((st = check_shape(N, T, Ci, Cout, dtype))) return st;
+  if (!wspec || (N > 0 && (!f || !y))) return EQL_ERR_INVALID_ARG;
+  const size_t e = elem_bytes(dtype);
+  if (!aligned(wspec, 16) || (f && !aligned(f, 16)) || (y && !aligned(y, 16)) || (bias && !aligned(bias, e)))
+    return EQL_ERR_ALIGNMENT;
+  const size_t fb = (size_t)N * Cin * T * e;
+  if (fb >= ((size_t)1 << 31)) return EQL_ERR_UNSUPPORTED;  // one 31-bit buffer range over the features
+  const Range r[4] = {{f, fb},
+                      {y, (size_t)N * Cout * T * e},
+                      {wspec, eqlinear_weight_spectrum_bytes(T, Ci, Cout, dtype)},
+                      {bias, bias ? (size_t)Cout * e : 0}};
+  if (any_overlap(r, 4)) return EQL_ERR_INVALID_ARG;
+  if ((st = check_device())) return st;
+  if (N == 0) return EQL_OK;
+  const bool w16 = dtype != EQL_F32;
+  eqk::GemmArgs a{};
+  a.in = f;
+  a.wsp = wspec;
+  a.bias = bias;
+  a.out = y;
+  a.N = N;
+  a.Ci = Ci;
+  a.Co = Cout;
+  a.Ci_pad = eqk::wspec_dims(T, Ci, Cout, w16).CiF;
+  a.stream = (hipStream_t)stream;
+  {
+    const unsigned od = T == 4 ? (unsigned)(k / 2 + 1) : (unsigned)k;
+    a.geo = eqk::GatherGeom{H, W, Cin, k, eqk::div_magic(W), eqk::div_magic(H), eqk::div_magic(Cin * T),
+                            eqk::div_magic(od)};
+  }
+  a.plan = eqk::gemm_plan(T, Ci, Cout, w16);
+  eqk::gemm_plan_rows(a.plan, N, T, w16, eqk::device_cu_count());
+  if (a.plan.narrow) return EQL_ERR_UNSUPPORTED;
+  if (a.plan.mode == 1) {  // the gathered rows are not kept resident: stream the weights
+    a.plan.mode = 0;
+    a.plan.lds_bytes = eqk::gemm_lds_c(T, w16, a.plan.OT, eqk::gemm_wblocks(0, a.plan.n_oc, a.plan.n_ks));
+  }
+  return launched(eqk::launch_gemm_gather(dtype, T, a));
+}
+
 int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int Cout, int k, int dtype,
                                void* stream) {
   return gconv_common(2, psi, w_ct, 0, 0, 0, T, Cin, Cout, k, dtype, stream);

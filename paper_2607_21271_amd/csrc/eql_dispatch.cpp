@@ -36,6 +36,10 @@ hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a) {
   return by_type(dt, T, [&](auto inst) { return decltype(inst)::gemm(bwd, a); });
 }
 
+hipError_t launch_gemm_gather(int dt, int T, const GemmArgs& a) {
+  return by_type(dt, T, [&](auto inst) { return decltype(inst)::gemm_gather(a); });
+}
+
 hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p) {
   return by_type(dt, T, [&](auto inst) { return decltype(inst)::wgrad(a, p); });
 }

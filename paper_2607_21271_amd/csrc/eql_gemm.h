@@ -216,6 +216,54 @@ __device__ __forceinline__ void mask_raw(int nvalid_elems, uint32_t (&r)[NB / 4]
   }
 }
 
+// Implicit patch gather (group convolution): a lane's raw words hold T
+// vectors, vector j being the HKW elements vec_j[cc*T + s] = f[pixel + R^j d0,
+// c + cc, s] of one window orbit (M = HKW / T input channels c + cc, every
+// group position s).  The gathered channel (cc, u) at group position j is
+// vec_j[cc*T + (u + j) mod T] (the shear u = s - j); this rewrites the words
+// into the plain order, element (cc*T + u)*T + j.  The centre of the window is
+// already in plain order (keep).
+template <int T, int HKW, int EB>
+__device__ __forceinline__ void gather_shear(uint32_t (&r)[HKW * T * EB / 4], bool keep) {
+  constexpr int NW = HKW * T * EB / 4;
+  // source element of plain element i = (cc*T + u)*T + j
+  constexpr auto src = [](int i) {
+    const int j = i % T, u = (i / T) % T, cc = i / (T * T);
+    return j * HKW + cc * T + (u + j) % T;
+  };
+  // every index below is a compile-time constant: the sheared words are
+  // built into their own array and the lane's choice applied per word (a
+  // per-element choice of source index became a runtime-indexed array)
+  uint32_t o[NW];
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    if constexpr (EB == 4) {
+      o[w] = r[src(w)];
+    } else {
+      const int s0 = src(2 * w), s1 = src(2 * w + 1);
+      const uint32_t lo = (r[s0 / 2] >> (16 * (s0 % 2))) & 0xffffu;
+      const uint32_t hi = (r[s1 / 2] >> (16 * (s1 % 2))) & 0xffffu;
+      o[w] = lo | (hi << 16);
+    }
+  }
+  const uint32_t km = keep ? 0xffffffffu : 0u;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) r[w] = (r[w] & km) | (o[w] & ~km);
+}
+
+// n / d and n mod d for n < 2^31 and a launch-constant divisor d with its
+// multiplier m = floor(2^32 / d) (2^32 - 1 for d = 1): the product estimate
+// is exact or one low
+__device__ __forceinline__ uint32_t gather_div(uint32_t n, uint32_t d, uint32_t m, uint32_t& r) {
+  uint32_t q = __umulhi(n, m);
+  r = n - q * d;
+  if (r >= d) {
+    ++q;
+    r -= d;
+  }
+  return q;
+}
+
 // Transform the HKW channels held raw by one lane; P[p][j] is plane p of channel j.
 template <int T, int DT, int HKW>
 __device__ __forceinline__ void raw_to_planes(const uint32_t (&r)[HKW * T * (DT != kF32 ? 2 : 4) / 4],
@@ -284,13 +332,18 @@ struct GemmLds {
 // barrier both waves read complete MFMA operands from it.  Weight blocks are
 // double buffered in LDS: the next block is loaded into registers while the
 // current one feeds the MFMAs, then written to the idle buffer.
-template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW>
+//
+// GATHER (forward of the group convolution, T in {1, 2, 4}): `in` is the feature map
+// f [N pixels, geo.Cin, T] and row n of the layer's input is the gathered
+// patch row of pixel n (k*k*Cin channels: window orbits, then the centre),
+// read straight from f instead of a materialised patch buffer.
+template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW, bool GATHER>
 __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __restrict__ in,
                                                        const void* __restrict__ wsp,
                                                        const void* __restrict__ bias,
                                                        void* __restrict__ out, int64_t N, int Ci,
                                                        int Co, int Ci_pad, int Co_pad, int n_oc,
-                                                       int n_ks) {
+                                                       int n_ks, GatherGeom geo) {
   using S = GemmShape<T, DT>;
   using Bn = Bins<T>;
   using FR = Frag<S::FB>;
@@ -310,6 +363,8 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   constexpr int UPT = (NU + NTH - 1) / NTH; // weight units per thread
   constexpr int XBLK = GemmLds<T, DT, OT>::XBLK;  // bytes of one spectrum buffer
   static_assert(KW >= 2, "contraction split");
+  static_assert(!GATHER || (!BWD && !NARROW && (T == 1 || T == 2 || T == 4) && HKW % T == 0),
+                "implicit gather: forward, T in {1, 2, 4}");
 
   // dynamic LDS: xl[2][XBLK], then the weight blocks (2 streamed, 2 * NKR with a
   // resident spectrum, n_oc * n_ks resident)
@@ -334,7 +389,9 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   const char* xin = reinterpret_cast<const char*>(in);
   const int rowb = Ci * T * EB;
   constexpr int LW = NARROW ? EB : S::WV;  // load width; the host checks rowb % LW == 0
-  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(xin + r0 * rowb, (uint32_t)(len * rowb));
+  // rows of this workgroup (GATHER: the whole feature map, below 2^31 bytes)
+  const __amdgpu_buffer_rsrc_t xrs =
+      GATHER ? make_rsrc(xin, (uint32_t)(N * geo.Cin * T * EB)) : make_rsrc(xin + r0 * rowb, (uint32_t)(len * rowb));
   if (rounds == 0) return;
 
   // ---- weight block (oc, kc): global -> registers -> LDS buffer.  Per-thread
@@ -431,18 +488,90 @@ __global__ __launch_bounds__(kGemmThreads) void eql_gemm_kernel(const void* __re
   constexpr int NXS = RES ? NKR : 1;
   uint32_t xr[NXS][NBH / 4];
   int xr_valid[NXS];  // valid elements per set (the rest belong to the next row)
+  bool xr_plain[NXS];  // GATHER: the words are already in plain order (window centre)
   auto issue_x = [&](auto set, int m, int kc) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
     const int q = m * kGemmRoundRows + kGemmPairs * li + rg;
     const int c0 = oh * (KSTEP / 2) + g * HKW;  // channel within the step
-    const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
     const int cabs = kc * KSTEP + c0;
-    xr_valid[X] = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
-    load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr[X]);
+    if constexpr (GATHER) {
+      // T loads of HKW elements each: the lane's gathered channels are M =
+      // HKW / T input channels c.. of one window orbit O (all T sheared
+      // positions), or HKW channels of the centre.  The host keeps Cin a
+      // multiple of HKW, so a lane never straddles two blocks.  Pixels outside
+      // the image, rows past the workgroup's and channels past k*k*Cin read
+      // zero (dropped offsets).  Divisions by launch constants are multiplies
+      // (GatherGeom), offsets 32-bit (the feature map is below 2^31 bytes).
+      constexpr int VB = HKW * EB;  // bytes per vector
+      const uint32_t CT = (uint32_t)geo.Cin * T;
+      const uint32_t p = (uint32_t)(r0 + q);
+      const bool row_ok = q < len && cabs < Ci;
+      uint32_t x, y, rem;
+      const uint32_t py = gather_div(p, (uint32_t)geo.W, geo.mW, x);
+      gather_div(py, (uint32_t)geo.H, geo.mH, y);
+      uint32_t cr;
+      const uint32_t O = gather_div((uint32_t)cabs, CT, geo.mCT, cr);
+      const int h = geo.k >> 1;
+      const bool centre = (int)O >= (geo.k * geo.k - 1) / T;  // past the last orbit block
+      // orbit base point (a0, b0)
+      int a0, b0;
+      if constexpr (T == 4) {
+        const uint32_t qa = gather_div(O, (uint32_t)(h + 1), geo.mO, rem);
+        a0 = 1 + (int)qa;
+        b0 = (int)rem;
+      } else if constexpr (T == 2) {
+        const uint32_t qa = gather_div(O, (uint32_t)geo.k, geo.mO, rem);
+        const bool upper = (int)qa < h;
+        a0 = upper ? 1 + (int)qa : 0;
+        b0 = upper ? (int)rem - h : 1 + (int)rem;
+      } else {
+        const uint32_t idx = O + (O >= (uint32_t)((geo.k * geo.k - 1) / 2) ? 1u : 0u);
+        const uint32_t qa = gather_div(idx, (uint32_t)geo.k, geo.mO, rem);
+        a0 = (int)qa - h;
+        b0 = (int)rem - h;
+      }
+      if (centre) { a0 = 0; b0 = 0; }
+      // byte offset of the lane's first channel in a pixel row: orbit lanes
+      // read channel c = cr / T of T pixels, centre lanes T consecutive
+      // vectors of their own pixel
+      const uint32_t coff = centre ? ((uint32_t)cabs - O * CT) * T * EB : (cr / T) * T * EB;
+      const uint32_t rowf = CT * EB;
+      xr_valid[X] = HKW * T;
+      xr_plain[X] = centre;
+      static_for<T>([&](auto ji) {
+        constexpr int j = decltype(ji)::value;
+        // R^j (a0, b0): R(a, b) = (-b, a) at T = 4, (-a, -b) at T = 2
+        int a = a0, b = b0;
+        if constexpr (T == 4) {
+          if constexpr (j == 1) { a = -b0; b = a0; }
+          if constexpr (j == 2) { a = -a0; b = -b0; }
+          if constexpr (j == 3) { a = b0; b = -a0; }
+        } else if constexpr (T == 2) {
+          if constexpr (j == 1) { a = -a0; b = -b0; }
+        }
+        const bool in_img = (uint32_t)((int)y + a) < (uint32_t)geo.H && (uint32_t)((int)x + b) < (uint32_t)geo.W;
+        const uint32_t pix = p + (uint32_t)(a * geo.W + b);
+        const uint32_t off = (row_ok && in_img) ? pix * rowf + coff + (centre ? (uint32_t)(j * VB) : 0u)
+                                                : kDropOffset;
+        if constexpr (VB == 16) {
+          const u32x4 v = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
+          xr[X][4 * j] = v[0]; xr[X][4 * j + 1] = v[1]; xr[X][4 * j + 2] = v[2]; xr[X][4 * j + 3] = v[3];
+        } else {
+          static_assert(VB == 8, "gather vector");
+          const u32x2 v = __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(xrs, off, 0, 0));
+          xr[X][2 * j] = v[0]; xr[X][2 * j + 1] = v[1];
+        }
+      });
+    } else {
+      const uint32_t voff = (uint32_t)(((int64_t)q * Ci + c0) * T * EB);
+      xr_valid[X] = (Ci - cabs >= HKW) ? HKW * T : (Ci - cabs > 0 ? (Ci - cabs) * T : 0);
+      load_raw<NBH, LW>(xrs, voff, kc * KSTEP * T * EB, xr[X]);
+    }
   };
   // transform and publish this lane's part of the step's operand spectrum
   auto publish_x = [&](auto set, int xb) __attribute__((always_inline)) {
     constexpr int X = decltype(set)::value;
+    if constexpr (GATHER) gather_shear<T, HKW, EB>(xr[X], xr_plain[X]);
     mask_raw<NBH, EB>(xr_valid[X], xr[X]);
     const int byte = (oh * (KSTEP / 2) + g * HKW) * EB;
     if constexpr (DT != kF32) {

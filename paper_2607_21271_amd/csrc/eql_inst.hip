@@ -20,6 +20,11 @@ hipError_t Inst<T, DT>::gemm(bool bwd, const GemmArgs& a) {
 }
 
 template <int T, int DT>
+hipError_t Inst<T, DT>::gemm_gather(const GemmArgs& a) {
+  return gemm_gather_t<T, DT>(a);
+}
+
+template <int T, int DT>
 hipError_t Inst<T, DT>::wgrad(const WgradArgs& a, const WgradPlan& p) {
   return wgrad_t<T, DT>(a, p);
 }

@@ -240,6 +240,7 @@ struct GemmArgs {
   int Ci, Co, Ci_pad;
   GemmPlan plan;
   hipStream_t stream;
+  GatherGeom geo;    // implicit patch gather only (else zero)
 };
 
 struct WgradArgs {
@@ -274,6 +275,7 @@ template <int T, int DT>
 struct Inst {
   static hipError_t wspec(const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
   static hipError_t gemm(bool bwd, const GemmArgs& a);
+  static hipError_t gemm_gather(const GemmArgs& a);
   static hipError_t wgrad(const WgradArgs& a, const WgradPlan& p);
   static hipError_t bwd_fused(const FusedArgs& a, const FusedPlan& p);
 };
@@ -281,6 +283,7 @@ struct Inst {
 // Dispatch over T and the element type code dt (eql_dispatch.cpp).
 hipError_t launch_wspec(int dt, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
 hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a);
+hipError_t launch_gemm_gather(int dt, int T, const GemmArgs& a);
 hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p);
 hipError_t launch_bwd_fused(int dt, int T, const FusedArgs& a, const FusedPlan& p);
 

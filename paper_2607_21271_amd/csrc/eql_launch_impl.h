@@ -61,10 +61,10 @@ inline int persistent_grid(const void* kernel, int threads, int lds, int64_t N, 
   return (int)g;
 }
 
-template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW = false>
+template <int T, int DT, bool BWD, int OT, int MODE, int NKR, bool NARROW = false, bool GATHER = false>
 hipError_t gemm_variant(const GemmArgs& a) {
   static_assert(GemmShape<T, DT>::WV == gemm_wide_load_c(T, DT != kF32), "host and kernel load widths");
-  auto k = eql_gemm_kernel<T, DT, BWD, OT, MODE, NKR, NARROW>;
+  auto k = eql_gemm_kernel<T, DT, BWD, OT, MODE, NKR, NARROW, GATHER>;
   const int lds = a.plan.lds_bytes;
   if (lds != gemm_lds_c(T, DT != kF32, OT, gemm_wblocks(MODE, a.plan.n_oc, a.plan.n_ks)) || lds > kLdsBytes ||
       (MODE == kRes && a.plan.n_ks != NKR))
@@ -77,20 +77,33 @@ hipError_t gemm_variant(const GemmArgs& a) {
   const int grid = persistent_grid((const void*)k, kGemmThreads, lds, a.N,
                                    (int64_t)(a.Ci > a.Co ? a.Ci : a.Co) * T * (DT != kF32 ? 2 : 4));
   hipLaunchKernelGGL(k, dim3((unsigned)grid), dim3(kGemmThreads), lds, a.stream, a.in, a.wsp, a.bias, a.out,
-                     a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks);
+                     a.N, a.Ci, a.Co, a.Ci_pad, a.plan.Co_pad, a.plan.n_oc, a.plan.n_ks, a.geo);
   return hipGetLastError();
 }
 
-template <int T, int DT, bool BWD, int MODE>
+template <int T, int DT, bool BWD, int MODE, bool GATHER = false>
 hipError_t gemm_ot(const GemmArgs& a) {
   hipError_t r = hipErrorInvalidValue;
   static_for<8>([&](auto oi) {
     constexpr int OT = decltype(oi)::value + 1;
     if constexpr (gemm_ot_inst(T, DT != kF32, OT)) {
-      if (a.plan.OT == OT) r = gemm_variant<T, DT, BWD, OT, MODE, 0>(a);
+      if (a.plan.OT == OT) r = gemm_variant<T, DT, BWD, OT, MODE, 0, false, GATHER>(a);
     }
   });
   return r;
+}
+
+// Forward with the implicit patch gather (group convolution, T in {1, 2,
+// 4}): the plan's mode is streamed or resident weights, never narrow loads.
+template <int T, int DT>
+hipError_t gemm_gather_t(const GemmArgs& a) {
+  if constexpr (T == 1 || T == 2 || T == 4) {
+    const GemmPlan& p = a.plan;
+    if (p.narrow) return hipErrorInvalidValue;
+    if (p.mode == kStat) return gemm_ot<T, DT, false, kStat, true>(a);
+    if (p.mode == kStream) return gemm_ot<T, DT, false, kStream, true>(a);
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int T, int DT, bool BWD>

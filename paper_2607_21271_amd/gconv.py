@@ -13,7 +13,10 @@ C_T layer with k*k*Cin input channels on gathered patches
 (``eqlinear_gconv_gather``) with a permuted weight
 (``eqlinear_gconv_pack_weight``); the forward pass and the gradients run on
 the C_T kernels, and ``eqlinear_gconv_scatter`` / ``eqlinear_gconv_unpack_weight``
-take the gradients back.  This module only allocates and marshals.
+take the gradients back.  Where Cin is a multiple of 4 the forward kernel
+reads the patches straight from f (``eqlinear_gconv_forward``) and no patch
+buffer is formed unless the weight gradient needs one.  This module only
+allocates and marshals.
 """
 from __future__ import annotations
 
@@ -83,6 +86,32 @@ def unpack_weight_grad(dw_ct: torch.Tensor, k: int, stream=None) -> torch.Tensor
     return dpsi
 
 
+def forward_implicit(f: torch.Tensor, wspec: torch.Tensor, bias, T: int, Cout: int, k: int, stream=None):
+    """y [B, H, W, Cout, T] with the forward kernel reading the patches straight
+    from f [B, H, W, Cin, T] (``eqlinear_gconv_forward``; needs Cin % 4 == 0);
+    bit for bit the result of gather followed by ``ops.forward``."""
+    Cin = f.shape[-2]
+    B, H, W = _dims(f, Cin, T)
+    ops._check_same_dtype(f, bias=bias)
+    f = f.contiguous()
+    dt = ops._dtype_code(f)
+    ops._check_wspec(wspec, T, k * k * Cin, Cout, f.dtype)
+    ops._check_dev(f, wspec, *([bias] if bias is not None else []))
+    if bias is not None:
+        ops._check_out("bias", bias, (Cout,), f.dtype)
+    y = torch.empty(B, H, W, Cout, T, dtype=f.dtype, device=f.device)
+    _lib.check(_lib.eqlinear_gconv_forward(ops._ptr(f), ops._ptr(wspec), ops._ptr(bias) if bias is not None else None,
+                                           ops._ptr(y), B, H, W, T, Cin, Cout, k, dt, ops._stream(stream)),
+               "eqlinear_gconv_forward")
+    return y
+
+
+def implicit_ok(Cin: int) -> bool:
+    """Whether ``forward_implicit`` takes this layer (its lanes read four
+    gathered channels of one block, so Cin must be a multiple of 4)."""
+    return Cin % 4 == 0
+
+
 # C_T weights and spectrum per psi, reused while psi's storage and version
 # counter (bumped by in-place updates) and the stream are unchanged.
 _CACHE: dict = {}
@@ -110,20 +139,31 @@ class GroupConv2dFunction(torch.autograd.Function):
         k, _, T, Cout, Cin = psi.shape
         B, H, W = _dims(f, Cin, T)
         _, wspec = cached_ct_weight(psi)
-        xcol = gather(f, T, k)
-        y = ops.forward(xcol, wspec, b, T, k * k * Cin, Cout)
-        ctx.save_for_backward(xcol)
+        f = f.contiguous()
+        want_w = ctx.needs_input_grad[1] or (b is not None and ctx.needs_input_grad[2])
+        if implicit_ok(Cin) and not want_w:
+            # patches read straight from f (no patch buffer); the weight
+            # gradient, which needs them, takes the explicit gather below
+            y = forward_implicit(f, wspec, b, T, Cout, k)
+            ctx.save_for_backward(f)
+            ctx.xcol_saved = False
+        else:
+            xcol = gather(f, T, k)
+            y = ops.forward(xcol, wspec, b, T, k * k * Cin, Cout).view(B, H, W, Cout, T)
+            ctx.save_for_backward(xcol)
+            ctx.xcol_saved = True
         ctx.wspec, ctx.dims, ctx.has_bias = wspec, (B, H, W, T, Cin, Cout, k), b is not None
-        return y.view(B, H, W, Cout, T)
+        return y
 
     @staticmethod
     def backward(ctx, gy):
-        (xcol,) = ctx.saved_tensors
+        (saved,) = ctx.saved_tensors
         B, H, W, T, Cin, Cout, k = ctx.dims
+        want_w = ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2])
+        xcol = saved if ctx.xcol_saved else (gather(saved, T, k) if want_w else None)
         C2 = k * k * Cin
         gy2 = gy.contiguous().view(B * H * W, Cout, T)
         gf = gpsi = gb = None
-        want_w = ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2])
         dx2 = dw2 = None
         if ctx.needs_input_grad[0] and want_w:
             dx2, dw2, gb = ops.backward(xcol, gy2, ctx.wspec, T, C2, Cout, with_bias=ctx.has_bias)

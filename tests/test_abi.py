@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 18, names
+    assert len(names) == 19, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -302,6 +302,27 @@ def test_gconv_argument_checks(lib):
         assert call(1, A + 64) == L.EQL_ERR_INVALID_ARG     # output overlaps input
         if not _gpu_visible():
             assert call(2, 0) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)   # empty image: no-op
+    # the forward with the implicit patch gather
+    fw = L.eqlinear_gconv_forward
+    base = [A, A + 64 * MB, None, A + 128 * MB, B, H, W, T, 8, Cout, k, L.EQL_F32, None]
+
+    def callf(i, v):
+        args = list(base)
+        args[i] = v
+        return fw(*args)
+    assert callf(7, 3) == L.EQL_ERR_UNSUPPORTED             # T not in {1, 2, 4}
+    assert callf(8, 6) == L.EQL_ERR_UNSUPPORTED             # Cin not a multiple of 4
+    assert callf(10, 4) == L.EQL_ERR_UNSUPPORTED            # even kernel
+    assert callf(8, 0) == L.EQL_ERR_INVALID_ARG
+    assert callf(1, None) == L.EQL_ERR_INVALID_ARG          # no spectrum
+    assert callf(0, None) == L.EQL_ERR_INVALID_ARG
+    assert callf(3, None) == L.EQL_ERR_INVALID_ARG
+    assert callf(0, A + 4) == L.EQL_ERR_ALIGNMENT
+    assert callf(3, A + 16) == L.EQL_ERR_INVALID_ARG        # output overlaps the features
+    assert callf(2, A + 64 * MB) == L.EQL_ERR_INVALID_ARG   # bias overlaps the spectrum
+    assert callf(11, 7) == L.EQL_ERR_INVALID_ARG
+    if not _gpu_visible():
+        assert callf(4, 0) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)
     for f in (pk, up):
         base = [A, A + 64 * MB, T, Cin, Cout, k, L.EQL_F16, None]
 

@@ -32,9 +32,9 @@ def _draw(B, H, W, T, Cin, Cout, k, bias, seed, dt):
     """Seeded unit-normal features and gradients, weights scaled by
     1/sqrt(k*k*T*Cin), rounded to the run dtype (the oracle gets the rounded
     values)."""
-    from synth import DTYPES
+    import synth
     rs = np.random.RandomState(seed)
-    rnd = lambda a: a.astype(DTYPES[dt]).astype(np.float64)
+    rnd = lambda a: synth.round_to(a, dt).astype(np.float64)
     f = rnd(rs.standard_normal((B, H, W, Cin, T)))
     psi = rnd(rs.standard_normal((k, k, T, Cout, Cin)) / np.sqrt(k * k * T * Cin))
     b = rnd(0.1 * rs.standard_normal(Cout)) if bias else None
@@ -75,12 +75,13 @@ def test_group_conv_matches_oracle(go, B, H, W, T, Cin, Cout, k, bias, dt):
 
 @pytest.mark.parametrize("dt", ["f32", "f16"])
 @pytest.mark.parametrize("T", [4, 2])
-def test_group_conv_is_equivariant_on_gpu(dt, T):
+@pytest.mark.parametrize("Cin", [6, 8])
+def test_group_conv_is_equivariant_on_gpu(dt, T, Cin):
     """Rotating the image about its centre by 360/T degrees and shifting the
     group axis by one rotates and shifts the GPU output the same way (to the
-    dtype's rounding)."""
+    dtype's rounding); Cin = 8 takes the implicit-gather forward."""
     from paper_2607_21271_amd import gconv
-    B, H, Cin, Cout, k = 2, 9, 6, 8, 3
+    B, H, Cout, k = 2, 9, 8, 3
     f, psi, b, _ = _draw(B, H, H, T, Cin, Cout, k, True, 8400 + T, dt)
     quarter = 1 if T == 4 else 2
     act = lambda z: np.roll(np.rot90(z, k=quarter, axes=(1, 2)), 1, axis=-1)
@@ -111,3 +112,63 @@ def test_gather_scatter_adjoint_and_weight_permutation():
         rhs = float((f.double() * df.double()).sum())
         assert abs(lhs - rhs) <= 1e-4 * max(1.0, abs(lhs)), (T, k, lhs, rhs)
         assert torch.equal(back, psi), (T, k)
+
+
+IMPLICIT = [(2, 7, 7, 4, 4, 5, 3, True), (1, 9, 6, 4, 8, 16, 5, False), (3, 5, 8, 2, 8, 4, 3, True),
+            (2, 6, 5, 1, 4, 7, 3, True), (2, 8, 8, 4, 24, 48, 3, True), (1, 4, 4, 4, 4, 2, 1, True),
+            (2, 5, 5, 2, 4, 4, 7, False), (4, 16, 16, 4, 12, 24, 3, True), (1, 11, 13, 4, 32, 96, 3, False)]
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("B,H,W,T,Cin,Cout,k,bias", IMPLICIT,
+                         ids=["B%dx%dx%d-T%d-%dx%d-k%d" % c[:7] for c in IMPLICIT])
+def test_implicit_gather_forward(go, B, H, W, T, Cin, Cout, k, bias, dt):
+    """eqlinear_gconv_forward (patches read straight from f by the forward
+    kernel) equals the patch gather followed by eqlinear_forward bit for bit,
+    and the oracle to the dtype's bar."""
+    from paper_2607_21271_amd import gconv, ops
+    say("gconv implicit", B, H, W, T, Cin, Cout, k, bias, dt)
+    f, psi, b, _ = _draw(B, H, W, T, Cin, Cout, k, bias, 8700 + 7 * T + k + Cin + Cout, dt)
+    ft, pt = to_dev(f, dt), to_dev(psi, dt)
+    bt = to_dev(b, dt) if b is not None else None
+    wspec = ops.weight_spectrum(gconv.pack_weight(pt))
+    y = gconv.forward_implicit(ft, wspec, bt, T, Cout, k)
+    y_ref = ops.forward(gconv.gather(ft, T, k), wspec, bt, T, k * k * Cin, Cout).view(B, H, W, Cout, T)
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int16 if dt != "f32" else torch.int32),
+                       y_ref.view(torch.int16 if dt != "f32" else torch.int32))
+    err = rel_err(y.float().cpu().numpy(), go.forward(f, psi, b))
+    say("  ", "%.2e" % err)
+    assert err <= TOL[dt]
+
+
+def test_implicit_gather_refuses_unaligned_channels():
+    from paper_2607_21271_amd import _lib, gconv, ops
+    f = torch.zeros(1, 4, 4, 3, 4, device="cuda")
+    wspec = ops.weight_spectrum(gconv.pack_weight(torch.zeros(3, 3, 4, 5, 3, device="cuda")))
+    with pytest.raises(_lib.EqlError) as e:
+        gconv.forward_implicit(f, wspec, None, 4, 5, 3)
+    assert e.value.status == _lib.EQL_ERR_UNSUPPORTED
+    assert not gconv.implicit_ok(3) and gconv.implicit_ok(8)
+
+
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("B,H,W,T,Cin,Cout,k,bias", IMPLICIT[:5],
+                         ids=["B%dx%dx%d-T%d-%dx%d-k%d" % c[:7] for c in IMPLICIT[:5]])
+def test_frozen_weight_group_conv(go, B, H, W, T, Cin, Cout, k, bias, dt):
+    """A frozen weight (no gradient for psi or b): the autograd function runs
+    the implicit-gather forward and the input gradient alone; output and
+    feature gradient against the oracle."""
+    from paper_2607_21271_amd import gconv
+    say("gconv frozen", B, H, W, T, Cin, Cout, k, bias, dt)
+    f, psi, b, dout = _draw(B, H, W, T, Cin, Cout, k, bias, 8700 + 7 * T + k + Cin, dt)
+    ft = to_dev(f, dt).requires_grad_(True)
+    pt = to_dev(psi, dt)
+    bt = to_dev(b, dt) if b is not None else None
+    y = gconv.GroupConv2dFunction.apply(ft, pt, bt)
+    y.backward(to_dev(dout, dt))
+    torch.cuda.synchronize()
+    ey = rel_err(y.detach().float().cpu().numpy(), go.forward(f, psi, b))
+    edf = rel_err(ft.grad.float().cpu().numpy(), go.backward_input(dout, psi))
+    say("  y %.2e df %.2e" % (ey, edf))
+    assert ey <= TOL[dt] and edf <= TOL[dt], (ey, edf)
