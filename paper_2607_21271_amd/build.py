@@ -23,7 +23,7 @@ BUILD_DIR = os.path.join(HERE, "_build")
 HOST_SOURCES = ["eql_api.cpp", "eql_dispatch.cpp"]
 MAX_T = 16
 # (source, object stem, extra defines)
-UNITS = [(s, os.path.splitext(s)[0], []) for s in HOST_SOURCES] + [
+UNITS = [("eql_big.hip", "eql_big", [])] + [(s, os.path.splitext(s)[0], []) for s in HOST_SOURCES] + [
     ("eql_inst.hip", "inst_%s_t%02d" % (name, t), ["-DEQK_T=%d" % t, "-DEQK_DT=%d" % dt])
     for t in range(MAX_T, 0, -1) for dt, name in ((1, "f16"), (0, "f32"), (2, "bf16"))]
 
@@ -31,9 +31,13 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 # Packed-fp32 instructions are switched off for all device code.
 # MFMA accumulators may live in arch VGPRs (gfx950 has a unified register
-# file); with this selection the large-tile kernels allocate without scratch.
-DEVICE_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang",
-                "-packed-fp32-ops", "-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+# file); with this selection the kernels of two waves per SIMD allocate
+# without scratch.  The large-tile unit (one wave per SIMD, T * 64
+# accumulators per lane) keeps them in the accumulation registers instead.
+LINK_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+VGPR_FORM = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+DEVICE_FLAGS = LINK_FLAGS + VGPR_FORM
+ACC_REG_UNITS = {"eql_big"}
 COMMON_FLAGS = ["-O3", "-std=c++20", "-fPIC", "-Wall", "-Wno-unused-function",
                 "-I" + os.path.join(os.path.dirname(HERE), "include")]
 
@@ -44,7 +48,8 @@ def _compile(unit) -> str:
     os.makedirs(wd, exist_ok=True)
     obj = os.path.join(wd, stem + ".o")
     lang = ["-x", "hip"] if src.endswith(".cpp") else []
-    cmd = [HIPCC, *DEVICE_FLAGS, *COMMON_FLAGS, *defs, "-save-temps", *lang, "-c",
+    dev = LINK_FLAGS if stem in ACC_REG_UNITS else DEVICE_FLAGS
+    cmd = [HIPCC, *dev, *COMMON_FLAGS, *defs, "-save-temps", *lang, "-c",
            os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True, cwd=wd)
     if r.returncode != 0:

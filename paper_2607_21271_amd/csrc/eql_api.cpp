@@ -355,6 +355,10 @@ int gemm_forced_mode() {
   const char* v = getenv("EQL_GEMM_MODE");
   return (v != nullptr && v[0] >= '0' && v[0] <= '2' && v[1] == 0) ? v[0] - '0' : -1;
 }
+int gemm_big_forced() {
+  const char* v = getenv("EQL_GEMM_BIG");
+  return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
+}
 // Valid after check_device() succeeded on the current device.
 int device_cu_count() {
   int dev = 0;
@@ -427,6 +431,21 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   if ((st = check_device())) return st;
   if (N == 0) return EQL_OK;
   const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype != EQL_F32);
+  const size_t fwd_block = (size_t)T * d.CoF * d.CiF * e;  // forward-layout planes
+  if (eqk::gemm_big_choose(T, Ci, Co, dtype != EQL_F32)) {
+    eqk::BigArgs b{};
+    b.in = in;
+    b.bias = bias;
+    b.out = out;
+    b.N = N;
+    b.Ci = Ci;
+    b.Co = Co;
+    b.wsp = bwd ? (const void*)((const char*)wspec + fwd_block) : wspec;
+    b.w_rows = bwd ? d.CinB : d.CoF;
+    b.w_pitch = bwd ? d.CoutB : d.CiF;
+    b.stream = (hipStream_t)stream;
+    return launched(eqk::launch_gemm_big(dtype, T, bwd, b));
+  }
   eqk::GemmArgs a{};
   a.in = in;
   a.bias = bias;
@@ -441,7 +460,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
     a.wsp = wspec;
     a.Ci_pad = d.CiF;
   } else {
-    a.wsp = (const char*)wspec + (size_t)T * d.CoF * d.CiF * e;
+    a.wsp = (const char*)wspec + fwd_block;
     a.Ci_pad = d.CoutB;
   }
   return launched(eqk::launch_gemm(dtype, T, bwd, a));

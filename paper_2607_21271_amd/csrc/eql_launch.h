@@ -283,6 +283,36 @@ struct Inst {
 // Dispatch over T and the element type code dt (eql_dispatch.cpp).
 hipError_t launch_wspec(int dt, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
 hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a);
+
+// Large-tile forward / input gradient (eql_gemm_big.h): 16-bit elements, T in
+// {2, 4}, contraction channels a multiple of 32, and every 128-row tile of the
+// input and output below 2^31 bytes.  Taken by default for wide layers (both
+// channel counts at least kBigMinC), where the spectral products bound the
+// pass; EQL_GEMM_BIG=0 never takes it, =1 whenever the shape allows (tests,
+// A/B timing).
+struct BigArgs {
+  const void* in;
+  const void* wsp;   // plane block of the layout this pass reads
+  const void* bias;  // forward only; may be null
+  void* out;
+  int64_t N;
+  int Ci, Co;        // contraction and output channels of this pass
+  int w_rows, w_pitch;  // rows (>= Co) and row pitch (>= Ci) of a spectrum plane
+  hipStream_t stream;
+};
+constexpr int kBigMinC = 512;
+int gemm_big_forced();  // -1 unset, 0, 1
+inline bool gemm_big_fits(int T, int Ci, int Co, bool w16) {
+  return w16 && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&
+         (int64_t)128 * Ci * T * 2 < ((int64_t)1 << 31) && (int64_t)128 * Co * T * 2 < ((int64_t)1 << 31);
+}
+inline bool gemm_big_choose(int T, int Ci, int Co, bool w16) {
+  if (!gemm_big_fits(T, Ci, Co, w16)) return false;
+  const int f = gemm_big_forced();
+  if (f >= 0) return f == 1;
+  return Ci >= kBigMinC && Co >= kBigMinC;
+}
+hipError_t launch_gemm_big(int dt, int T, bool bwd, const BigArgs& a);
 hipError_t launch_gemm_gather(int dt, int T, const GemmArgs& a);
 hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p);
 hipError_t launch_bwd_fused(int dt, int T, const FusedArgs& a, const FusedPlan& p);
