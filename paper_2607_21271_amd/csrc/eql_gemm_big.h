@@ -124,25 +124,22 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
     woff[v] = (uint32_t)(((int64_t)p * w_rows + o0 + row) * w_pitch * EB + ch * 16);
   }
 
-  // Pipeline, per step s: the real-bin MFMAs of s; the activations of s + 1
-  // (loaded during step s - 1) transformed into LDS buffer (s + 1) & 1; the
-  // weight chunks of s + 2 issued into LDS buffer (s + 2) % 3 and the raw
-  // activations of s + 2 into registers; the complex-bin MFMAs of s.  Each
-  // load has a full step (weights 5/3 of one) to arrive, and at the staging
-  // point the newest loads in flight are the ones it consumes, so no wait
-  // covers loads issued later.
+  // Pipeline, per step s: the weight chunks of s + 2 issued into LDS buffer
+  // (s + 2) % 3; the MFMAs of s, real bins then complex bins, and between the
+  // row tiles of the first complex bin (of the real bins at T = 2) the four
+  // staging units of the activations of s + 1 (loaded during step s - 1),
+  // each transformed into LDS buffer (s + 1) & 1 and then reloaded with the
+  // raw activations of s + 2.  Weights have two steps to arrive, activations
+  // one, and the scheduler spreads the transforms between the MFMAs.
   uint32_t xr[XU][UB / 4];
   // (past the last step the reads land in padding or past the resources, in
   // buffers that are never read again)
-  auto load_x = [&](int s) __attribute__((always_inline)) {
+  auto load_x = [&](int s, int v) __attribute__((always_inline)) {
     const int xs = s * kBigBK * T * EB;
 #pragma unroll
-    for (int v = 0; v < XU; ++v) {
-#pragma unroll
-      for (int h = 0; h < UB / 16; ++h) {
-        const u32x4 a = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff[v] + 16 * h, xs, 0));
-        xr[v][4 * h] = a[0]; xr[v][4 * h + 1] = a[1]; xr[v][4 * h + 2] = a[2]; xr[v][4 * h + 3] = a[3];
-      }
+    for (int h = 0; h < UB / 16; ++h) {
+      const u32x4 a = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff[v] + 16 * h, xs, 0));
+      xr[v][4 * h] = a[0]; xr[v][4 * h + 1] = a[1]; xr[v][4 * h + 2] = a[2]; xr[v][4 * h + 3] = a[3];
     }
   };
   auto load_w = [&](int s) __attribute__((always_inline)) {
@@ -158,32 +155,41 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
     (void)wrs;
 #endif
   };
-  // vector-memory instructions issued per step after a step's weight chunks
-  // (those of the next step's weights and activations): the wait before each
-  // barrier leaves them in flight.  vmcnt n is encoded in bits 3:0 and 15:14.
-  constexpr int NV = XU * (UB / 16) + WDU;
+  // Barrier of step s: this wave's LDS writes done (lgkmcnt 0) and the weight
+  // chunks of s in LDS; the vector-memory instructions issued after those
+  // (activations of s and s + 1, weights of s + 1) may stay in flight.  The
+  // barrier carries no memory fence (a workgroup fence would also wait for
+  // the weight chunks of s + 1, which are still arriving); the signal fences
+  // keep the compiler from moving memory accesses across it.  vmcnt n is
+  // encoded in bits 3:0 and 15:14, lgkmcnt in 11:8.
+  constexpr int NV = 2 * XU * (UB / 16) + WDU;
   static_assert(NV < 64, "vmcnt range");
-  constexpr int kWaitW = (NV & 15) | ((NV >> 4) << 14) | 0x0F70;
-  // transform the raw activations into T planes in LDS activation buffer b
-  auto publish = [&](int b) __attribute__((always_inline)) {
-    char* base = xbase + b * XB;
-#pragma unroll
-    for (int v = 0; v < XU; ++v) {
-      uint32_t W[T][HKW / 2];
-      if constexpr (DT == kF16) {
-        raw_to_packed_planes<T, HKW>(xr[v], W);
-      } else {
-        float P[T][HKW];
-        raw_to_planes<T, DT, HKW>(xr[v], P);
-#pragma unroll
-        for (int p = 0; p < T; ++p)
-#pragma unroll
-          for (int j = 0; j < HKW / 2; ++j) W[p][j] = pack2<DT>(P[p][2 * j], P[p][2 * j + 1]);
-      }
-#pragma unroll
-      for (int p = 0; p < T; ++p) *reinterpret_cast<u32x2*>(base + p * XPL + xlds[v]) = u32x2{W[p][0], W[p][1]};
-    }
+  constexpr int kWaitBar = (NV & 15) | ((NV >> 4) << 14) | 0x0070;
+  auto barrier = [&]() __attribute__((always_inline)) {
+    __builtin_amdgcn_s_waitcnt(kWaitBar);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
   };
+  // transform the raw activations of unit v into T planes in LDS activation
+  // buffer b
+  auto publish = [&](int b, int v) __attribute__((always_inline)) {
+    char* base = xbase + b * XB;
+    uint32_t W[T][HKW / 2];
+    if constexpr (DT == kF16) {
+      raw_to_packed_planes<T, HKW>(xr[v], W);
+    } else {
+      float P[T][HKW];
+      raw_to_planes<T, DT, HKW>(xr[v], P);
+#pragma unroll
+      for (int p = 0; p < T; ++p)
+#pragma unroll
+        for (int j = 0; j < HKW / 2; ++j) W[p][j] = pack2<DT>(P[p][2 * j], P[p][2 * j + 1]);
+    }
+#pragma unroll
+    for (int p = 0; p < T; ++p) *reinterpret_cast<u32x2*>(base + p * XPL + xlds[v]) = u32x2{W[p][0], W[p][1]};
+  };
+  static_assert(XU == 4, "one staging unit per row tile");
 
   floatx4 acc[T][4][4];
 #pragma unroll
@@ -230,12 +236,13 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
         for (int p = 0; p < R; ++p)
 #pragma unroll
           for (int j = 0; j < 4; ++j) frag_mma<DT, 8>(acc[p][i][j], A[i & 1][p], B[p][j]);
+        if constexpr (Bn::K == 0) {
+          publish((s + 1) & 1, i);
+          load_x(s + 2, i);
+        }
         __builtin_amdgcn_sched_barrier(0);
       });
     }
-    publish((s + 1) & 1);
-    load_x(s + 2);
-    __builtin_amdgcn_sched_barrier(0);
     static_for<Bn::K>([&](auto ki) {
       constexpr int k = decltype(ki)::value + 1;
       constexpr int re = Bn::re(k), im = Bn::im(k);
@@ -270,23 +277,31 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
             frag_mma<DT, 8>(acc[im][i][j], xn, Bi[j]);
           }
         }
+        // one staging unit of the next step per row tile (first complex
+        // bin), interleaved with these MFMAs by the scheduler
+        if constexpr (k == 1) {
+          publish((s + 1) & 1, i);
+          load_x(s + 2, i);
+        }
         __builtin_amdgcn_sched_barrier(0);
       });
     });
   };
 
   // prologue: activations of step 0 staged, weights of steps 0 and 1 and raw
-  // activations of step 1 in flight.  Step s: wait for the weight chunks of s
-  // (the newest NV loads may stay in flight); the barrier makes buffers
+  // activations of step 1 in flight.  The barrier of step s makes buffers
   // s & 1 / s % 3 complete and frees those read in step s - 1.
-  load_x(0);
   load_w(0);
-  publish(0);
-  load_x(1);
+#pragma unroll
+  for (int v = 0; v < XU; ++v) load_x(0, v);
+  load_w(1);
+#pragma unroll
+  for (int v = 0; v < XU; ++v) publish(0, v);
+#pragma unroll
+  for (int v = 0; v < XU; ++v) load_x(1, v);
   for (int s = 0; s < nks; ++s) {
-    __builtin_amdgcn_s_waitcnt(kWaitW);
-    __syncthreads();
-    load_w(s + 1);
+    barrier();
+    load_w(s + 2);
     step(s);
   }
 

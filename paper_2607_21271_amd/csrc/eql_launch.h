@@ -300,7 +300,7 @@ struct BigArgs {
   int w_rows, w_pitch;  // rows (>= Co) and row pitch (>= Ci) of a spectrum plane
   hipStream_t stream;
 };
-constexpr int kBigMinC = 512;
+constexpr int kBigMinC = 256;
 int gemm_big_forced();  // -1 unset, 0, 1
 inline bool gemm_big_fits(int T, int Ci, int Co, bool w16) {
   return w16 && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&
