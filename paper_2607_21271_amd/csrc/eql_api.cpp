@@ -117,10 +117,37 @@ static WgradPlan wgrad_plan_rd(int64_t N, int T, int Cin, int Cout, bool w16) {
   return p;
 }
 
-// Which weight-gradient kernel: EQL_WGRAD_KIND=0/1 forces one (tests, A/B timing).
+// Which weight-gradient kernel: EQL_WGRAD_KIND=0/1/2 forces one (tests, A/B timing).
 static int wgrad_forced_kind() {
   const char* v = getenv("EQL_WGRAD_KIND");
-  return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
+  return (v != nullptr && v[0] >= '0' && v[0] <= '2' && v[1] == 0) ? v[0] - '0' : -1;
+}
+
+// Large-tile plan: 128 x 128 channel tiles, and row splits (whole steps of 32
+// rows, at least 8 per split) until about one workgroup per CU.
+static WgradPlan wgrad_plan_big(int64_t N, int T, int Cin, int Cout) {
+  WgradPlan p{};
+  p.kind = 2;
+  p.BC = p.BO = 128;
+  p.KR = 32;
+  p.n_ct = (Cin + 127) / 128;
+  p.n_ot = (Cout + 127) / 128;
+  p.Cin_pad = p.n_ct * 128;
+  p.Cout_pad = p.n_ot * 128;
+  p.N_pad = (N + 63) / 64 * 64;  // whole blocks of the spectrum pre-pass
+  const int64_t steps = p.N_pad / 32;
+  const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
+  int64_t S = tiles >= 256 ? 1 : (256 + tiles - 1) / tiles;
+  const int64_t max_s = steps / 8 > 1 ? steps / 8 : 1;
+  if (S > max_s) S = max_s;
+  const int64_t per = (steps + S - 1) / S;
+  p.rows_per_split = per * 32;
+  p.S = (int)((steps + per - 1) / per);
+  p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
+  p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
+  p.xs_bytes = (size_t)T * p.Cin_pad * p.N_pad * 2;
+  p.ds_bytes = (size_t)T * p.Cout_pad * p.N_pad * 2;
+  return p;
 }
 
 static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16);
@@ -137,9 +164,15 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16
 // 2048 fp32, 7.6 vs 26.8 ms at 2048 fp16), level at 96 x 384 and 256 x 256,
 // and slower on Swin stage 1 (24 x 96: 120 vs 79 us) and the 64 x 64 sweep.
 // bf16 plans as fp16 (same shapes and tiles).
-WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt) {
+WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt, size_t max_ws) {
   const bool w16 = dt != kF32;  // 16-bit elements: same shapes for fp16 and bf16
-  const int forced = wgrad_forced_kind();
+  int forced = wgrad_forced_kind();
+  if (wgrad_big_fits(N, T, Cin, Cout, w16) &&
+      (forced == 2 || (forced < 0 && Cin >= wgrad_big_min_c(dt) && Cout >= wgrad_big_min_c(dt)))) {
+    const WgradPlan p = wgrad_plan_big(N, T, Cin, Cout);
+    if (wgrad_workspace(p) <= max_ws) return p;
+  }
+  if (forced == 2) forced = -1;
   const int lo = Cin < Cout ? Cin : Cout, hi = Cin < Cout ? Cout : Cin;
   if (forced == 1 || (forced < 0 && (hi <= 48 || lo >= 512)))
     return wgrad_plan_rd(N, T, Cin, Cout, w16);
@@ -478,8 +511,7 @@ int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t
 
 size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype) {
   if (check_shape(N, T, Cin, Cout, dtype) != EQL_OK || N == 0) return 0;
-  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype);
-  return align256(p.part_bytes) + align256(p.dbpart_bytes);
+  return eqk::wgrad_workspace(eqk::wgrad_plan(N, T, Cin, Cout, dtype));
 }
 
 static int backward_weight_impl(const void* x, const void* dy, void* dw, void* dbias, void* workspace,
@@ -542,7 +574,10 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
   if ((x && !aligned(x, 16)) || (dy && !aligned(dy, 16)) || !aligned(dw, e) ||
       (dbias && !aligned(dbias, e)) || (workspace && !aligned(workspace, 16)))
     return EQL_ERR_ALIGNMENT;
-  const size_t need = eqlinear_backward_weight_workspace_bytes(N, T, Cin, Cout, dtype);
+  // the allocation-free entry point plans within its static scratch
+  const eqk::WgradPlan p =
+      eqk::wgrad_plan(N, T, Cin, Cout, dtype, static_scratch ? EQLINEAR_STATIC_SCRATCH_BYTES : (size_t)-1);
+  const size_t need = N > 0 ? eqk::wgrad_workspace(p) : 0;
   if (static_scratch && need > EQLINEAR_STATIC_SCRATCH_BYTES) return EQL_ERR_SCRATCH;
   if (!static_scratch && need > 0 && (!workspace || workspace_bytes < need)) return EQL_ERR_WORKSPACE;
   const Range r[5] = {{x, (size_t)N * Cin * T * e},
@@ -556,7 +591,6 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
     workspace = device_scratch();
     if (!workspace) return EQL_ERR_LAUNCH;
   }
-  const eqk::WgradPlan p = eqk::wgrad_plan(N, T, Cin, Cout, dtype);
   eqk::WgradArgs a{};
   a.x = x;
   a.dy = dy;
@@ -564,10 +598,19 @@ static int backward_weight_impl(const void* x, const void* dy, void* dw, void* d
   a.db = dbias;
   a.part = (float*)workspace;
   a.dbpart = workspace ? (float*)((char*)workspace + align256(p.part_bytes)) : nullptr;
+  if (p.kind == 2) {
+    char* w = (char*)workspace + align256(p.part_bytes) + align256(p.dbpart_bytes);
+    a.xs = w;
+    a.ds = w + align256(p.xs_bytes);
+  }
   a.N = N;
   a.Cin = Cin;
   a.Cout = Cout;
   a.stream = (hipStream_t)stream;
+  if (p.kind == 2 && N > 0) {
+    st = launched(eqk::launch_wgrad_big(dtype, T, a, p));
+    if (st) return st;
+  }
   return launched(eqk::launch_wgrad(dtype, T, a, p));
 }
 

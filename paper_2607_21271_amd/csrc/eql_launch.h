@@ -159,8 +159,34 @@ struct WgradPlan {
   int64_t rows_per_split;
   int Cin_pad, Cout_pad;
   size_t part_bytes, dbpart_bytes;
+  // kind 2 (eql_wgrad_big.h): row-contiguous spectra of x and dy in the
+  // workspace, N_pad rows (a multiple of 64) per plane row
+  int64_t N_pad;
+  size_t xs_bytes, ds_bytes;
 };
-WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt);  // dt: element type code
+// dt: element type code.  Plans whose workspace would exceed max_ws fall
+// back to the split-row kernels (the allocation-free entry point passes its
+// static scratch size).
+WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt, size_t max_ws = (size_t)-1);
+inline size_t align256z(size_t v) { return (v + 255) / 256 * 256; }
+// workspace of a plan: partials, bias partials, then (kind 2) the spectra
+inline size_t wgrad_workspace(const WgradPlan& p) {
+  return align256z(p.part_bytes) + align256z(p.dbpart_bytes) + align256z(p.xs_bytes) + align256z(p.ds_bytes);
+}
+// Large-tile weight gradient (kind 2): 16-bit elements, T in {2, 4}, and the
+// spectra of x and dy addressable with 31-bit offsets.  Taken by default from
+// wgrad_big_min_c channels each way, where it measured faster than the
+// register-direct kernel (T = 4, 32,768 rows: fp16 from 1024, 0.85 vs 0.97 ms,
+// level at 512; bf16 from 512, 0.27 vs 0.34 ms); EQL_WGRAD_KIND=2 forces it
+// where it fits.
+inline int wgrad_big_min_c(int dt) { return dt == kBF16 ? 512 : 1024; }
+inline bool wgrad_big_fits(int64_t N, int T, int Cin, int Cout, bool w16) {
+  const int64_t np = (N + 63) / 64 * 64;
+  const int64_t ci = (Cin + 127) / 128 * 128, co = (Cout + 127) / 128 * 128;
+  const int64_t lim = (int64_t)1 << 31;
+  return w16 && (T == 2 || T == 4) && N > 0 && (int64_t)T * ci * np * 2 < lim && (int64_t)T * co * np * 2 < lim &&
+         (int64_t)64 * (Cin > Cout ? Cin : Cout) * T * 2 < lim;
+}
 
 // Shape of the partial reduction: NTHR threads per workgroup, runs of IPW
 // items (IPW * 16 bytes per split and plane), G = NTHR / (IPW * T) split
@@ -250,6 +276,8 @@ struct WgradArgs {
   void* db;          // may be null
   float* part;
   float* dbpart;
+  void* xs;          // kind 2: row-contiguous spectra of x and dy
+  void* ds;
   int64_t N;
   int Cin, Cout;
   hipStream_t stream;
@@ -315,6 +343,9 @@ inline bool gemm_big_choose(int T, int Ci, int Co, bool w16) {
 hipError_t launch_gemm_big(int dt, int T, bool bwd, const BigArgs& a);
 hipError_t launch_gemm_gather(int dt, int T, const GemmArgs& a);
 hipError_t launch_wgrad(int dt, int T, const WgradArgs& a, const WgradPlan& p);
+// kind 2: the spectrum pre-passes and the product kernel (launch_wgrad then
+// runs the reduction)
+hipError_t launch_wgrad_big(int dt, int T, const WgradArgs& a, const WgradPlan& p);
 hipError_t launch_bwd_fused(int dt, int T, const FusedArgs& a, const FusedPlan& p);
 
 }  // namespace eqk

@@ -248,6 +248,8 @@ hipError_t fused_t(const FusedArgs& f, const FusedPlan& p) {
 
 template <int T, int DT>
 hipError_t wgrad_t(const WgradArgs& a, const WgradPlan& p) {
+  // large-tile plan: its pre-passes and product kernel ran (launch_wgrad_big)
+  if (p.kind == 2) return wgrad_reduce<T, DT>(a, p);
   if (p.kind == 1) {
 #define EQK_RD(C_, O_)                                             \
   if constexpr (rd_fits(T, C_, O_)) {                              \

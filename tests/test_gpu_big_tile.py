@@ -1,12 +1,15 @@
-"""GPU parity of the large-tile forward / input-gradient kernel
-(csrc/eql_gemm_big.h: 128 x 128 output tiles, 16-bit elements, T in {2, 4})
-against the fp64 oracle, through the C ABI.
+"""GPU parity of the large-tile kernels (16-bit elements, T in {2, 4}) against
+the fp64 oracle, through the C ABI: the forward / input gradient
+(csrc/eql_gemm_big.h: 128 x 128 output tiles) and the weight gradient
+(csrc/eql_wgrad_big.h: row-contiguous spectra, 128 x 128 (c, o) tiles, row
+splits, the split-partial reduction).
 
 The host takes this kernel for wide layers only; EQL_GEMM_BIG=1 forces it
 wherever the shape allows (contraction channels a multiple of 32), so small
 shapes with ragged rows and ragged output-channel tiles cover its tails.  A
 pass whose contraction channels are not a multiple of 32 keeps the other
-kernel (the input gradient of the Cout = 200 case).  Bar as for the layer:
+kernel (the input gradient of the Cout = 200 case).  EQL_WGRAD_KIND=2 forces
+the weight-gradient path likewise.  Bar as for the layer:
 max|gpu - oracle| / max|oracle| <= 5e-3 (fp16), 4e-2 (bf16).
 """
 import numpy as np
@@ -89,3 +92,82 @@ def test_big_tile_table_shape_sampled(orc, dt):
     edx = rel_err(dx[idx].float().cpu().numpy(), rdx)
     say("  table shape", dt, "y %.2e dx %.2e" % (ey, edx))
     assert ey <= TOL[dt] and edx <= TOL[dt], (ey, edx)
+
+
+WG_CASES = [(4, 32, 128, 128, True), (4, 64, 200, 300, True), (2, 96, 256, 777, True),
+            (4, 160, 96, 1000, False), (4, 300, 130, 2000, True), (2, 256, 64, 129, False),
+            (4, 384, 256, 2100, True), (4, 16, 40, 33, True)]
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", WG_CASES, ids=["T%d-%dx%d-N%d" % c[:4] for c in WG_CASES])
+def test_big_wgrad_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+    """dw and db of the forced large-tile weight gradient (single split for
+    the small row counts, several for the 384 x 256 and 300 x 130 cases)."""
+    say("big wgrad", T, Cin, Cout, N, bias, dt)
+    monkeypatch.setenv("EQL_WGRAD_KIND", "2")
+    inp = synth.draw(T, Cin, Cout, N, bias, 9500 + 13 * T + Cin + Cout).rounded(dt)
+    g = run_gpu(inp, dt, want=("dw",))
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy, with_bias=bias)
+    errs = {"dw": rel_err(g["dw"], ref_dw)}
+    if bias:
+        errs["db"] = rel_err(g["db"], ref_db)
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (k, v)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+def test_big_whole_backward_default_plan(orc, dt):
+    """A layer wide enough for both large-tile kernels by default (1024 ->
+    1024 at T = 4; 520 rows keep the fp64 oracle fast): the whole backward
+    (eqlinear_backward) and the forward against the oracle."""
+    from paper_2607_21271_amd import ops
+    T, Cin, Cout, N = 4, 1024, 1024, 520
+    inp = synth.draw(T, Cin, Cout, N, True, 9600).rounded(dt)
+    x, w, dy, b = to_dev(inp.x, dt), to_dev(inp.w, dt), to_dev(inp.dy, dt), to_dev(inp.b, dt)
+    wspec = ops.weight_spectrum(w)
+    y = ops.forward(x, wspec, b, T, Cin, Cout)
+    dx, dw, db = ops.backward(x, dy, wspec, T, Cin, Cout, with_bias=True)
+    torch.cuda.synchronize()
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy)
+    errs = {"y": rel_err(y.float().cpu().numpy(), orc.forward(inp.x, inp.w, inp.b)),
+            "dx": rel_err(dx.float().cpu().numpy(), orc.backward_input(inp.dy, inp.w)),
+            "dw": rel_err(dw.float().cpu().numpy(), ref_dw),
+            "db": rel_err(db.float().cpu().numpy(), ref_db)}
+    say("  whole backward", dt, {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (k, v)
+
+
+def test_big_wgrad_noalloc_falls_back_within_scratch():
+    """A wide layer whose large-tile plan needs more workspace than the static
+    scratch of the allocation-free entry point (1024 x 1024 at T = 4, 4,096
+    rows: spectra of 2 x 32 MiB plus partials): that entry point plans the
+    split-row kernels instead, and agrees with the workspace entry point to
+    the fp16 bar."""
+    from paper_2607_21271_amd import _lib as L
+    L.lib()
+    T, C, N = 4, 1024, 4096
+    need = L.eqlinear_backward_weight_workspace_bytes(N, T, C, C, L.EQL_F16)
+    assert need > L.STATIC_SCRATCH_BYTES, need
+    rs = np.random.RandomState(9700)
+    x = torch.from_numpy(rs.standard_normal((N, C, T)).astype(np.float16)).cuda()
+    dy = torch.from_numpy(rs.standard_normal((N, C, T)).astype(np.float16)).cuda()
+    stream = torch.cuda.current_stream().cuda_stream
+    dw_ws = torch.empty(T, C, C, dtype=torch.float16, device="cuda")
+    db_ws = torch.empty(C, dtype=torch.float16, device="cuda")
+    ws = torch.empty(need, dtype=torch.uint8, device="cuda")
+    st = L.eqlinear_backward_weight(x.data_ptr(), dy.data_ptr(), dw_ws.data_ptr(), db_ws.data_ptr(), ws.data_ptr(),
+                                    need, N, T, C, C, L.EQL_F16, stream)
+    assert st == L.EQL_OK, L.eqlinear_status_string(st)
+    dw_na = torch.empty_like(dw_ws)
+    db_na = torch.empty_like(db_ws)
+    st = L.eqlinear_backward_weight_noalloc(x.data_ptr(), dy.data_ptr(), dw_na.data_ptr(), db_na.data_ptr(), N, T,
+                                            C, C, L.EQL_F16, stream)
+    assert st == L.EQL_OK, L.eqlinear_status_string(st)
+    torch.cuda.synchronize()
+    e_dw = rel_err(dw_na.float().cpu().numpy(), dw_ws.float().cpu().numpy())
+    e_db = rel_err(db_na.float().cpu().numpy(), db_ws.float().cpu().numpy())
+    say("  noalloc vs workspace", "%.2e %.2e" % (e_dw, e_db))
+    assert e_dw <= TOL["f16"] and e_db <= TOL["f16"], (e_dw, e_db)
