@@ -131,7 +131,9 @@ int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t
                             int Cin, int Cout, int dtype, void* stream);
 
 /* Bytes of device workspace that eqlinear_backward_weight needs for this
- * problem (fp32 partial sums of the row splits); 0 if the arguments are
+ * problem (fp32 partial sums of the row splits; for wide layers with 16-bit
+ * elements and T = 2 or 4 also the transformed x and dy, stored with the
+ * rows contiguous, about 2 (Cin + Cout) T N bytes); 0 if the arguments are
  * invalid or N = 0. */
 size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype);
 
@@ -257,13 +259,16 @@ int eqlinear_gconv_forward(const void* f, const void* wspec, const void* bias, v
 
 /* eqlinear_backward_weight without a workspace argument, for callers that
  * cannot allocate device memory (code under HIP graph capture, serving loops,
- * harnesses that forbid allocation).  Same operation, arguments (minus the
- * workspace), kernels and bits as eqlinear_backward_weight; the fp32 split
- * partials live in a file-scope static device array of
- * EQLINEAR_STATIC_SCRATCH_BYTES per GPU instead, and the call performs no
- * allocation of any kind.  A problem whose partials need more than that
- * (eqlinear_backward_weight_workspace_bytes() >
- * EQLINEAR_STATIC_SCRATCH_BYTES) returns EQL_ERR_SCRATCH before any HIP call.
+ * harnesses that forbid allocation).  Same operation and arguments (minus
+ * the workspace) as eqlinear_backward_weight; the workspace contents live in
+ * a file-scope static device array of EQLINEAR_STATIC_SCRATCH_BYTES per GPU
+ * instead, and the call performs no allocation of any kind.  Wherever
+ * eqlinear_backward_weight_workspace_bytes() <= EQLINEAR_STATIC_SCRATCH_BYTES
+ * it runs the same kernels and gives the same bits; for wide layers whose
+ * plan needs more (the transformed x and dy above) it plans the split-row
+ * kernels instead, whose partials are smaller (same result up to rounding).
+ * A problem whose partials still need more than the array returns
+ * EQL_ERR_SCRATCH before any HIP call.
  * Every call on one GPU uses that GPU's one array, and every partial a call
  * reads it first writes in the same call, so nothing carries over between
  * calls; but two calls whose executions overlap on one GPU (different
