@@ -170,6 +170,56 @@ def test_noalloc_argument_checks(lib):
     assert int(m.group(1)) << int(m.group(2)) == L.STATIC_SCRATCH_BYTES
 
 
+def _a256(v):
+    return (v + 255) // 256 * 256
+
+
+def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
+    """Wide 16-bit layers with T = 2 or 4 plan the large-tile weight gradient,
+    whose workspace holds the fp32 partials of its row splits plus the
+    row-contiguous transformed x and dy (T x C rounded up to 128 x N rounded
+    up to 64, 16-bit); narrower layers, fp32 and other T keep the split-row
+    plans.  Host-side queries, no device."""
+    monkeypatch.delenv("EQL_WGRAD_KIND", raising=False)
+    q = L.eqlinear_backward_weight_workspace_bytes
+    T, C, N = 4, 2048, 32768
+    # 16 x 16 channel tiles of 128 fill 256 CUs: one split
+    spec = T * C * N * 2
+    want = _a256(1 * T * C * C * 4) + _a256(C * 4) + 2 * _a256(spec)
+    assert q(N, T, C, C, L.EQL_F16) == want
+    assert q(N, T, C, C, L.EQL_BF16) == want
+    # 1030 -> 1100 channels at 5,000 rows: both pad to 1152, N to 5,056
+    Ci, Co, n = 1030, 1100, 5000
+    got = q(n, T, Ci, Co, L.EQL_F16)
+    assert got >= 2 * _a256(T * 1152 * 5056 * 2)
+    # below the thresholds (fp16 1024, bf16 512), fp32, T = 8: no spectra
+    for args in ((N, T, 512, 512, L.EQL_F16), (N, T, 256, 256, L.EQL_BF16), (N, T, C, C, L.EQL_F32),
+                 (N, 8, C, C, L.EQL_F16)):
+        assert q(*args) < args[0] * args[1] * (args[2] + args[3]) * 2, args
+    assert q(N, T, 512, 512, L.EQL_BF16) > N * T * 1024 * 2
+    # forced on a small layer
+    small = q(1000, 2, 64, 96, L.EQL_F16)
+    monkeypatch.setenv("EQL_WGRAD_KIND", "2")
+    assert q(1000, 2, 64, 96, L.EQL_F16) >= _a256(2 * 128 * 1024 * 2) * 2
+    assert q(1000, 2, 64, 96, L.EQL_F32) < 1000 * 2 * 160 * 4  # fp32: never
+    monkeypatch.delenv("EQL_WGRAD_KIND")
+    assert q(1000, 2, 64, 96, L.EQL_F16) == small
+
+
+def test_noalloc_plans_within_static_scratch(lib):
+    """The allocation-free entry point takes the split-row plan where the
+    large-tile workspace exceeds its scratch (so it does not refuse a wide
+    layer that the split-row kernels can handle): with no device it reaches
+    the device check (EQL_ERR_NO_DEVICE), not EQL_ERR_SCRATCH."""
+    T, C, N = 4, 1024, 4096
+    assert L.eqlinear_backward_weight_workspace_bytes(N, T, C, C, L.EQL_F16) > L.STATIC_SCRATCH_BYTES
+    GB = 1 << 30
+    st = L.eqlinear_backward_weight_noalloc(A, A + GB, A + 2 * GB, None, N, T, C, C, L.EQL_F16, None)
+    if _gpu_visible():
+        pytest.skip("a device is visible: the call would launch")
+    assert st == L.EQL_ERR_NO_DEVICE, L.eqlinear_status_string(st)
+
+
 def test_whole_backward_plan_and_workspace(lib):
     """eqlinear_backward fuses large row counts against a small tile (Swin
     stage 1) and not the EQ-ViT-B MLP (96 x 384 x 8 does not fit one
