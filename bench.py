@@ -669,7 +669,9 @@ def run_gconv(args):
     gradient back onto psi).  Forward = one layer call with the C_T weight and
     spectrum precomputed (a frozen weight), reading the patches straight from
     the features where the channel count allows, else gather + layer call;
-    training step = weight permutation, spectrum, forward, backward.  Mean and median of ``--tables-runs`` runs."""
+    training step = weight permutations (forward and adjoint), spectra,
+    forward, backward (input gradient as the adjoint convolution where Cout
+    allows).  Mean and median of ``--tables-runs`` runs."""
     import numpy as np
     import torch
     import torch.nn.functional as F
@@ -730,6 +732,7 @@ def run_gconv(args):
 
             def flash_train():
                 gconv._CACHE.clear()
+                gconv._CACHE_ADJ.clear()
                 y = gconv.GroupConv2dFunction.apply(fg, pg, bg)
                 y.backward(gy)
             rec["flash_train"] = _time_fn(flash_train, runs)

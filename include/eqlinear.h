@@ -67,7 +67,7 @@
 extern "C" {
 #endif
 
-#define EQLINEAR_ABI_VERSION 7
+#define EQLINEAR_ABI_VERSION 8
 #define EQLINEAR_MAX_T 16
 
 typedef enum { EQL_F32 = 0, EQL_F16 = 1, EQL_BF16 = 2 } eql_dtype_t;
@@ -244,6 +244,20 @@ int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int 
                                void* stream);
 int eqlinear_gconv_unpack_weight(const void* dw_ct, void* dpsi, int T, int Cin, int Cout, int k, int dtype,
                                  void* stream);
+
+/* The weight of the adjoint convolution: the input gradient of the group
+ * convolution is itself a group convolution of the output gradient,
+ *     df[n, c, s] = sum_(a,b) sum_l sum_o psi'[R^-s (a,b)][l][c][o] dy[n + (a,b), o, (s + l) mod T]
+ *     psi'[(a,b)][l][c][o] = psi[-R^-l (a,b)][-l mod T][o][c]
+ * (the adjoint of the forward map above, Sec. 5), so it runs as the forward
+ * of a layer with Cout inputs and Cin outputs and no bias.  Writes that
+ * layer's C_T weight w_adj [T, Cin, k*k*Cout] from psi [k,k,T,Cout,Cin] (a
+ * permutation); its spectrum (eqlinear_weight_spectrum with T, k*k*Cout,
+ * Cin) feeds eqlinear_gconv_forward(dy, ..., Cin = Cout, Cout = Cin) or the
+ * gather + eqlinear_forward pair, with no patch buffer of dy's gradient and
+ * no scatter.  Checks as for eqlinear_gconv_pack_weight. */
+int eqlinear_gconv_pack_weight_adjoint(const void* psi, void* w_adj, int T, int Cin, int Cout, int k, int dtype,
+                                       void* stream);
 
 /* The group convolution's forward pass without the patch buffer: y
  * [B,H,W,Cout,T] = eqlinear_forward of the gathered patches (T, k*k*Cin ->

@@ -50,6 +50,7 @@ SIGNATURES = {
     "eqlinear_gconv_gather": (_i, [_vp, _vp, _i64, _i, _i, _i, _i, _i, _i, _vp]),
     "eqlinear_gconv_scatter": (_i, [_vp, _vp, _i64, _i, _i, _i, _i, _i, _i, _vp]),
     "eqlinear_gconv_pack_weight": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
+    "eqlinear_gconv_pack_weight_adjoint": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "eqlinear_gconv_unpack_weight": (_i, [_vp, _vp, _i, _i, _i, _i, _i, _vp]),
     "eqlinear_gconv_forward": (_i, [_vp, _vp, _vp, _vp, _i64, _i, _i, _i, _i, _i, _i, _i, _vp]),
 }
@@ -162,6 +163,10 @@ def eqlinear_gconv_scatter(dxcol, df, B, H, W, T, Cin, k, dtype, stream) -> int:
 
 def eqlinear_gconv_pack_weight(psi, w_ct, T, Cin, Cout, k, dtype, stream) -> int:
     return lib().eqlinear_gconv_pack_weight(psi, w_ct, T, Cin, Cout, k, dtype, stream)
+
+
+def eqlinear_gconv_pack_weight_adjoint(psi, w_adj, T, Cin, Cout, k, dtype, stream) -> int:
+    return lib().eqlinear_gconv_pack_weight_adjoint(psi, w_adj, T, Cin, Cout, k, dtype, stream)
 
 
 def eqlinear_gconv_unpack_weight(dw_ct, dpsi, T, Cin, Cout, k, dtype, stream) -> int:

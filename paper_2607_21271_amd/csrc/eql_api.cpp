@@ -810,6 +810,9 @@ int gconv_launch_t(int op, const void* in, void* out, int64_t B, int H, int W, i
     if (op == 2)
       hipLaunchKernelGGL((eqk::eql_gconv_pack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
                          (const E*)in, (E*)out, T, Cin, Cout, k);
+    else if (op == 4)
+      hipLaunchKernelGGL((eqk::eql_gconv_pack_kernel<E, true>), dim3(gather_grid(total)), dim3(256), 0, s,
+                         (const E*)in, (E*)out, T, Cin, Cout, k);
     else
       hipLaunchKernelGGL((eqk::eql_gconv_unpack_kernel<E>), dim3(gather_grid(total)), dim3(256), 0, s,
                          (const E*)in, (E*)out, T, Cin, Cout, k);
@@ -826,7 +829,7 @@ int gconv_launch(int op, const void* in, void* out, int64_t B, int H, int W, int
 }
 
 // op 0 gather (in f, out X), 1 scatter (in dX, out df), 2 pack (in psi, out w),
-// 3 unpack (in dw, out dpsi)
+// 3 unpack (in dw, out dpsi), 4 adjoint pack (in psi, out w')
 int gconv_common(int op, const void* in, void* out, int64_t B, int H, int W, int T, int Cin, int Cout, int k,
                  int dtype, void* stream) {
   int st = gconv_shape(T, Cin, Cout, k, dtype);
@@ -919,6 +922,11 @@ int eqlinear_gconv_pack_weight(const void* psi, void* w_ct, int T, int Cin, int 
 int eqlinear_gconv_unpack_weight(const void* dw_ct, void* dpsi, int T, int Cin, int Cout, int k, int dtype,
                                  void* stream) {
   return gconv_common(3, dw_ct, dpsi, 0, 0, 0, T, Cin, Cout, k, dtype, stream);
+}
+
+int eqlinear_gconv_pack_weight_adjoint(const void* psi, void* w_adj, int T, int Cin, int Cout, int k, int dtype,
+                                       void* stream) {
+  return gconv_common(4, psi, w_adj, 0, 0, 0, T, Cin, Cout, k, dtype, stream);
 }
 
 }  // extern "C"

@@ -239,23 +239,28 @@ __global__ __launch_bounds__(256) void eql_gconv_scatter_kernel(const E* __restr
 }
 
 // w[m][o][c'] from psi
-template <typename E>
+template <typename E, bool ADJ = false>
 __global__ __launch_bounds__(256) void eql_gconv_pack_kernel(const E* __restrict__ psi, E* __restrict__ w,
                                                              int T, int Cin, int Cout, int k) {
-  const GconvDims d = gconv_dims(T, k, Cin);
-  const int64_t total = (int64_t)T * Cout * d.Cin2;
+  // ADJ: the weight of the adjoint convolution (the input gradient as a group
+  // convolution of the output gradient), psi'[d][l][c][o] = psi[-R^-l d][-l
+  // mod T][o][c], packed as a layer with k*k*Cout inputs and Cin outputs:
+  // w'[T, Cin, k*k*Cout].  Here Ci / Co name that layer's channel counts.
+  const int Ci = ADJ ? Cout : Cin, Co = ADJ ? Cin : Cout;
+  const GconvDims d = gconv_dims(T, k, Ci);
+  const int64_t total = (int64_t)T * Co * d.Cin2;
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  const int ob = d.n_orb * Cin * T;
+  const int ob = d.n_orb * Ci * T;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
     const int cc = (int)(i % d.Cin2);
     const int64_t r = i / d.Cin2;
-    const int o = (int)(r % Cout);
-    const int m = (int)(r / Cout);
+    const int o = (int)(r % Co);
+    const int m = (int)(r / Co);
     const int l = (T - m) % T;
     int a = 0, b = 0, c, sp;
     if (cc < ob) {
-      const int O = cc / (Cin * T);
-      const int rem = cc - O * Cin * T;
+      const int O = cc / (Ci * T);
+      const int rem = cc - O * Ci * T;
       c = rem / T;
       const int u = rem - c * T;
       gconv_base(d, O, a, b);
@@ -265,7 +270,13 @@ __global__ __launch_bounds__(256) void eql_gconv_pack_kernel(const E* __restrict
       c = cc - ob;
       sp = l;
     }
-    w[i] = psi[((((int64_t)(a + d.h) * k + (b + d.h)) * T + sp) * Cout + o) * Cin + c];
+    if constexpr (ADJ) {
+      // psi'[(a,b)][sp][o][c] = psi[-R^-sp (a,b)][-sp mod T][c][o]
+      gconv_rot(-sp, T, a, b);
+      w[i] = psi[((((int64_t)(d.h - a) * k + (d.h - b)) * T + (T - sp) % T) * Cout + c) * Cin + o];
+    } else {
+      w[i] = psi[((((int64_t)(a + d.h) * k + (b + d.h)) * T + sp) * Cout + o) * Cin + c];
+    }
   }
 }
 

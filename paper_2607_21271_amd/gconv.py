@@ -71,6 +71,22 @@ def pack_weight(psi: torch.Tensor, stream=None) -> torch.Tensor:
     return w
 
 
+def pack_weight_adjoint(psi: torch.Tensor, stream=None) -> torch.Tensor:
+    """w_adj [T, Cin, k*k*Cout] from psi [k, k, T, Cout, Cin]: the C_T weight of
+    the adjoint convolution (``eqlinear_gconv_pack_weight_adjoint``), which
+    maps the output gradient [B, H, W, Cout, T] to the input gradient."""
+    if psi.dim() != 5 or psi.shape[0] != psi.shape[1]:
+        raise ValueError("psi must be [k, k, T, Cout, Cin], got %s" % (tuple(psi.shape),))
+    k, _, T, Cout, Cin = psi.shape
+    dt = ops._dtype_code(psi)
+    psi = psi.contiguous()
+    ops._check_dev(psi)
+    w = torch.empty(T, Cin, k * k * Cout, dtype=psi.dtype, device=psi.device)
+    _lib.check(_lib.eqlinear_gconv_pack_weight_adjoint(ops._ptr(psi), ops._ptr(w), T, Cin, Cout, k, dt,
+                                                       ops._stream(stream)), "eqlinear_gconv_pack_weight_adjoint")
+    return w
+
+
 def unpack_weight_grad(dw_ct: torch.Tensor, k: int, stream=None) -> torch.Tensor:
     """dpsi [k, k, T, Cout, Cin] from the gradient of w_ct [T, Cout, k*k*Cin]."""
     T, Cout, C2 = dw_ct.shape
@@ -112,26 +128,42 @@ def implicit_ok(Cin: int) -> bool:
     return Cin % 4 == 0
 
 
-# C_T weights and spectrum per psi, reused while psi's storage and version
-# counter (bumped by in-place updates) and the stream are unchanged.
+# C_T weights and spectrum per psi (forward and adjoint), reused while psi's
+# storage and version counter (bumped by in-place updates) and the stream are
+# unchanged.
 _CACHE: dict = {}
+_CACHE_ADJ: dict = {}
 
 
-def cached_ct_weight(psi: torch.Tensor):
+def _cached(cache, psi: torch.Tensor, pack):
     stream = torch.cuda.current_stream(psi.device).cuda_stream
     key = (psi.data_ptr(), psi._version, tuple(psi.shape), psi.dtype, stream)
-    ent = _CACHE.get(id(psi))
+    ent = cache.get(id(psi))
     if ent is not None and ent[0]() is psi and ent[1] == key:
         return ent[2]
-    w_ct = pack_weight(psi)
+    w_ct = pack(psi)
     val = (w_ct, ops.weight_spectrum(w_ct))
     pid = id(psi)
-    _CACHE[pid] = (weakref.ref(psi, lambda _r, pid=pid: _CACHE.pop(pid, None)), key, val)
+    cache[pid] = (weakref.ref(psi, lambda _r, pid=pid: cache.pop(pid, None)), key, val)
     return val
 
 
+def cached_ct_weight(psi: torch.Tensor):
+    return _cached(_CACHE, psi, pack_weight)
+
+
+def cached_adjoint_weight(psi: torch.Tensor):
+    return _cached(_CACHE_ADJ, psi, pack_weight_adjoint)
+
+
 class GroupConv2dFunction(torch.autograd.Function):
-    """Autograd: f [B, H, W, Cin, T], psi [k, k, T, Cout, Cin], b [Cout] or None."""
+    """Autograd: f [B, H, W, Cin, T], psi [k, k, T, Cout, Cin], b [Cout] or None.
+
+    Input gradient: where Cout is a multiple of 4, the adjoint convolution of
+    the output gradient (``pack_weight_adjoint``) through the implicit-gather
+    forward, so neither the patch gradient nor its scatter is formed; else
+    the C_T input gradient of the patches and ``scatter``.  Weight gradient:
+    the C_T weight gradient of the gathered patches."""
 
     @staticmethod
     def forward(ctx, f, psi, b):
@@ -145,27 +177,33 @@ class GroupConv2dFunction(torch.autograd.Function):
             # patches read straight from f (no patch buffer); the weight
             # gradient, which needs them, takes the explicit gather below
             y = forward_implicit(f, wspec, b, T, Cout, k)
-            ctx.save_for_backward(f)
+            ctx.save_for_backward(f, psi)
             ctx.xcol_saved = False
         else:
             xcol = gather(f, T, k)
             y = ops.forward(xcol, wspec, b, T, k * k * Cin, Cout).view(B, H, W, Cout, T)
-            ctx.save_for_backward(xcol)
+            ctx.save_for_backward(xcol, psi)
             ctx.xcol_saved = True
         ctx.wspec, ctx.dims, ctx.has_bias = wspec, (B, H, W, T, Cin, Cout, k), b is not None
         return y
 
     @staticmethod
     def backward(ctx, gy):
-        (saved,) = ctx.saved_tensors
+        saved, psi = ctx.saved_tensors
         B, H, W, T, Cin, Cout, k = ctx.dims
         want_w = ctx.needs_input_grad[1] or (ctx.has_bias and ctx.needs_input_grad[2])
         xcol = saved if ctx.xcol_saved else (gather(saved, T, k) if want_w else None)
         C2 = k * k * Cin
-        gy2 = gy.contiguous().view(B * H * W, Cout, T)
+        gy = gy.contiguous()
+        gy2 = gy.view(B * H * W, Cout, T)
         gf = gpsi = gb = None
         dx2 = dw2 = None
-        if ctx.needs_input_grad[0] and want_w:
+        if ctx.needs_input_grad[0] and implicit_ok(Cout):
+            _, wspec_adj = cached_adjoint_weight(psi)
+            gf = forward_implicit(gy, wspec_adj, None, T, Cin, k)
+            if want_w:
+                dw2, gb = ops.backward_weight(xcol, gy2, T, C2, Cout, with_bias=ctx.has_bias)
+        elif ctx.needs_input_grad[0] and want_w:
             dx2, dw2, gb = ops.backward(xcol, gy2, ctx.wspec, T, C2, Cout, with_bias=ctx.has_bias)
         elif ctx.needs_input_grad[0]:
             dx2 = ops.backward_input(gy2, ctx.wspec, T, C2, Cout)

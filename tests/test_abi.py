@@ -34,7 +34,7 @@ def _gpu_visible():
 
 def test_exports_every_declared_symbol(lib):
     names = _header_functions()
-    assert len(names) == 19, names
+    assert len(names) == 20, names
     for n in names:
         assert hasattr(lib, n), n
         assert n in L.SIGNATURES, n
@@ -373,7 +373,7 @@ def test_gconv_argument_checks(lib):
     assert callf(11, 7) == L.EQL_ERR_INVALID_ARG
     if not _gpu_visible():
         assert callf(4, 0) in (L.EQL_OK, L.EQL_ERR_NO_DEVICE)
-    for f in (pk, up):
+    for f in (pk, up, L.eqlinear_gconv_pack_weight_adjoint):
         base = [A, A + 64 * MB, T, Cin, Cout, k, L.EQL_F16, None]
 
         def call(i, v, f=f):

@@ -12,7 +12,10 @@ oracle is pinned against facts that do not come from it:
   the lag read as a correlation;
 * T = 1 is a plain 2-d cross-correlation with zero padding
   (torch.nn.functional.conv2d in float64);
-* the gradients are the adjoints of the forward map.
+* the gradients are the adjoints of the forward map;
+* the input gradient is itself a group convolution of the output gradient,
+  with the weight psi'[d][l][c][o] = psi[-R^-l d][-l mod T][o][c] (the form
+  the GPU path uses for it).
 Planted mistakes in copies of the source are caught by these pins.
 """
 import os
@@ -96,6 +99,34 @@ def test_gradients_are_adjoints(go, T, k):
     assert abs(lhs - float(np.sum(f * df))) <= 1e-10 * max(1.0, abs(lhs))
     assert abs(lhs - float(np.sum(psi * dpsi))) <= 1e-10 * max(1.0, abs(lhs))
     np.testing.assert_allclose(db, dout.sum(axis=(0, 1, 2, 4)), rtol=0, atol=1e-11)
+
+
+def _adjoint_weight(psi, T):
+    """psi'[d][l][c][o] = psi[-R^-l d][-l mod T][o][c] for psi [k, k, T, Cout,
+    Cin] (offsets d = (a, b) at index (a + k//2, b + k//2); R(a, b) = (-b, a)
+    at T = 4, (-a, -b) at T = 2)."""
+    k = psi.shape[0]
+    h = k // 2
+    Cout, Cin = psi.shape[3], psi.shape[4]
+    out = np.zeros((k, k, T, Cin, Cout))
+    for a in range(-h, h + 1):
+        for b in range(-h, h + 1):
+            for l in range(T):
+                ra, rb = a, b
+                for _ in range((T - l) % T * (4 // T if T > 1 else 0)):   # R^-l = R^(T-l), quarter turns
+                    ra, rb = -rb, ra
+                out[a + h, b + h, l] = psi[-ra + h, -rb + h, (-l) % T].T
+    return out
+
+
+@pytest.mark.parametrize("T,k", [(4, 3), (4, 5), (2, 3), (2, 5), (1, 3), (4, 1)])
+def test_input_gradient_is_the_adjoint_convolution(go, T, k):
+    B, H, W, Cin, Cout = 2, 6, 5, 3, 4
+    psi = _rand(20 + k, k, k, T, Cout, Cin)
+    dout = _rand(21 + T, B, H, W, Cout, T)
+    df = go.backward_input(dout, psi)
+    via = go.forward(dout, _adjoint_weight(psi, T), None)
+    np.testing.assert_allclose(via, df, rtol=0, atol=1e-12 * max(1.0, float(np.abs(df).max())))
 
 
 def _pins_pass(lib_path):

@@ -172,3 +172,22 @@ def test_frozen_weight_group_conv(go, B, H, W, T, Cin, Cout, k, bias, dt):
     edf = rel_err(ft.grad.float().cpu().numpy(), go.backward_input(dout, psi))
     say("  y %.2e df %.2e" % (ey, edf))
     assert ey <= TOL[dt] and edf <= TOL[dt], (ey, edf)
+
+
+@pytest.mark.parametrize("T,k", [(4, 3), (4, 5), (2, 3), (1, 3), (4, 1), (2, 7)])
+def test_adjoint_weight_pack_is_the_permuted_pack(T, k):
+    """pack_weight_adjoint(psi) equals pack_weight of the adjoint weight
+    psi'[d][l][c][o] = psi[-R^-l d][-l mod T][o][c] built on the host (the
+    identity pinned against the oracle on the CPU), bit for bit: both are
+    permutations."""
+    from paper_2607_21271_amd import gconv
+    from test_gconv_oracle import _adjoint_weight
+    rs = np.random.RandomState(30 + 7 * T + k)
+    Cout, Cin = 5, 3
+    psi = rs.standard_normal((k, k, T, Cout, Cin)).astype(np.float32)
+    adj = _adjoint_weight(psi.astype(np.float64), T).astype(np.float32)
+    got = gconv.pack_weight_adjoint(torch.from_numpy(psi).cuda())
+    want = gconv.pack_weight(torch.from_numpy(np.ascontiguousarray(adj)).cuda())
+    torch.cuda.synchronize()
+    assert got.shape == (T, Cin, k * k * Cout)
+    assert torch.equal(got, want)
