@@ -38,7 +38,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default=None, help="layer name from synth.LAYERS")
+    ap.add_argument("--workload", default=None, help="layer name from synth.LAYERS or extra_layers()")
     ap.add_argument("--dtype", default=None, choices=["f32", "f16", "bf16"])
     ap.add_argument("--rotate", type=int, default=4, help="input sets used in turn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -324,6 +324,22 @@ KERNELS = {"wspec": "eqlinear_weight_spectrum (eql_wspec_kernel)",
            "bwd": "eqlinear_backward, single pass (eql_bwd_fused_kernel + eql_wgrad_reduce_kernel)"}
 
 
+def kernel_name(kind, l, dt):
+    """The kernels behind one pass, for the JSON line: the library's size rules
+    for its large-tile kernels (16-bit elements, T = 2 or 4; forward / input
+    gradient from 256 channels each way with the contraction channels a
+    multiple of 32, weight gradient from 1024 (fp16) / 512 (bf16))."""
+    w16 = dt != "f32" and l.T in (2, 4)
+    lo = min(l.Cin, l.Cout)
+    if kind == "fwd" and w16 and lo >= 256 and l.Cin % 32 == 0:
+        return "eqlinear_forward (eql_gemm_big_kernel, forward)"
+    if kind == "dx" and w16 and lo >= 256 and l.Cout % 32 == 0:
+        return "eqlinear_backward_input (eql_gemm_big_kernel, input gradient)"
+    if kind == "dw" and w16 and lo >= (512 if dt == "bf16" else 1024):
+        return "eqlinear_backward_weight (eql_spec_rows_kernel x 2 + eql_wgrad_big_kernel + eql_wgrad_reduce_kernel)"
+    return KERNELS[kind]
+
+
 def measure(layer, dt, args, digest, with_cpu):
     import torch
 
@@ -357,7 +373,7 @@ def measure(layer, dt, args, digest, with_cpu):
         peak, unit = rf.PEAK_MFMA_TFLOPS[dt], "TFLOP/s"
     traffic = stored_traffic(l.name, dt, dom, digest)
     roof = {"bound": bound, "achieved": round(achieved, 2), "peak": peak, "unit": unit,
-            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": KERNELS[dom],
+            "frac": round(achieved / peak, 4), "traffic": traffic, "kernel": kernel_name(dom, l, dt),
             "algorithmic_bytes_per_launch": nbytes[dom], "avg_launch_us": round(per[dom], 2)}
     roof_all = sum(rf.roofline_time_s(k, N, l.T, l.Cin, l.Cout, dt, l.bias) for k in step_passes)
     rec = {
@@ -768,6 +784,16 @@ def run_gconv(args):
 EXTRA_DTYPES = {"vit_b_mlp_up": ("bf16",), "swin_s1": ("bf16",)}
 
 
+def extra_layers():
+    """Workloads measured beside the survey's layers (not parity-test shapes:
+    the fp64 oracle could not check them whole): the paper's operator
+    benchmark at c = 1024 (T = 4, 32,768 rows, Sec. 4.1 Tables 1-2), the
+    MFMA-bound regime of the large-tile kernels."""
+    import synth
+    return {"table_T4_c1024": synth.Layer("table_T4_c1024", 4, 1024, 1024, 32768, True, 6000, ("f16", "bf16"),
+                                          "operator benchmark row, c = 1024 per group element")}
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -796,8 +822,10 @@ def main():
         run_gconv(args)
         return
     digest = source_digest()
+    layers = dict(synth.LAYERS)
+    layers.update(extra_layers())
     name = args.workload or synth.HEADLINE
-    layer = synth.LAYERS[name]
+    layer = layers[name]
     dt = args.dtype or layer.dtypes[0]
     rec = measure(layer, dt, args, digest, with_cpu=not args.no_cpu_baseline)
     if args.all or not (args.headline_only or args.workload):
@@ -806,7 +834,7 @@ def main():
         a2 = argparse.Namespace(**vars(args))
         a2.steps, a2.warmup = min(args.steps, 30), min(args.warmup, 5)
         others = {}
-        for n2, l2 in synth.LAYERS.items():
+        for n2, l2 in layers.items():
             for d2 in l2.dtypes + EXTRA_DTYPES.get(n2, ()):
                 if (n2, d2) == (name, dt):
                     continue
