@@ -88,9 +88,9 @@ def passes_of(name, fused):
         return ["bwd"]
     if "wgrad_reduce" in name:
         return ["dw", "bwd"] if fused else ["dw"]
-    if "wgrad" in name:
+    if "wgrad" in name or "spec_rows" in name:
         return ["dw"]
-    if "gemm_kernel" in name:
+    if "gemm_kernel" in name or "gemm_big_kernel" in name:
         targs = name.split("<")[1].split(">")[0].split(",")
         return ["dx"] if targs[2].strip() == "true" else ["fwd"]
     return []
@@ -101,12 +101,13 @@ def pass_of(name, fused=False):
     return "/".join(ps) if ps else None
 
 
-def summarize(d, workload, dt, digest, commands):
-    """Write the kernel-trace, traffic and pipe summaries of one workload."""
+def summarize(d, workload, dt, digest, commands, layer=None):
+    """Write the kernel-trace, traffic and pipe summaries of one workload
+    (a layer of synth.LAYERS, or the one given)."""
     sys.path.insert(0, ROOT)
     import synth
     from paper_2607_21271_amd import roofline as rf
-    L = synth.LAYERS[workload]
+    L = layer if layer is not None else synth.LAYERS[workload]
     from paper_2607_21271_amd import _lib
     fused = bool(_lib.eqlinear_backward_is_fused(L.N, L.T, L.Cin, L.Cout,
                                                  _lib.EQL_F16 if dt == "f16" else _lib.EQL_F32))
@@ -252,7 +253,7 @@ def main(argv):
     digest = bench.source_digest()
     commands = {k: c.replace("<out>", d.rstrip("/")) + " > %s/%s.log 2>&1" % (d.rstrip("/"), k)
                 for k, c in commands_for(workload, dt).items()}
-    summarize(d, workload, dt, digest, commands)
+    summarize(d, workload, dt, digest, commands, layer=bench.extra_layers().get(workload))
     return commands
 
 
