@@ -171,3 +171,39 @@ def test_big_wgrad_noalloc_falls_back_within_scratch():
     e_db = rel_err(db_na.float().cpu().numpy(), db_ws.float().cpu().numpy())
     say("  noalloc vs workspace", "%.2e %.2e" % (e_dw, e_db))
     assert e_dw <= TOL["f16"] and e_db <= TOL["f16"], (e_dw, e_db)
+
+
+def _random_shapes(n, seed):
+    rs = np.random.RandomState(seed)
+    out = []
+    for _ in range(n):
+        T = int(rs.choice([2, 4]))
+        Cin = int(32 * rs.randint(1, 14))          # the contraction of the forward
+        Cout = int(rs.randint(1, 301))             # anything (the input gradient takes
+        N = int(rs.randint(1, 700))                # the large tiles only at multiples of 32)
+        out.append((T, Cin, Cout, N, bool(rs.randint(0, 2))))
+    return out
+
+
+RANDOM = _random_shapes(12, 9800)
+
+
+@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", RANDOM, ids=["T%d-%dx%d-N%d" % c[:4] for c in RANDOM])
+def test_big_tile_random_shapes(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
+    """Seeded random shapes with both large-tile paths forced: y, dx, dw and
+    db against the oracle."""
+    say("big random", T, Cin, Cout, N, bias, dt)
+    monkeypatch.setenv("EQL_GEMM_BIG", "1")
+    monkeypatch.setenv("EQL_WGRAD_KIND", "2")
+    inp = synth.draw(T, Cin, Cout, N, bias, 9900 + T + Cin + Cout + N).rounded(dt)
+    g = run_gpu(inp, dt)
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy, with_bias=bias)
+    errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
+            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w)),
+            "dw": rel_err(g["dw"], ref_dw)}
+    if bias:
+        errs["db"] = rel_err(g["db"], ref_db)
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL[dt], (k, v)
