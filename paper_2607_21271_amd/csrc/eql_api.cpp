@@ -465,7 +465,7 @@ static int gemm_common(const void* in, const void* wspec, const void* bias, void
   if (N == 0) return EQL_OK;
   const eqk::WspecDims d = eqk::wspec_dims(T, Cin, Cout, dtype != EQL_F32);
   const size_t fwd_block = (size_t)T * d.CoF * d.CiF * e;  // forward-layout planes
-  if (eqk::gemm_big_choose(T, Ci, Co, dtype != EQL_F32)) {
+  if (eqk::gemm_big_choose(T, Ci, Co, dtype)) {
     eqk::BigArgs b{};
     b.in = in;
     b.bias = bias;

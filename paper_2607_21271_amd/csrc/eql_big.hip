@@ -65,9 +65,10 @@ hipError_t launch_wgrad_big(int dt, int T, const WgradArgs& a, const WgradPlan& 
 }
 
 hipError_t launch_gemm_big(int dt, int T, bool bwd, const BigArgs& a) {
-  if (!gemm_big_fits(T, a.Ci, a.Co, dt != kF32)) return hipErrorInvalidValue;
+  if (!gemm_big_fits(T, a.Ci, a.Co, dt)) return hipErrorInvalidValue;
   if (dt == kF16) return big_dt<kF16>(T, bwd, a);
   if (dt == kBF16) return big_dt<kBF16>(T, bwd, a);
+  if (dt == kF32) return big_dt<kF32>(T, bwd, a);
   return hipErrorInvalidValue;
 }
 

@@ -1,5 +1,5 @@
-// eql_gemm_big.h -- forward / input-gradient kernel for wide layers with
-// 16-bit elements (fp16, bf16): large output tiles for the MFMA-bound regime.
+// eql_gemm_big.h -- forward / input-gradient kernel for wide layers: large
+// output tiles for the MFMA-bound regime (fp16, bf16 and fp32).
 //
 // The same computation as eql_gemm_kernel (Alg. 1; Sec. 3.3-3.5: rDFT of the
 // activations in registers, per-bin products against the precomputed weight
@@ -10,10 +10,13 @@
 // quarter (4 x 4 MFMA tiles per plane, T * 64 accumulator registers, which
 // live in the accumulation registers at one wave per SIMD).  Per contraction
 // step of 32 input channels the workgroup stages the activation spectrum
-// (128 rows) and the weight spectrum (128 output channels) in LDS, double
-// buffered; each wave reads four row fragments and four channel fragments per
-// plane and issues 16 MFMAs per product.  LDS operand traffic per MFMA is a
-// quarter of the 16-row tiles of eql_gemm_kernel.
+// (128 rows; two LDS buffers) and the weight spectrum (128 output channels;
+// three LDS buffers, loaded two steps ahead straight from global memory);
+// each wave reads four row fragments and four channel fragments per plane
+// and issues 16 MFMAs per product.  LDS operand traffic per MFMA is a quarter
+// of the 16-row tiles of eql_gemm_kernel.  Each step's barrier is an explicit
+// wait plus s_barrier with compiler fences only, so loads of later steps stay
+// in flight across it.
 //
 // Workgroups are renumbered so that each XCD (blocks dealt round-robin over
 // the 8 of them) takes a contiguous run of tiles, and runs sweep groups of four
@@ -27,7 +30,7 @@ namespace eqk {
 constexpr int kBigThreads = 256;
 constexpr int kBigBM = 128;  // rows per workgroup tile
 constexpr int kBigBN = 128;  // output channels per workgroup tile
-constexpr int kBigBK = 32;   // contraction channels per step
+constexpr int kBigBK = 32;   // contraction channels per step (16-bit elements; 16 for fp32)
 constexpr int kBigRB = 64;   // bytes of one staged row per step (32 16-bit channels)
 constexpr int kBigGroup = 4; // row tiles per sweep group
 
@@ -50,20 +53,24 @@ __device__ __forceinline__ void big_tile(int bid, int n_rt, int n_ct, int& rt, i
 // in [N, Ci, T], weight spectrum planes [T][w_rows][w_pitch] (row = output
 // channel, w_pitch >= Ci padded with zeros), out [N, Co, T].  Requires
 // Ci % 32 == 0 and the per-tile row ranges below 2^31 bytes (host checks).
+// A step covers 64 bytes of each staged row: 32 channels of 16-bit elements
+// (v_mfma_f32_16x16x32_f16 / bf16), 16 of fp32 (four v_mfma_f32_16x16x4f32
+// per fragment pair, a quarter of the contraction each).
 // BWD: in = dy, the transposed spectrum, conjugate products, no bias.
 template <int T, int DT, bool BWD>
 __global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ wsp,
                          const void* __restrict__ bias, void* __restrict__ out, int64_t N, int Ci, int Co,
                          int w_rows, int w_pitch, int n_rt, int n_ct) {
-  static_assert(DT != kF32, "16-bit elements");
   static_assert(T == 2 || T == 4, "accumulators for T <= 4 planes");
   using Bn = Bins<T>;
   using FR = Frag<16>;
-  constexpr int EB = 2;
+  constexpr int EB = DT == kF32 ? 4 : 2;
+  constexpr int BK = kBigRB / EB;               // contraction channels per step
+  constexpr int KWM = 16 / EB;                  // contraction elements per fragment
   constexpr int HKW = 4;                        // channels of one staging unit
-  constexpr int UB = HKW * T * EB;              // raw bytes of a unit: 16 or 32
-  constexpr int UPR = kBigBK / HKW;             // units per row and step
+  constexpr int UB = HKW * T * EB;              // raw bytes of a unit: 16, 32 or 64
+  constexpr int UPR = BK / HKW;                 // units per row and step
   constexpr int XU = kBigBM * UPR / kBigThreads;  // units per thread
   constexpr int XPL = kBigBM * kBigRB;          // bytes of one activation plane
   constexpr int WPL = kBigBN * kBigRB;          // bytes of one weight plane
@@ -135,7 +142,7 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   // (past the last step the reads land in padding or past the resources, in
   // buffers that are never read again)
   auto load_x = [&](int s, int v) __attribute__((always_inline)) {
-    const int xs = s * kBigBK * T * EB;
+    const int xs = s * BK * T * EB;
 #pragma unroll
     for (int h = 0; h < UB / 16; ++h) {
       const u32x4 a = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff[v] + 16 * h, xs, 0));
@@ -144,7 +151,7 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   };
   auto load_w = [&](int s) __attribute__((always_inline)) {
 #if defined(__HIP_DEVICE_COMPILE__)
-    const int ws = s * kBigBK * EB;
+    const int ws = s * BK * EB;
     char* wl = wbase + (s % 3) * WB;
 #pragma unroll
     for (int v = 0; v < WDU; ++v)
@@ -175,21 +182,34 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   // buffer b
   auto publish = [&](int b, int v) __attribute__((always_inline)) {
     char* base = xbase + b * XB;
-    uint32_t W[T][HKW / 2];
-    if constexpr (DT == kF16) {
-      raw_to_packed_planes<T, HKW>(xr[v], W);
-    } else {
+    if constexpr (DT == kF32) {
       float P[T][HKW];
       raw_to_planes<T, DT, HKW>(xr[v], P);
 #pragma unroll
       for (int p = 0; p < T; ++p)
+        *reinterpret_cast<u32x4*>(base + p * XPL + xlds[v]) =
+            u32x4{__builtin_bit_cast(uint32_t, P[p][0]), __builtin_bit_cast(uint32_t, P[p][1]),
+                  __builtin_bit_cast(uint32_t, P[p][2]), __builtin_bit_cast(uint32_t, P[p][3])};
+    } else {
+      uint32_t W[T][HKW / 2];
+      if constexpr (DT == kF16) {
+        raw_to_packed_planes<T, HKW>(xr[v], W);
+      } else {
+        float P[T][HKW];
+        raw_to_planes<T, DT, HKW>(xr[v], P);
 #pragma unroll
-        for (int j = 0; j < HKW / 2; ++j) W[p][j] = pack2<DT>(P[p][2 * j], P[p][2 * j + 1]);
+        for (int p = 0; p < T; ++p)
+#pragma unroll
+          for (int j = 0; j < HKW / 2; ++j) W[p][j] = pack2<DT>(P[p][2 * j], P[p][2 * j + 1]);
+      }
+#pragma unroll
+      for (int p = 0; p < T; ++p) *reinterpret_cast<u32x2*>(base + p * XPL + xlds[v]) = u32x2{W[p][0], W[p][1]};
     }
-#pragma unroll
-    for (int p = 0; p < T; ++p) *reinterpret_cast<u32x2*>(base + p * XPL + xlds[v]) = u32x2{W[p][0], W[p][1]};
   };
-  static_assert(XU == 4, "one staging unit per row tile");
+  // staging units per thread: 4 (16-bit) or 2 (fp32); unit v is staged in
+  // row tile UI * v + UI - 1 of the phase that carries them
+  static_assert(XU == 4 || XU == 2, "staging units per thread");
+  constexpr int UI = 4 / XU;
 
   floatx4 acc[T][4][4];
 #pragma unroll
@@ -207,7 +227,7 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   //   forward:  Re += Xr Wr + (-Xi) Wi,  Im += Xr Wi + Xi Wr
   //   backward: Re += Dr Wr + Di Wi,     Im += Di Wr + (-Dr) Wi
   // each accumulator's second product coming eight MFMAs after its first.
-  const int nks = Ci / kBigBK;
+  const int nks = Ci / BK;
   auto step = [&](int s) __attribute__((always_inline)) {
     const char* xl = xbase + (s & 1) * XB;
     const char* wl = wbase + (s % 3) * WB;
@@ -235,10 +255,10 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
 #pragma unroll
         for (int p = 0; p < R; ++p)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) frag_mma<DT, 8>(acc[p][i][j], A[i & 1][p], B[p][j]);
-        if constexpr (Bn::K == 0) {
-          publish((s + 1) & 1, i);
-          load_x(s + 2, i);
+          for (int j = 0; j < 4; ++j) frag_mma<DT, KWM>(acc[p][i][j], A[i & 1][p], B[p][j]);
+        if constexpr (Bn::K == 0 && i % UI == UI - 1) {
+          publish((s + 1) & 1, i / UI);
+          load_x(s + 2, i / UI);
         }
         __builtin_amdgcn_sched_barrier(0);
       });
@@ -263,25 +283,25 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
         const FR xn = frag_neg<DT, 16>(BWD ? xre : xim);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          frag_mma<DT, 8>(acc[re][i][j], xre, Br[j]);
-          if constexpr (!BWD) frag_mma<DT, 8>(acc[im][i][j], xre, Bi[j]);
-          else frag_mma<DT, 8>(acc[im][i][j], xim, Br[j]);
+          frag_mma<DT, KWM>(acc[re][i][j], xre, Br[j]);
+          if constexpr (!BWD) frag_mma<DT, KWM>(acc[im][i][j], xre, Bi[j]);
+          else frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
         }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           if constexpr (!BWD) {
-            frag_mma<DT, 8>(acc[re][i][j], xn, Bi[j]);
-            frag_mma<DT, 8>(acc[im][i][j], xim, Br[j]);
+            frag_mma<DT, KWM>(acc[re][i][j], xn, Bi[j]);
+            frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
           } else {
-            frag_mma<DT, 8>(acc[re][i][j], xim, Bi[j]);
-            frag_mma<DT, 8>(acc[im][i][j], xn, Bi[j]);
+            frag_mma<DT, KWM>(acc[re][i][j], xim, Bi[j]);
+            frag_mma<DT, KWM>(acc[im][i][j], xn, Bi[j]);
           }
         }
         // one staging unit of the next step per row tile (first complex
         // bin), interleaved with these MFMAs by the scheduler
-        if constexpr (k == 1) {
-          publish((s + 1) & 1, i);
-          load_x(s + 2, i);
+        if constexpr (k == 1 && i % UI == UI - 1) {
+          publish((s + 1) & 1, i / UI);
+          load_x(s + 2, i / UI);
         }
         __builtin_amdgcn_sched_barrier(0);
       });

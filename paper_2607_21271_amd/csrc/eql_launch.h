@@ -312,9 +312,9 @@ struct Inst {
 hipError_t launch_wspec(int dt, int T, const void* w, void* wspec, int Cin, int Cout, hipStream_t s);
 hipError_t launch_gemm(int dt, int T, bool bwd, const GemmArgs& a);
 
-// Large-tile forward / input gradient (eql_gemm_big.h): 16-bit elements, T in
-// {2, 4}, contraction channels a multiple of 32, and every 128-row tile of the
-// input and output below 2^31 bytes.  Taken by default for wide layers (both
+// Large-tile forward / input gradient (eql_gemm_big.h): T in {2, 4},
+// contraction channels a multiple of 32, and every 128-row tile of the input
+// and output below 2^31 bytes.  Taken by default for wide layers (both
 // channel counts at least kBigMinC), where the spectral products bound the
 // pass; EQL_GEMM_BIG=0 never takes it, =1 whenever the shape allows (tests,
 // A/B timing).
@@ -330,12 +330,13 @@ struct BigArgs {
 };
 constexpr int kBigMinC = 256;
 int gemm_big_forced();  // -1 unset, 0, 1
-inline bool gemm_big_fits(int T, int Ci, int Co, bool w16) {
-  return w16 && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&
-         (int64_t)128 * Ci * T * 2 < ((int64_t)1 << 31) && (int64_t)128 * Co * T * 2 < ((int64_t)1 << 31);
+inline bool gemm_big_fits(int T, int Ci, int Co, int dt) {
+  const int64_t eb = dt == kF32 ? 4 : 2;
+  return (dt == kF32 || dt == kF16 || dt == kBF16) && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&
+         (int64_t)128 * Ci * T * eb < ((int64_t)1 << 31) && (int64_t)128 * Co * T * eb < ((int64_t)1 << 31);
 }
-inline bool gemm_big_choose(int T, int Ci, int Co, bool w16) {
-  if (!gemm_big_fits(T, Ci, Co, w16)) return false;
+inline bool gemm_big_choose(int T, int Ci, int Co, int dt) {
+  if (!gemm_big_fits(T, Ci, Co, dt)) return false;
   const int f = gemm_big_forced();
   if (f >= 0) return f == 1;
   return Ci >= kBigMinC && Co >= kBigMinC;

@@ -1,8 +1,8 @@
-"""GPU parity of the large-tile kernels (16-bit elements, T in {2, 4}) against
-the fp64 oracle, through the C ABI: the forward / input gradient
-(csrc/eql_gemm_big.h: 128 x 128 output tiles) and the weight gradient
-(csrc/eql_wgrad_big.h: row-contiguous spectra, 128 x 128 (c, o) tiles, row
-splits, the split-partial reduction).
+"""GPU parity of the large-tile kernels (T in {2, 4}) against the fp64 oracle,
+through the C ABI: the forward / input gradient (csrc/eql_gemm_big.h: 128 x 128
+output tiles; fp32, fp16 and bf16) and the weight gradient
+(csrc/eql_wgrad_big.h: 16-bit elements; row-contiguous spectra, 128 x 128
+(c, o) tiles, row splits, the split-partial reduction).
 
 The host takes this kernel for wide layers only; EQL_GEMM_BIG=1 forces it
 wherever the shape allows (contraction channels a multiple of 32), so small
@@ -10,7 +10,7 @@ shapes with ragged rows and ragged output-channel tiles cover its tails.  A
 pass whose contraction channels are not a multiple of 32 keeps the other
 kernel (the input gradient of the Cout = 200 case).  EQL_WGRAD_KIND=2 forces
 the weight-gradient path likewise.  Bar as for the layer:
-max|gpu - oracle| / max|oracle| <= 5e-3 (fp16), 4e-2 (bf16).
+max|gpu - oracle| / max|oracle| <= 1e-5 (fp32), 5e-3 (fp16), 4e-2 (bf16).
 """
 import numpy as np
 import pytest
@@ -34,7 +34,7 @@ CASES = [(4, 32, 128, 128, True), (4, 64, 200, 300, True), (4, 160, 96, 1000, Fa
          (4, 128, 384, 1, True), (4, 1024, 160, 259, True)]
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("T,Cin,Cout,N,bias", CASES, ids=["T%d-%dx%d-N%d" % c[:4] for c in CASES])
 def test_big_tile_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
     say("big tile", T, Cin, Cout, N, bias, dt)
@@ -48,7 +48,7 @@ def test_big_tile_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
         assert v <= TOL[dt], (k, v)
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_big_tile_same_as_default_kernel_off(orc, monkeypatch, dt):
     """The kernel switch changes no result beyond rounding: forced on and off
     agree with each other to the dtype's bar (the two kernels sum in
@@ -65,7 +65,7 @@ def test_big_tile_same_as_default_kernel_off(orc, monkeypatch, dt):
         assert e <= TOL[dt], (k, e)
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_big_tile_table_shape_sampled(orc, dt):
     """The operator-table shape the kernel is chosen for by default (T = 4,
     1024 -> 1024 channels per group element, 32,768 rows): rows spread over
@@ -188,7 +188,7 @@ def _random_shapes(n, seed):
 RANDOM = _random_shapes(12, 9800)
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("T,Cin,Cout,N,bias", RANDOM, ids=["T%d-%dx%d-N%d" % c[:4] for c in RANDOM])
 def test_big_tile_random_shapes(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
     """Seeded random shapes with both large-tile paths forced: y, dx, dw and
