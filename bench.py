@@ -457,7 +457,7 @@ def run_tables(args):
     from paper_2607_21271_amd import roofline as rf
     T, N = 4, 32768
     runs = args.tables_runs
-    for dt in ("f32", "f16", "bf16"):
+    for dt in ((args.dtype,) if args.dtype else ("f32", "f16", "bf16")):
         tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
         for c in [int(v) for v in args.tables_c.split(",")]:
             torch.cuda.empty_cache()

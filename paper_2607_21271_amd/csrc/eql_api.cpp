@@ -392,6 +392,10 @@ int gemm_big_forced() {
   const char* v = getenv("EQL_GEMM_BIG");
   return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
 }
+int gauss_forced() {
+  const char* v = getenv("EQL_GAUSS");
+  return (v != nullptr && (v[0] == '0' || v[0] == '1') && v[1] == 0) ? v[0] - '0' : -1;
+}
 // Valid after check_device() succeeded on the current device.
 int device_cu_count() {
   int dev = 0;

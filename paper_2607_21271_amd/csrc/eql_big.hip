@@ -10,14 +10,15 @@
 namespace eqk {
 namespace {
 
-template <int T, int DT, bool BWD>
+template <int T, int DT, bool BWD, bool GAUSS = false>
 hipError_t big_t(const BigArgs& a) {
-  auto k = eql_gemm_big_kernel<T, DT, BWD>;
-  const int lds = big_lds_bytes(T);
+  auto k = eql_gemm_big_kernel<T, DT, BWD, GAUSS>;
+  const int lds = big_lds_bytes(T, GAUSS);
   hipError_t e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
   const int64_t n_rt = (a.N + kBigBM - 1) / kBigBM;
-  const int n_ct = (a.Co + kBigBN - 1) / kBigBN;
+  const int bn = big_bn(GAUSS);
+  const int n_ct = (a.Co + bn - 1) / bn;
   if (n_rt * n_ct >= ((int64_t)1 << 31) || a.w_rows < a.Co || a.w_pitch < a.Ci) return hipErrorInvalidValue;
   hipLaunchKernelGGL(k, dim3((unsigned)(n_rt * n_ct)), dim3(kBigThreads), lds, a.stream, a.in, a.wsp, a.bias,
                      a.out, a.N, a.Ci, a.Co, a.w_rows, a.w_pitch, (int)n_rt, n_ct);
@@ -27,6 +28,10 @@ hipError_t big_t(const BigArgs& a) {
 template <int DT>
 hipError_t big_dt(int T, bool bwd, const BigArgs& a) {
   if (T == 2) return bwd ? big_t<2, DT, true>(a) : big_t<2, DT, false>(a);
+  if constexpr (DT == kF32) {
+    if (T == 4 && big_gauss(T, DT))
+      return bwd ? big_t<4, DT, true, true>(a) : big_t<4, DT, false, true>(a);
+  }
   if (T == 4) return bwd ? big_t<4, DT, true>(a) : big_t<4, DT, false>(a);
   return hipErrorInvalidValue;
 }

@@ -18,6 +18,17 @@
 // wait plus s_barrier with compiler fences only, so loads of later steps stay
 // in flight across it.
 //
+// GAUSS (fp32, T = 4): each complex bin in three products instead of four
+// (Eq. 5's product in the three-multiplication form), accumulated apart and
+// combined in the epilogue:
+//   A1 += (Xr + Xi) Wr,  A2 += Xr (Wi - Wr),  A3 += Xi (Wr + Wi)
+//   forward:  Re = A1 - A3,  Im = A1 + A2
+//   backward (D = dy spectrum): A2 += Di (Wi - Wr), A3 += Dr (Wr + Wi),
+//             Re = A1 + A2,  Im = A1 - A3
+// The operand sums are formed in registers from the staged planes.  The third
+// accumulator plane takes the channel tile to 96 (4 x 3 MFMA tiles per wave
+// and plane, 5 * 48 accumulators per lane).
+//
 // Workgroups are renumbered so that each XCD (blocks dealt round-robin over
 // the 8 of them) takes a contiguous run of tiles, and runs sweep groups of four
 // row tiles across all channel tiles, so the workgroups resident on one XCD
@@ -29,14 +40,16 @@ namespace eqk {
 
 constexpr int kBigThreads = 256;
 constexpr int kBigBM = 128;  // rows per workgroup tile
-constexpr int kBigBN = 128;  // output channels per workgroup tile
+constexpr int kBigBN = 128;  // output channels per workgroup tile (96 with GAUSS)
 constexpr int kBigBK = 32;   // contraction channels per step (16-bit elements; 16 for fp32)
 constexpr int kBigRB = 64;   // bytes of one staged row per step (32 16-bit channels)
 constexpr int kBigGroup = 4; // row tiles per sweep group
 
+constexpr int big_bn(bool gauss) { return gauss ? 96 : kBigBN; }
+
 // dynamic LDS of one workgroup: two buffers of T activation planes, three of
-// T weight planes (160 KB at T = 4)
-constexpr int big_lds_bytes(int T) { return T * (2 * kBigBM + 3 * kBigBN) * kBigRB; }
+// T weight planes (160 KB at T = 4; 136 KB with GAUSS)
+constexpr int big_lds_bytes(int T, bool gauss = false) { return T * (2 * kBigBM + 3 * big_bn(gauss)) * kBigRB; }
 
 // tile (rt, ct) of block bid out of n_rt * n_ct blocks
 __device__ __forceinline__ void big_tile(int bid, int n_rt, int n_ct, int& rt, int& ct) {
@@ -57,12 +70,16 @@ __device__ __forceinline__ void big_tile(int bid, int n_rt, int n_ct, int& rt, i
 // (v_mfma_f32_16x16x32_f16 / bf16), 16 of fp32 (four v_mfma_f32_16x16x4f32
 // per fragment pair, a quarter of the contraction each).
 // BWD: in = dy, the transposed spectrum, conjugate products, no bias.
-template <int T, int DT, bool BWD>
+template <int T, int DT, bool BWD, bool GAUSS = false>
 __global__ __launch_bounds__(kBigThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ wsp,
                          const void* __restrict__ bias, void* __restrict__ out, int64_t N, int Ci, int Co,
                          int w_rows, int w_pitch, int n_rt, int n_ct) {
   static_assert(T == 2 || T == 4, "accumulators for T <= 4 planes");
+  static_assert(!GAUSS || (T == 4 && DT == kF32), "three-product bins: fp32, T = 4");
+  constexpr int NJ = GAUSS ? 3 : 4;             // MFMA column tiles per wave
+  constexpr int BN = 32 * NJ;                   // output channels of the tile
+  constexpr int NA = T + (GAUSS ? 1 : 0);       // accumulator planes
   using Bn = Bins<T>;
   using FR = Frag<16>;
   constexpr int EB = DT == kF32 ? 4 : 2;
@@ -73,12 +90,12 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   constexpr int UPR = BK / HKW;                 // units per row and step
   constexpr int XU = kBigBM * UPR / kBigThreads;  // units per thread
   constexpr int XPL = kBigBM * kBigRB;          // bytes of one activation plane
-  constexpr int WPL = kBigBN * kBigRB;          // bytes of one weight plane
+  constexpr int WPL = BN * kBigRB;              // bytes of one weight plane
   constexpr int XB = T * XPL;                   // one activation buffer
   constexpr int WB = T * WPL;                   // one weight buffer
-  constexpr int WCH = T * kBigBN * (kBigRB / 16); // 16-byte weight chunks per step
+  constexpr int WCH = T * BN * (kBigRB / 16);   // 16-byte weight chunks per step
   static_assert((kBigBM * UPR) % kBigThreads == 0, "thread split");
-  static_assert(2 * XB + 3 * WB == big_lds_bytes(T), "LDS size");
+  static_assert(2 * XB + 3 * WB == big_lds_bytes(T, GAUSS), "LDS size");
 
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char* const xbase = smem;           // activation buffers
@@ -93,7 +110,7 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   big_tile(blockIdx.x, n_rt, n_ct, rt, ct);
   const int64_t r0 = (int64_t)rt * kBigBM;
   const int len = N - r0 < kBigBM ? (int)(N - r0) : kBigBM;
-  const int o0 = ct * kBigBN;
+  const int o0 = ct * BN;
   const int rowb_in = Ci * T * EB;
   const int rowb_out = Co * T * EB;
   // rows of the tile as buffer resources: loads past them read zero, stores
@@ -120,12 +137,12 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   // its slot
   constexpr int NWV = kBigThreads / 64;
   constexpr int WDU = WCH / (64 * NWV);  // wave-loads per wave and step
-  static_assert(WCH % (64 * NWV) == 0 && (kBigBN * kBigRB) % 1024 == 0, "weight wave-loads");
+  static_assert(WCH % (64 * NWV) == 0 && (BN * kBigRB) % 1024 == 0, "weight wave-loads");
   uint32_t woff[WDU];
 #pragma unroll
   for (int v = 0; v < WDU; ++v) {
     const int slot = (v * NWV + wave) * 64 + lane;  // 16-byte slot of the weight planes
-    const int p = slot / (kBigBN * 4), rem = slot - p * (kBigBN * 4);
+    const int p = slot / (BN * 4), rem = slot - p * (BN * 4);
     const int row = rem / 4, cs = rem % 4;
     const int ch = cs ^ ((row >> 1) & 3);           // source chunk swizzled to slot cs
     woff[v] = (uint32_t)(((int64_t)p * w_rows + o0 + row) * w_pitch * EB + ch * 16);
@@ -211,13 +228,28 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   static_assert(XU == 4 || XU == 2, "staging units per thread");
   constexpr int UI = 4 / XU;
 
-  floatx4 acc[T][4][4];
+  floatx4 acc[NA][4][NJ];
 #pragma unroll
-  for (int p = 0; p < T; ++p)
+  for (int p = 0; p < NA; ++p)
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) acc[p][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int j = 0; j < NJ; ++j) acc[p][i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // fp32 fragment sums (GAUSS operands)
+  auto fsum = [](const FR& a, const FR& b) __attribute__((always_inline)) {
+    FR r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      r.w[q] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a.w[q]) + __builtin_bit_cast(float, b.w[q]));
+    return r;
+  };
+  auto fdiff = [](const FR& a, const FR& b) __attribute__((always_inline)) {
+    FR r;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      r.w[q] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(float, a.w[q]) - __builtin_bit_cast(float, b.w[q]));
+    return r;
+  };
 
   // Products of step s from activation buffer s & 1 and weight buffer s % 3,
   // in two phases: the real bins, then each complex bin.  A phase keeps its
@@ -231,16 +263,16 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
   auto step = [&](int s) __attribute__((always_inline)) {
     const char* xl = xbase + (s & 1) * XB;
     const char* wl = wbase + (s % 3) * WB;
-    auto colf = [&](int p, FR (&Bp)[4]) __attribute__((always_inline)) {
+    auto colf = [&](int p, FR (&Bp)[NJ]) __attribute__((always_inline)) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) Bp[j] = lds_frag<16, kBigRB>(wl + p * WPL, wc * 64 + j * 16 + li, g);
+      for (int j = 0; j < NJ; ++j) Bp[j] = lds_frag<16, kBigRB>(wl + p * WPL, wc * 16 * NJ + j * 16 + li, g);
     };
     auto rowf = [&](int p, int i) __attribute__((always_inline)) {
       return lds_frag<16, kBigRB>(xl + p * XPL, wr * 64 + i * 16 + li, g);
     };
     {
       constexpr int R = Bn::R;
-      FR B[R][4];
+      FR B[R][NJ];
       FR A[2][R];
 #pragma unroll
       for (int p = 0; p < R; ++p) colf(p, B[p]);
@@ -255,7 +287,7 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
 #pragma unroll
         for (int p = 0; p < R; ++p)
 #pragma unroll
-          for (int j = 0; j < 4; ++j) frag_mma<DT, KWM>(acc[p][i][j], A[i & 1][p], B[p][j]);
+          for (int j = 0; j < NJ; ++j) frag_mma<DT, KWM>(acc[p][i][j], A[i & 1][p], B[p][j]);
         if constexpr (Bn::K == 0 && i % UI == UI - 1) {
           publish((s + 1) & 1, i / UI);
           load_x(s + 2, i / UI);
@@ -263,13 +295,18 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
         __builtin_amdgcn_sched_barrier(0);
       });
     }
-    static_for<Bn::K>([&](auto ki) {
-      constexpr int k = decltype(ki)::value + 1;
-      constexpr int re = Bn::re(k), im = Bn::im(k);
-      FR Br[4], Bi[4];
+    if constexpr (GAUSS) {
+      static_assert(Bn::K == 1, "one complex bin");
+      constexpr int re = Bn::re(1), im = Bn::im(1);
+      FR Br[NJ], Bd[NJ], Bu[NJ];
       FR Ar[2], Ai[2];
       colf(re, Br);
-      colf(im, Bi);
+      colf(im, Bd);
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        Bu[j] = fsum(Br[j], Bd[j]);   // Wr + Wi
+        Bd[j] = fdiff(Bd[j], Br[j]);  // Wi - Wr
+      }
       Ar[0] = rowf(re, 0);
       Ai[0] = rowf(im, 0);
       static_for<4>([&](auto ii) {
@@ -280,32 +317,64 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
         }
         const FR& xre = Ar[i & 1];
         const FR& xim = Ai[i & 1];
-        const FR xn = frag_neg<DT, 16>(BWD ? xre : xim);
+        const FR xs = fsum(xre, xim);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          frag_mma<DT, KWM>(acc[re][i][j], xre, Br[j]);
-          if constexpr (!BWD) frag_mma<DT, KWM>(acc[im][i][j], xre, Bi[j]);
-          else frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
-        }
+        for (int j = 0; j < NJ; ++j) frag_mma<DT, KWM>(acc[re][i][j], xs, Br[j]);
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          if constexpr (!BWD) {
-            frag_mma<DT, KWM>(acc[re][i][j], xn, Bi[j]);
-            frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
-          } else {
-            frag_mma<DT, KWM>(acc[re][i][j], xim, Bi[j]);
-            frag_mma<DT, KWM>(acc[im][i][j], xn, Bi[j]);
-          }
-        }
-        // one staging unit of the next step per row tile (first complex
-        // bin), interleaved with these MFMAs by the scheduler
-        if constexpr (k == 1 && i % UI == UI - 1) {
+        for (int j = 0; j < NJ; ++j) frag_mma<DT, KWM>(acc[im][i][j], BWD ? xim : xre, Bd[j]);
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) frag_mma<DT, KWM>(acc[T][i][j], BWD ? xre : xim, Bu[j]);
+        if constexpr (i % UI == UI - 1) {
           publish((s + 1) & 1, i / UI);
           load_x(s + 2, i / UI);
         }
         __builtin_amdgcn_sched_barrier(0);
       });
-    });
+    } else {
+      static_for<Bn::K>([&](auto ki) {
+        constexpr int k = decltype(ki)::value + 1;
+        constexpr int re = Bn::re(k), im = Bn::im(k);
+        FR Br[NJ], Bi[NJ];
+        FR Ar[2], Ai[2];
+        colf(re, Br);
+        colf(im, Bi);
+        Ar[0] = rowf(re, 0);
+        Ai[0] = rowf(im, 0);
+        static_for<4>([&](auto ii) {
+          constexpr int i = decltype(ii)::value;
+          if constexpr (i + 1 < 4) {
+            Ar[(i + 1) & 1] = rowf(re, i + 1);
+            Ai[(i + 1) & 1] = rowf(im, i + 1);
+          }
+          const FR& xre = Ar[i & 1];
+          const FR& xim = Ai[i & 1];
+          const FR xn = frag_neg<DT, 16>(BWD ? xre : xim);
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            frag_mma<DT, KWM>(acc[re][i][j], xre, Br[j]);
+            if constexpr (!BWD) frag_mma<DT, KWM>(acc[im][i][j], xre, Bi[j]);
+            else frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
+          }
+#pragma unroll
+          for (int j = 0; j < NJ; ++j) {
+            if constexpr (!BWD) {
+              frag_mma<DT, KWM>(acc[re][i][j], xn, Bi[j]);
+              frag_mma<DT, KWM>(acc[im][i][j], xim, Br[j]);
+            } else {
+              frag_mma<DT, KWM>(acc[re][i][j], xim, Bi[j]);
+              frag_mma<DT, KWM>(acc[im][i][j], xn, Bi[j]);
+            }
+          }
+          // one staging unit of the next step per row tile (first complex
+          // bin), interleaved with these MFMAs by the scheduler
+          if constexpr (k == 1 && i % UI == UI - 1) {
+            publish((s + 1) & 1, i / UI);
+            load_x(s + 2, i / UI);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        });
+      });
+    }
   };
 
   // prologue: activations of step 0 staged, weights of steps 0 and 1 and raw
@@ -325,14 +394,14 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
     step(s);
   }
 
-  // D = X W^T: lane (g, li) of tile (i, j) holds channel o0 + wc*64 + j*16 + li
+  // D = X W^T: lane (g, li) of tile (i, j) holds channel o0 + wc*16*NJ + j*16 + li
   // of rows wr*64 + i*16 + 4g .. +3; the 16 lanes of a lane group store 16
   // consecutive channels of one row (16*T contiguous elements)
   using E = typename Elem<DT>::T;
   const E* __restrict__ bp = reinterpret_cast<const E*>(bias);
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int o = o0 + wc * 64 + j * 16 + li;
+  for (int j = 0; j < NJ; ++j) {
+    const int o = o0 + wc * 16 * NJ + j * 16 + li;
     float bv = 0.0f;
     if constexpr (!BWD) {
       if (bp != nullptr) bv = (float)bp[o < Co ? o : Co - 1];
@@ -345,6 +414,12 @@ void eql_gemm_big_kernel(const void* __restrict__ in, const void* __restrict__ w
         float Pl[T], ul[T];
 #pragma unroll
         for (int p = 0; p < T; ++p) Pl[p] = acc[p][i][j][r];
+        if constexpr (GAUSS) {
+          constexpr int re = Bn::re(1), im = Bn::im(1);
+          const float a1 = acc[re][i][j][r], a2 = acc[im][i][j][r], a3 = acc[T][i][j][r];
+          Pl[re] = BWD ? a1 + a2 : a1 - a3;
+          Pl[im] = BWD ? a1 - a3 : a1 + a2;
+        }
         // a constant added to every group position is T times it added to bin 0
         Pl[0] = __builtin_fmaf((float)T, bv, Pl[0]);
         irdft<T>(Pl, ul);

@@ -330,6 +330,11 @@ struct BigArgs {
 };
 constexpr int kBigMinC = 256;
 int gemm_big_forced();  // -1 unset, 0, 1
+// Three-product complex bins in the large-tile kernel (fp32, T = 4; 96-channel
+// tiles).  EQL_GAUSS=0 takes the four-product form instead, =1 or unset the
+// three-product one.
+int gauss_forced();  // -1 unset, 0, 1
+inline bool big_gauss(int T, int dt) { return T == 4 && dt == kF32 && gauss_forced() != 0; }
 inline bool gemm_big_fits(int T, int Ci, int Co, int dt) {
   const int64_t eb = dt == kF32 ? 4 : 2;
   return (dt == kF32 || dt == kF16 || dt == kBF16) && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&

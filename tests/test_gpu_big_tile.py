@@ -1,8 +1,9 @@
 """GPU parity of the large-tile kernels (T in {2, 4}) against the fp64 oracle,
 through the C ABI: the forward / input gradient (csrc/eql_gemm_big.h: 128 x 128
-output tiles; fp32, fp16 and bf16) and the weight gradient
-(csrc/eql_wgrad_big.h: 16-bit elements; row-contiguous spectra, 128 x 128
-(c, o) tiles, row splits, the split-partial reduction).
+output tiles; fp32, fp16 and bf16; fp32 at T = 4 takes three-product complex
+bins and 96-channel tiles by default, EQL_GAUSS=0 the four products) and the
+weight gradient (csrc/eql_wgrad_big.h: 16-bit elements; row-contiguous
+spectra, 128 x 128 (c, o) tiles, row splits, the split-partial reduction).
 
 The host takes this kernel for wide layers only; EQL_GEMM_BIG=1 forces it
 wherever the shape allows (contraction channels a multiple of 32), so small
@@ -46,6 +47,28 @@ def test_big_tile_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
     say("  ", {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
         assert v <= TOL[dt], (k, v)
+
+
+GAUSS_CASES = [(4, 32, 96, 128, True), (4, 64, 200, 300, True), (4, 160, 97, 1000, False),
+               (4, 128, 384, 1, True), (4, 512, 512, 515, True), (4, 96, 1, 77, True)]
+
+
+@pytest.mark.parametrize("gauss", ["0", "1"])
+@pytest.mark.parametrize("T,Cin,Cout,N,bias", GAUSS_CASES, ids=["T%d-%dx%d-N%d" % c[:4] for c in GAUSS_CASES])
+def test_big_tile_fp32_three_and_four_products(orc, monkeypatch, T, Cin, Cout, N, bias, gauss):
+    """fp32 at T = 4 in both forms of the complex-bin product: the three
+    multiplications (96-channel tiles, ragged channel tiles included) and the
+    four, forward and input gradient against the oracle."""
+    say("big tile fp32 gauss", gauss, T, Cin, Cout, N, bias)
+    monkeypatch.setenv("EQL_GEMM_BIG", "1")
+    monkeypatch.setenv("EQL_GAUSS", gauss)
+    inp = synth.draw(T, Cin, Cout, N, bias, 9200 + Cin + Cout + N).rounded("f32")
+    g = run_gpu(inp, "f32", want=("y", "dx"))
+    errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
+            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w))}
+    say("  ", {k: "%.2e" % v for k, v in errs.items()})
+    for k, v in errs.items():
+        assert v <= TOL["f32"], (k, v)
 
 
 @pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
