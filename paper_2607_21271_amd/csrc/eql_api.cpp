@@ -125,28 +125,44 @@ static int wgrad_forced_kind() {
 
 // Large-tile plan: 128 x 128 channel tiles, and row splits (whole steps of 32
 // rows, at least 8 per split) until about one workgroup per CU.
-static WgradPlan wgrad_plan_big(int64_t N, int T, int Cin, int Cout) {
+static WgradPlan wgrad_plan_big(int64_t N, int T, int Cin, int Cout, int dt) {
   WgradPlan p{};
+  const size_t eb = dt == kF32 ? 4 : 2;
   p.kind = 2;
-  p.BC = p.BO = 128;
-  p.KR = 32;
+  p.BC = 128;
+  p.BO = wgrad_big_o_tile(T, Cin, Cout, dt);
+  p.KR = dt == kF32 ? 16 : 32;  // rows per step: 64 bytes of each channel row
   p.n_ct = (Cin + 127) / 128;
-  p.n_ot = (Cout + 127) / 128;
+  p.n_ot = (Cout + p.BO - 1) / p.BO;
   p.Cin_pad = p.n_ct * 128;
-  p.Cout_pad = p.n_ot * 128;
+  p.Cout_pad = p.n_ot * p.BO;
   p.N_pad = (N + 63) / 64 * 64;  // whole blocks of the spectrum pre-pass
   const int64_t steps = p.N_pad / 32;
   const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
-  int64_t S = tiles >= 256 ? 1 : (256 + tiles - 1) / tiles;
+  // Row splits: each workgroup runs its rows to the end, so the pass lasts
+  // about ceil(S * tiles / 256) rounds of workgroups of steps / S steps each.
+  // Take the S with the fewest such steps (the smaller S on ties), from 1 to
+  // max(8, what first fills the 256 CUs), with at least 8 steps per split.
   const int64_t max_s = steps / 8 > 1 ? steps / 8 : 1;
-  if (S > max_s) S = max_s;
+  int64_t s_hi = (256 + tiles - 1) / tiles;
+  if (s_hi < 8) s_hi = 8;
+  if (s_hi > max_s) s_hi = max_s;
+  int64_t S = 1;
+  double best = 0.0;
+  for (int64_t s = 1; s <= s_hi; ++s) {
+    const double cost = (double)((s * tiles + 255) / 256) / (double)s;
+    if (s == 1 || cost < best * 0.999) {
+      best = cost;
+      S = s;
+    }
+  }
   const int64_t per = (steps + S - 1) / S;
   p.rows_per_split = per * 32;
   p.S = (int)((steps + per - 1) / per);
   p.part_bytes = (size_t)p.S * T * p.Cout_pad * p.Cin_pad * sizeof(float);
   p.dbpart_bytes = (size_t)p.S * p.Cout_pad * sizeof(float);
-  p.xs_bytes = (size_t)T * p.Cin_pad * p.N_pad * 2;
-  p.ds_bytes = (size_t)T * p.Cout_pad * p.N_pad * 2;
+  p.xs_bytes = (size_t)T * p.Cin_pad * p.N_pad * eb;
+  p.ds_bytes = (size_t)T * p.Cout_pad * p.N_pad * eb;
   return p;
 }
 
@@ -167,9 +183,9 @@ static WgradPlan wgrad_plan_staged(int64_t N, int T, int Cin, int Cout, bool w16
 WgradPlan wgrad_plan(int64_t N, int T, int Cin, int Cout, int dt, size_t max_ws) {
   const bool w16 = dt != kF32;  // 16-bit elements: same shapes for fp16 and bf16
   int forced = wgrad_forced_kind();
-  if (wgrad_big_fits(N, T, Cin, Cout, w16) &&
+  if (wgrad_big_fits(N, T, Cin, Cout, dt) &&
       (forced == 2 || (forced < 0 && Cin >= wgrad_big_min_c(dt) && Cout >= wgrad_big_min_c(dt)))) {
-    const WgradPlan p = wgrad_plan_big(N, T, Cin, Cout);
+    const WgradPlan p = wgrad_plan_big(N, T, Cin, Cout, dt);
     if (wgrad_workspace(p) <= max_ws) return p;
   }
   if (forced == 2) forced = -1;

@@ -36,10 +36,12 @@ hipError_t big_dt(int T, bool bwd, const BigArgs& a) {
   return hipErrorInvalidValue;
 }
 
-template <int T, int DT>
+template <int T, int DT, bool GAUSS = false>
 hipError_t wgrad_big_t(const WgradArgs& a, const WgradPlan& p) {
-  if (p.kind != 2 || p.BC != kWbBC || p.BO != kWbBC || p.KR != kWbKR || p.rows_per_split % kWbKR != 0 ||
-      p.Cin_pad % kWbBC != 0 || p.Cout_pad % kWbBC != 0 || p.N_pad % 64 != 0 || !a.xs || !a.ds)
+  const int bo = wgrad_big_bo(GAUSS);
+  const int kr = kWbRB / (DT == kF32 ? 4 : 2);
+  if (p.kind != 2 || p.BC != kWbBC || p.BO != bo || p.KR != kr || p.rows_per_split % kWbKR != 0 ||
+      p.Cin_pad % kWbBC != 0 || p.Cout_pad % bo != 0 || p.N_pad % 64 != 0 || !a.xs || !a.ds)
     return hipErrorInvalidValue;
   const int64_t n_rb = p.N_pad / 64;  // pre-pass blocks: 64 rows x 32 channels
   const int ncb_x = p.Cin_pad / 32, ncb_d = p.Cout_pad / 32;
@@ -49,8 +51,8 @@ hipError_t wgrad_big_t(const WgradArgs& a, const WgradPlan& p) {
                      a.ds, a.N, a.Cout, p.Cout_pad, p.N_pad, ncb_d);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  auto k = eql_wgrad_big_kernel<T, DT>;
-  const int lds = wgrad_big_lds_bytes(T);
+  auto k = eql_wgrad_big_kernel<T, DT, GAUSS>;
+  const int lds = wgrad_big_lds_bytes(T, GAUSS);
   e = hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return e;
   const int64_t G = (int64_t)p.S * p.n_ct * p.n_ot;
@@ -63,9 +65,14 @@ hipError_t wgrad_big_t(const WgradArgs& a, const WgradPlan& p) {
 }  // namespace
 
 hipError_t launch_wgrad_big(int dt, int T, const WgradArgs& a, const WgradPlan& p) {
-  if (!wgrad_big_fits(a.N, T, a.Cin, a.Cout, dt != kF32)) return hipErrorInvalidValue;
+  if (!wgrad_big_fits(a.N, T, a.Cin, a.Cout, dt)) return hipErrorInvalidValue;
   if (dt == kF16) return T == 2 ? wgrad_big_t<2, kF16>(a, p) : T == 4 ? wgrad_big_t<4, kF16>(a, p) : hipErrorInvalidValue;
   if (dt == kBF16) return T == 2 ? wgrad_big_t<2, kBF16>(a, p) : T == 4 ? wgrad_big_t<4, kBF16>(a, p) : hipErrorInvalidValue;
+  if (dt == kF32) {
+    if (T == 2) return wgrad_big_t<2, kF32>(a, p);
+    // the plan's o-tile names the form (96: three products)
+    if (T == 4) return p.BO == wgrad_big_bo(true) ? wgrad_big_t<4, kF32, true>(a, p) : wgrad_big_t<4, kF32>(a, p);
+  }
   return hipErrorInvalidValue;
 }
 

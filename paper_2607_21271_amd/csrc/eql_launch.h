@@ -173,19 +173,39 @@ inline size_t align256z(size_t v) { return (v + 255) / 256 * 256; }
 inline size_t wgrad_workspace(const WgradPlan& p) {
   return align256z(p.part_bytes) + align256z(p.dbpart_bytes) + align256z(p.xs_bytes) + align256z(p.ds_bytes);
 }
-// Large-tile weight gradient (kind 2): 16-bit elements, T in {2, 4}, and the
-// spectra of x and dy addressable with 31-bit offsets.  Taken by default from
+// Three-product complex bins in the large-tile kernels (fp32, T = 4;
+// 96-channel output tiles).  EQL_GAUSS=0 takes the four-product form
+// everywhere, =1 the three-product one everywhere; unset, the forward and
+// input gradient take three products and the weight gradient as below.
+int gauss_forced();  // -1 unset, 0, 1
+inline bool big_gauss(int T, int dt) { return T == 4 && dt == kF32 && gauss_forced() != 0; }
+
+// Large-tile weight gradient (kind 2): T in {2, 4}, and the spectra of x and
+// dy addressable with 31-bit offsets.  Taken by default from
 // wgrad_big_min_c channels each way, where it measured faster than the
 // register-direct kernel (T = 4, 32,768 rows: fp16 from 1024, 0.85 vs 0.97 ms,
-// level at 512; bf16 from 512, 0.27 vs 0.34 ms); EQL_WGRAD_KIND=2 forces it
-// where it fits.
+// level at 512; bf16 from 512, 0.27 vs 0.34 ms; fp32 from 1024, 3.40 vs 3.72
+// ms, level at 512);
+// EQL_WGRAD_KIND=2 forces it where it fits.  fp32 at T = 4 takes the
+// three-product complex bin with 96-channel o-tiles (big_gauss) where the
+// 128-channel tiles alone fill the 256 CUs (c = 2048: 12.04 against 12.71
+// ms); with fewer tiles the row splits balance the four-product tiles as
+// well and the three products measured 2% slower (c = 1024: 3.48 vs 3.41 ms).
 inline int wgrad_big_min_c(int dt) { return dt == kBF16 ? 512 : 1024; }
-inline bool wgrad_big_fits(int64_t N, int T, int Cin, int Cout, bool w16) {
+inline int wgrad_big_o_tile(int T, int Cin, int Cout, int dt) {
+  if (T != 4 || dt != kF32) return 128;
+  const int f = gauss_forced();
+  const int64_t tiles128 = (int64_t)((Cin + 127) / 128) * ((Cout + 127) / 128);
+  return f == 1 || (f < 0 && tiles128 >= 256) ? 96 : 128;
+}
+inline bool wgrad_big_fits(int64_t N, int T, int Cin, int Cout, int dt) {
+  const int64_t eb = dt == kF32 ? 4 : 2;
   const int64_t np = (N + 63) / 64 * 64;
-  const int64_t ci = (Cin + 127) / 128 * 128, co = (Cout + 127) / 128 * 128;
+  const int64_t bo = wgrad_big_o_tile(T, Cin, Cout, dt);
+  const int64_t ci = (Cin + 127) / 128 * 128, co = (Cout + bo - 1) / bo * bo;
   const int64_t lim = (int64_t)1 << 31;
-  return w16 && (T == 2 || T == 4) && N > 0 && (int64_t)T * ci * np * 2 < lim && (int64_t)T * co * np * 2 < lim &&
-         (int64_t)64 * (Cin > Cout ? Cin : Cout) * T * 2 < lim;
+  return (dt == kF32 || dt == kF16 || dt == kBF16) && (T == 2 || T == 4) && N > 0 && (int64_t)T * ci * np * eb < lim &&
+         (int64_t)T * co * np * eb < lim && (int64_t)64 * (Cin > Cout ? Cin : Cout) * T * eb < lim;
 }
 
 // Shape of the partial reduction: NTHR threads per workgroup, runs of IPW
@@ -330,11 +350,7 @@ struct BigArgs {
 };
 constexpr int kBigMinC = 256;
 int gemm_big_forced();  // -1 unset, 0, 1
-// Three-product complex bins in the large-tile kernel (fp32, T = 4; 96-channel
-// tiles).  EQL_GAUSS=0 takes the four-product form instead, =1 or unset the
-// three-product one.
-int gauss_forced();  // -1 unset, 0, 1
-inline bool big_gauss(int T, int dt) { return T == 4 && dt == kF32 && gauss_forced() != 0; }
+
 inline bool gemm_big_fits(int T, int Ci, int Co, int dt) {
   const int64_t eb = dt == kF32 ? 4 : 2;
   return (dt == kF32 || dt == kF16 || dt == kBF16) && (T == 2 || T == 4) && Ci % 32 == 0 && Co >= 1 &&

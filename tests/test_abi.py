@@ -175,12 +175,17 @@ def _a256(v):
 
 
 def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
-    """Wide 16-bit layers with T = 2 or 4 plan the large-tile weight gradient,
-    whose workspace holds the fp32 partials of its row splits plus the
-    row-contiguous transformed x and dy (T x C rounded up to 128 x N rounded
-    up to 64, 16-bit); narrower layers, fp32 and other T keep the split-row
-    plans.  Host-side queries, no device."""
+    """Wide layers with T = 2 or 4 plan the large-tile weight gradient, whose
+    workspace holds the fp32 partials of its row splits plus the
+    row-contiguous transformed x and dy (T x C rounded up to the channel
+    tiles x N rounded up to 64, in the layer's element size); narrower
+    layers and other T keep the split-row plans.  fp32 at T = 4 takes
+    96-channel o-tiles (three-product bins) where 128-channel tiles alone
+    number 256 or more, unless EQL_GAUSS=0; the row splits are as many as
+    fill whole rounds of 256 workgroups best.  Host-side queries, no
+    device."""
     monkeypatch.delenv("EQL_WGRAD_KIND", raising=False)
+    monkeypatch.delenv("EQL_GAUSS", raising=False)
     q = L.eqlinear_backward_weight_workspace_bytes
     T, C, N = 4, 2048, 32768
     # 16 x 16 channel tiles of 128 fill 256 CUs: one split
@@ -188,20 +193,33 @@ def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
     want = _a256(1 * T * C * C * 4) + _a256(C * 4) + 2 * _a256(spec)
     assert q(N, T, C, C, L.EQL_F16) == want
     assert q(N, T, C, C, L.EQL_BF16) == want
+    # fp32: 16 c-tiles x 22 o-tiles of 96 (2112 padded) = 352 tiles; 8 splits
+    # make 2816 workgroups, 11 whole rounds
+    co = 2112
+    want32 = _a256(8 * T * co * C * 4) + _a256(8 * co * 4) + _a256(T * C * N * 4) + _a256(T * co * N * 4)
+    assert q(N, T, C, C, L.EQL_F32) == want32
+    monkeypatch.setenv("EQL_GAUSS", "0")
+    assert q(N, T, C, C, L.EQL_F32) == _a256(T * C * C * 4) + _a256(C * 4) + 2 * _a256(T * C * N * 4)
+    monkeypatch.delenv("EQL_GAUSS")
     # 1030 -> 1100 channels at 5,000 rows: both pad to 1152, N to 5,056
     Ci, Co, n = 1030, 1100, 5000
     got = q(n, T, Ci, Co, L.EQL_F16)
     assert got >= 2 * _a256(T * 1152 * 5056 * 2)
-    # below the thresholds (fp16 1024, bf16 512), fp32, T = 8: no spectra
-    for args in ((N, T, 512, 512, L.EQL_F16), (N, T, 256, 256, L.EQL_BF16), (N, T, C, C, L.EQL_F32),
+    # 9 x 9 tiles: 3 splits (243 workgroups, one round), not 4 (324, two)
+    assert got == _a256(3 * T * 1152 * 1152 * 4) + _a256(3 * 1152 * 4) + 2 * _a256(T * 1152 * 5056 * 2)
+    # below the thresholds (fp16 and fp32 1024, bf16 512), T = 8: no spectra
+    for args in ((N, T, 512, 512, L.EQL_F16), (N, T, 256, 256, L.EQL_BF16), (N, T, 512, 512, L.EQL_F32),
                  (N, 8, C, C, L.EQL_F16)):
         assert q(*args) < args[0] * args[1] * (args[2] + args[3]) * 2, args
     assert q(N, T, 512, 512, L.EQL_BF16) > N * T * 1024 * 2
+    # fp32 at 1024: 8 x 8 tiles of 128 (four products), 4 splits
+    assert q(N, T, 1024, 1024, L.EQL_F32) == (_a256(4 * T * 1024 * 1024 * 4) + _a256(4 * 1024 * 4)
+                                              + 2 * _a256(T * 1024 * N * 4))
     # forced on a small layer
     small = q(1000, 2, 64, 96, L.EQL_F16)
     monkeypatch.setenv("EQL_WGRAD_KIND", "2")
     assert q(1000, 2, 64, 96, L.EQL_F16) >= _a256(2 * 128 * 1024 * 2) * 2
-    assert q(1000, 2, 64, 96, L.EQL_F32) < 1000 * 2 * 160 * 4  # fp32: never
+    assert q(1000, 2, 64, 96, L.EQL_F32) >= _a256(2 * 128 * 1024 * 4) * 2
     monkeypatch.delenv("EQL_WGRAD_KIND")
     assert q(1000, 2, 64, 96, L.EQL_F16) == small
 

@@ -1,9 +1,9 @@
 """GPU parity of the large-tile kernels (T in {2, 4}) against the fp64 oracle,
 through the C ABI: the forward / input gradient (csrc/eql_gemm_big.h: 128 x 128
-output tiles; fp32, fp16 and bf16; fp32 at T = 4 takes three-product complex
-bins and 96-channel tiles by default, EQL_GAUSS=0 the four products) and the
-weight gradient (csrc/eql_wgrad_big.h: 16-bit elements; row-contiguous
-spectra, 128 x 128 (c, o) tiles, row splits, the split-partial reduction).
+output tiles) and the weight gradient (csrc/eql_wgrad_big.h: row-contiguous
+spectra, 128 x 128 (c, o) tiles, row splits, the split-partial reduction), in
+fp32, fp16 and bf16; fp32 at T = 4 takes three-product complex bins and
+96-channel output tiles by default, EQL_GAUSS=0 the four products.
 
 The host takes this kernel for wide layers only; EQL_GEMM_BIG=1 forces it
 wherever the shape allows (contraction channels a multiple of 32), so small
@@ -58,14 +58,20 @@ GAUSS_CASES = [(4, 32, 96, 128, True), (4, 64, 200, 300, True), (4, 160, 97, 100
 def test_big_tile_fp32_three_and_four_products(orc, monkeypatch, T, Cin, Cout, N, bias, gauss):
     """fp32 at T = 4 in both forms of the complex-bin product: the three
     multiplications (96-channel tiles, ragged channel tiles included) and the
-    four, forward and input gradient against the oracle."""
+    four; forward, input gradient and the large-tile weight gradient against
+    the oracle."""
     say("big tile fp32 gauss", gauss, T, Cin, Cout, N, bias)
     monkeypatch.setenv("EQL_GEMM_BIG", "1")
+    monkeypatch.setenv("EQL_WGRAD_KIND", "2")
     monkeypatch.setenv("EQL_GAUSS", gauss)
     inp = synth.draw(T, Cin, Cout, N, bias, 9200 + Cin + Cout + N).rounded("f32")
-    g = run_gpu(inp, "f32", want=("y", "dx"))
+    g = run_gpu(inp, "f32")
+    ref_dw, ref_db = orc.backward_weight(inp.x, inp.dy, with_bias=bias)
     errs = {"y": rel_err(g["y"], orc.forward(inp.x, inp.w, inp.b)),
-            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w))}
+            "dx": rel_err(g["dx"], orc.backward_input(inp.dy, inp.w)),
+            "dw": rel_err(g["dw"], ref_dw)}
+    if bias:
+        errs["db"] = rel_err(g["db"], ref_db)
     say("  ", {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
         assert v <= TOL["f32"], (k, v)
@@ -122,7 +128,7 @@ WG_CASES = [(4, 32, 128, 128, True), (4, 64, 200, 300, True), (2, 96, 256, 777, 
             (4, 384, 256, 2100, True), (4, 16, 40, 33, True)]
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 @pytest.mark.parametrize("T,Cin,Cout,N,bias", WG_CASES, ids=["T%d-%dx%d-N%d" % c[:4] for c in WG_CASES])
 def test_big_wgrad_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
     """dw and db of the forced large-tile weight gradient (single split for
