@@ -131,9 +131,9 @@ int eqlinear_backward_input(const void* dy, const void* wspec, void* dx, int64_t
                             int Cin, int Cout, int dtype, void* stream);
 
 /* Bytes of device workspace that eqlinear_backward_weight needs for this
- * problem (fp32 partial sums of the row splits; for wide layers with 16-bit
- * elements and T = 2 or 4 also the transformed x and dy, stored with the
- * rows contiguous, about 2 (Cin + Cout) T N bytes); 0 if the arguments are
+ * problem (fp32 partial sums of the row splits; for wide layers with T = 2 or
+ * 4 also the transformed x and dy, stored with the rows contiguous, about
+ * (Cin + Cout) T N times the element size in bytes); 0 if the arguments are
  * invalid or N = 0. */
 size_t eqlinear_backward_weight_workspace_bytes(int64_t N, int T, int Cin, int Cout, int dtype);
 
