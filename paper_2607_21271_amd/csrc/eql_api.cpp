@@ -136,7 +136,7 @@ static WgradPlan wgrad_plan_big(int64_t N, int T, int Cin, int Cout, int dt) {
   p.n_ot = (Cout + p.BO - 1) / p.BO;
   p.Cin_pad = p.n_ct * 128;
   p.Cout_pad = p.n_ot * p.BO;
-  p.N_pad = (N + 63) / 64 * 64;  // whole blocks of the spectrum pre-pass
+  p.N_pad = wgrad_big_npad(N);  // whole blocks of the spectrum pre-pass
   const int64_t steps = p.N_pad / 32;
   const int64_t tiles = (int64_t)p.n_ct * p.n_ot;
   // Row splits: each workgroup runs its rows to the end, so the pass lasts

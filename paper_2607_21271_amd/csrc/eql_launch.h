@@ -198,9 +198,18 @@ inline int wgrad_big_o_tile(int T, int Cin, int Cout, int dt) {
   const int64_t tiles128 = (int64_t)((Cin + 127) / 128) * ((Cout + 127) / 128);
   return f == 1 || (f < 0 && tiles128 >= 256) ? 96 : 128;
 }
+// Rows of the row-contiguous spectra: N in whole 64-row blocks of the
+// pre-pass, plus one more block where that count is even, so that the channel
+// rows' pitch is an odd multiple of 128 bytes (16-bit) or twice one (fp32)
+// and the rows one step reads spread over the L2 sets instead of sharing a
+// few (a pitch of 32,768 rows is 64 KB).  The extra rows are zero.
+inline int64_t wgrad_big_npad(int64_t N) {
+  const int64_t blocks = (N + 63) / 64;
+  return (blocks % 2 == 0 ? blocks + 1 : blocks) * 64;
+}
 inline bool wgrad_big_fits(int64_t N, int T, int Cin, int Cout, int dt) {
   const int64_t eb = dt == kF32 ? 4 : 2;
-  const int64_t np = (N + 63) / 64 * 64;
+  const int64_t np = wgrad_big_npad(N);
   const int64_t bo = wgrad_big_o_tile(T, Cin, Cout, dt);
   const int64_t ci = (Cin + 127) / 128 * 128, co = (Cout + bo - 1) / bo * bo;
   const int64_t lim = (int64_t)1 << 31;

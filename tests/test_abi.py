@@ -188,20 +188,21 @@ def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
     monkeypatch.delenv("EQL_GAUSS", raising=False)
     q = L.eqlinear_backward_weight_workspace_bytes
     T, C, N = 4, 2048, 32768
+    NP = N + 64  # 512 blocks of 64 rows, even: one more, for an odd row pitch in 128-byte lines
     # 16 x 16 channel tiles of 128 fill 256 CUs: one split
-    spec = T * C * N * 2
+    spec = T * C * NP * 2
     want = _a256(1 * T * C * C * 4) + _a256(C * 4) + 2 * _a256(spec)
     assert q(N, T, C, C, L.EQL_F16) == want
     assert q(N, T, C, C, L.EQL_BF16) == want
     # fp32: 16 c-tiles x 22 o-tiles of 96 (2112 padded) = 352 tiles; 8 splits
     # make 2816 workgroups, 11 whole rounds
     co = 2112
-    want32 = _a256(8 * T * co * C * 4) + _a256(8 * co * 4) + _a256(T * C * N * 4) + _a256(T * co * N * 4)
+    want32 = _a256(8 * T * co * C * 4) + _a256(8 * co * 4) + _a256(T * C * NP * 4) + _a256(T * co * NP * 4)
     assert q(N, T, C, C, L.EQL_F32) == want32
     monkeypatch.setenv("EQL_GAUSS", "0")
-    assert q(N, T, C, C, L.EQL_F32) == _a256(T * C * C * 4) + _a256(C * 4) + 2 * _a256(T * C * N * 4)
+    assert q(N, T, C, C, L.EQL_F32) == _a256(T * C * C * 4) + _a256(C * 4) + 2 * _a256(T * C * NP * 4)
     monkeypatch.delenv("EQL_GAUSS")
-    # 1030 -> 1100 channels at 5,000 rows: both pad to 1152, N to 5,056
+    # 1030 -> 1100 channels at 5,000 rows: both pad to 1152, N to 5,056 (79 blocks)
     Ci, Co, n = 1030, 1100, 5000
     got = q(n, T, Ci, Co, L.EQL_F16)
     assert got >= 2 * _a256(T * 1152 * 5056 * 2)
@@ -214,7 +215,7 @@ def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
     assert q(N, T, 512, 512, L.EQL_BF16) > N * T * 1024 * 2
     # fp32 at 1024: 8 x 8 tiles of 128 (four products), 4 splits
     assert q(N, T, 1024, 1024, L.EQL_F32) == (_a256(4 * T * 1024 * 1024 * 4) + _a256(4 * 1024 * 4)
-                                              + 2 * _a256(T * 1024 * N * 4))
+                                              + 2 * _a256(T * 1024 * NP * 4))
     # forced on a small layer
     small = q(1000, 2, 64, 96, L.EQL_F16)
     monkeypatch.setenv("EQL_WGRAD_KIND", "2")
