@@ -328,14 +328,14 @@ def kernel_name(kind, l, dt):
     """The kernels behind one pass, for the JSON line: the library's size rules
     for its large-tile kernels (T = 2 or 4; forward / input gradient from 256
     channels each way with the contraction channels a multiple of 32, weight
-    gradient from 1024 (fp16, fp32) / 512 (bf16) channels each way)."""
+    gradient from 768 (fp16, fp32) / 512 (bf16) channels each way)."""
     big = l.T in (2, 4)
     lo = min(l.Cin, l.Cout)
     if kind == "fwd" and big and lo >= 256 and l.Cin % 32 == 0:
         return "eqlinear_forward (eql_gemm_big_kernel, forward)"
     if kind == "dx" and big and lo >= 256 and l.Cout % 32 == 0:
         return "eqlinear_backward_input (eql_gemm_big_kernel, input gradient)"
-    if kind == "dw" and big and lo >= (512 if dt == "bf16" else 1024):
+    if kind == "dw" and big and lo >= (512 if dt == "bf16" else 768):
         return "eqlinear_backward_weight (eql_spec_rows_kernel x 2 + eql_wgrad_big_kernel + eql_wgrad_reduce_kernel)"
     return KERNELS[kind]
 

@@ -183,15 +183,16 @@ inline bool big_gauss(int T, int dt) { return T == 4 && dt == kF32 && gauss_forc
 // Large-tile weight gradient (kind 2): T in {2, 4}, and the spectra of x and
 // dy addressable with 31-bit offsets.  Taken by default from
 // wgrad_big_min_c channels each way, where it measured faster than the
-// register-direct kernel (T = 4, 32,768 rows: fp16 from 1024, 0.85 vs 0.97 ms,
-// level at 512; bf16 from 512, 0.27 vs 0.34 ms; fp32 from 1024, 3.40 vs 3.72
-// ms, level at 512);
+// register-direct kernel (T = 4, 32,768 rows, weight and bias gradient, µs
+// large-tile / register-direct: fp16 463 / 864 at c = 768, 261 / 221 at 512;
+// fp32 2059 / 3592 at 768, 988 / 888 at 512; bf16 261 / 320 at 512, 109 / 88
+// at 256);
 // EQL_WGRAD_KIND=2 forces it where it fits.  fp32 at T = 4 takes the
 // three-product complex bin with 96-channel o-tiles (big_gauss) where the
 // 128-channel tiles alone fill the 256 CUs (c = 2048: 12.04 against 12.71
 // ms); with fewer tiles the row splits balance the four-product tiles as
 // well and the three products measured 2% slower (c = 1024: 3.48 vs 3.41 ms).
-inline int wgrad_big_min_c(int dt) { return dt == kBF16 ? 512 : 1024; }
+inline int wgrad_big_min_c(int dt) { return dt == kBF16 ? 512 : 768; }
 inline int wgrad_big_o_tile(int T, int Cin, int Cout, int dt) {
   if (T != 4 || dt != kF32) return 128;
   const int f = gauss_forced();

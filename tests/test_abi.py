@@ -208,7 +208,7 @@ def test_large_tile_weight_gradient_plan_and_workspace(lib, monkeypatch):
     assert got >= 2 * _a256(T * 1152 * 5056 * 2)
     # 9 x 9 tiles: 3 splits (243 workgroups, one round), not 4 (324, two)
     assert got == _a256(3 * T * 1152 * 1152 * 4) + _a256(3 * 1152 * 4) + 2 * _a256(T * 1152 * 5056 * 2)
-    # below the thresholds (fp16 and fp32 1024, bf16 512), T = 8: no spectra
+    # below the thresholds (fp16 and fp32 768, bf16 512), T = 8: no spectra
     for args in ((N, T, 512, 512, L.EQL_F16), (N, T, 256, 256, L.EQL_BF16), (N, T, 512, 512, L.EQL_F32),
                  (N, 8, C, C, L.EQL_F16)):
         assert q(*args) < args[0] * args[1] * (args[2] + args[3]) * 2, args
