@@ -146,7 +146,7 @@ def test_big_wgrad_matches_oracle(orc, monkeypatch, T, Cin, Cout, N, bias, dt):
         assert v <= TOL[dt], (k, v)
 
 
-@pytest.mark.parametrize("dt", ["f16", "bf16"])
+@pytest.mark.parametrize("dt", ["f32", "f16", "bf16"])
 def test_big_whole_backward_default_plan(orc, dt):
     """A layer wide enough for both large-tile kernels by default (1024 ->
     1024 at T = 4; 520 rows keep the fp64 oracle fast): the whole backward
@@ -167,6 +167,37 @@ def test_big_whole_backward_default_plan(orc, dt):
     say("  whole backward", dt, {k: "%.2e" % v for k, v in errs.items()})
     for k, v in errs.items():
         assert v <= TOL[dt], (k, v)
+
+
+def test_big_fp32_default_plan_at_2048_sampled(orc):
+    """fp32 at T = 4, 2048 -> 2048 channels, 2,000 rows: the default plan
+    takes the three-product forward and input gradient (96-channel tiles)
+    and the three-product weight gradient (16 x 22 tiles of 128 x 96 in 8 row
+    splits, 2,816 workgroups).  Sampled rows of y and dx and sampled dw
+    entries against the oracle (db of this kernel: the smaller forced cases)."""
+    from paper_2607_21271_amd import ops
+    T, C, N = 4, 2048, 2000
+    rs = np.random.RandomState(9700)
+    w = (rs.standard_normal((T, C, C)) / np.sqrt(T * C)).astype(np.float32)
+    b = (0.1 * rs.standard_normal(C)).astype(np.float32)
+    x = rs.standard_normal((N, C, T)).astype(np.float32)
+    dy = rs.standard_normal((N, C, T)).astype(np.float32)
+    xt, wt, bt, dyt = to_dev(x, "f32"), to_dev(w, "f32"), to_dev(b, "f32"), to_dev(dy, "f32")
+    wspec = ops.weight_spectrum(wt)
+    y = ops.forward(xt, wspec, bt, T, C, C)
+    dx, dw, _ = ops.backward(xt, dyt, wspec, T, C, C, with_bias=True)
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([[0, 127, 128, N - 1], rs.randint(0, N, 12)]))
+    wd, bd = w.astype(np.float64), b.astype(np.float64)
+    ey = rel_err(y.cpu().numpy()[rows], orc.forward(x[rows].astype(np.float64), wd, bd))
+    edx = rel_err(dx.cpu().numpy()[rows], orc.backward_input(dy[rows].astype(np.float64), wd))
+    jj, oo, cc = rs.randint(0, T, 64), rs.randint(0, C, 64), rs.randint(0, C, 64)
+    ref = orc.backward_weight_entries(x, dy, jj, oo, cc)
+    got = dw.cpu().numpy()[jj, oo, cc]
+    edw = float(np.max(np.abs(got - ref)) / np.max(np.abs(ref)))
+    say("  fp32 2048 default", "y %.2e dx %.2e dw %.2e" % (ey, edx, edw))
+    for k, v in (("y", ey), ("dx", edx), ("dw", edw)):
+        assert v <= TOL["f32"], (k, v)
 
 
 def test_big_wgrad_noalloc_falls_back_within_scratch():
